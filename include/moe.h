@@ -1,0 +1,184 @@
+/*
+ * moe.h -- C ABI of one GPU's share of a Mixture-of-Experts layer on MI355X
+ * (gfx950): router, dispatch plan, routed + shared SwiGLU experts, combine,
+ * and the backward pass.
+ *
+ * The layer is the one of "Mixture-of-Kittens: MoE Megakernel for NVL72s",
+ * §2.1 (equation of MoE(x, s)):
+ *
+ *     Y[t] = f_shared(x_t) + sum_{e in S_t} w[t,e] * f_e(x_t),
+ *     f_e(x) = (silu(x W_gate[e]) * (x W_up[e])) W_down[e],
+ *
+ * with S_t the k largest router logits Z[t,:] = x_t W_r + bias and w the
+ * softmax of Z[t,:] renormalised over S_t.  Weights use row-vector
+ * orientation: W_gate[e] is [d, f], the transpose of the paper's
+ * column-vector matrix in R^{I x D}.
+ *
+ * Conventions shared by every entry point
+ * ----------------------------------------
+ * - Every tensor pointer is a DEVICE pointer to row-major, densely packed
+ *   memory owned by the caller.  The library allocates nothing, keeps no
+ *   global state, never synchronises the stream and never copies device
+ *   data to the host, so every call can be captured in a HIP graph.
+ * - bf16 tensors hold raw bf16 bit patterns (moe_bf16).  All conversions to
+ *   bf16 round to nearest even.
+ * - Every pointer must be 16-byte aligned.
+ * - Arguments are validated on the host before anything is launched; on a
+ *   validation error nothing is launched and outputs are untouched.
+ * - Outputs are overwritten, never accumulated into.
+ * - Work is enqueued on `stream` (a hipStream_t; NULL = null stream).  A
+ *   return of MOE_OK means the launches were accepted; kernel faults surface
+ *   through the HIP runtime at the caller's next synchronisation.
+ * - Results are bitwise deterministic: no floating-point atomics, every
+ *   reduction runs in a fixed order (§3.4 "Determinism").
+ * - Route ids are token-major: route j = t*k + slot, and a token's slots
+ *   list its selected experts in ascending expert id.
+ *
+ * Limits (MOE_EUNSUPPORTED outside them): d % 256 == 0, f % 256 == 0,
+ * f_shared % 256 == 0, 1 <= k <= 16, k <= E <= 256, T*k < 2^31.
+ */
+#ifndef MOE_H
+#define MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t moe_bf16;   /* bf16 bit pattern */
+typedef void *moe_stream;    /* a hipStream_t */
+
+/* Layer shape.  T tokens of width d, E local routed experts, top-k routing,
+ * routed intermediate size f, shared-expert intermediate size f_shared
+ * (0 = no shared expert). */
+typedef struct {
+    int64_t T, d, E, k, f, f_shared;
+} moe_shape;
+
+typedef enum {
+    MOE_OK = 0,
+    MOE_EINVAL = 1,        /* null/misaligned pointer, bad dimension, k > E */
+    MOE_EUNSUPPORTED = 2,  /* valid but outside the limits above */
+    MOE_ENOSPACE = 3,      /* workspace smaller than moe_workspace_bytes() */
+    MOE_EHIP = 4           /* a HIP launch was rejected */
+} moe_status;
+
+/* Expert weights (all bf16, caller-owned, read-only). */
+typedef struct {
+    const moe_bf16 *W_gate;  /* [E, d, f] */
+    const moe_bf16 *W_up;    /* [E, d, f] */
+    const moe_bf16 *W_down;  /* [E, f, d] */
+    const moe_bf16 *Wg_s;    /* [d, f_shared], NULL iff f_shared == 0 */
+    const moe_bf16 *Wu_s;    /* [d, f_shared], NULL iff f_shared == 0 */
+    const moe_bf16 *Wd_s;    /* [f_shared, d], NULL iff f_shared == 0 */
+} moe_weights;
+
+/* Dispatch plan (§3.1, Algorithm 1 with one source rank).  Written by
+ * moe_plan, read by moe_dispatch / moe_forward / moe_backward. */
+typedef struct {
+    int32_t *counts;     /* [E]   routes per expert                        */
+    int32_t *offsets;    /* [E+1] exclusive prefix of counts; [E] = T*k    */
+    int32_t *perm;       /* [T*k] buffer position p -> route j             */
+    int32_t *route_pos;  /* [T*k] route j -> buffer position p             */
+} moe_plan_bufs;
+
+/* Gradients written by moe_backward (fp32, overwritten). */
+typedef struct {
+    float *dW_gate;  /* [E, d, f] */
+    float *dW_up;    /* [E, d, f] */
+    float *dW_down;  /* [E, f, d] */
+    float *dW_r;     /* [d, E]    */
+    float *dZ;       /* [T, E] gradient wrt the router logits (zero for
+                        unselected experts); may be NULL (kept internally) */
+    float *dWg_s;    /* [d, f_shared], NULL iff f_shared == 0 */
+    float *dWu_s;    /* [d, f_shared], NULL iff f_shared == 0 */
+    float *dWd_s;    /* [f_shared, d], NULL iff f_shared == 0 */
+} moe_grads;
+
+/* Named regions of the workspace, for inspection after a synchronisation. */
+typedef enum {
+    MOE_WS_ERROR = 0,   /* int32[1]: nonzero after moe_plan saw an expert id
+                           outside [0, E) (such routes are left unplaced)   */
+    MOE_WS_A = 1,       /* bf16 [T*k, f]  x W_gate[e] in plan order         */
+    MOE_WS_B = 2,       /* bf16 [T*k, f]  x W_up[e]                         */
+    MOE_WS_H = 3,       /* bf16 [T*k, f]  silu(A) * B                       */
+    MOE_WS_YEXP = 4,    /* bf16 [T*k, d]  f_e(x) per route, plan order      */
+    MOE_WS_YSH = 5,     /* bf16 [T, d]    shared-expert output              */
+    MOE_WS_DG = 6,      /* fp32 [T*k]     <dY, f_e(x)> per route, plan order*/
+    MOE_WS_DA = 7,      /* bf16 [T*k, f]  gradient wrt A                    */
+    MOE_WS_DB = 8,      /* bf16 [T*k, f]  gradient wrt B                    */
+    MOE_WS_DXPERM = 9,  /* bf16 [T*k, d]  routed dX terms, plan order       */
+    MOE_WS_COUNT = 10
+} moe_ws_tensor;
+
+/* Workspace bytes needed by moe_route/moe_plan/moe_forward (with_backward=0)
+ * or additionally moe_backward (with_backward=1).  Pure host function;
+ * returns 0 for an invalid or unsupported shape. */
+size_t moe_workspace_bytes(const moe_shape *shape, int with_backward);
+
+/* Byte offset and size of a named workspace region (host only). */
+moe_status moe_workspace_region(const moe_shape *shape, int with_backward,
+                                moe_ws_tensor which, size_t *offset, size_t *bytes);
+
+/* Router (§2.1: the router projection selects the top-k experts and assigns
+ * each a weight).
+ *   X [T, d] bf16, W_r [d, E] bf16, bias [E] fp32 or NULL.
+ *   logits  [T, E] fp32 out: Z = X W_r + bias (fp32 accumulation).
+ *   topk_idx [T, k] int32 out: the k largest logits, ties to the lower
+ *            expert id, listed in ascending expert id.
+ *   topk_w  [T, k] fp32 out: exp(Z_te) / sum_{e' in S_t} exp(Z_te').
+ * Uses the workspace for a transposed copy of W_r. */
+moe_status moe_route(const moe_shape *shape, const moe_bf16 *X, const moe_bf16 *W_r,
+                     const float *bias, float *logits, int32_t *topk_idx, float *topk_w,
+                     void *ws, size_t ws_bytes, moe_stream stream);
+
+/* Dispatch plan (§3.1, Algorithm 1 for one source rank: a stable counting
+ * sort of the routes by expert; no host readback).
+ *   topk_idx [T, k] int32 in.  plan: counts, offsets, perm, route_pos out.
+ * An expert id outside [0, E) sets the MOE_WS_ERROR word; that route gets
+ * no position (perm/route_pos entries are then unspecified and the later
+ * steps bound-check every index they read). */
+moe_status moe_plan(const moe_shape *shape, const int32_t *topk_idx,
+                    const moe_plan_bufs *plan, void *ws, size_t ws_bytes,
+                    moe_stream stream);
+
+/* Materialised dispatch (§3.1 "Scheduling", local part): Xperm[p] =
+ * X[perm[p] / k] for p < T*k.  moe_forward does not need it (its GEMMs read
+ * token rows through the plan); it exists for callers that want the
+ * expert-contiguous buffer itself.  Xperm [T*k, d] bf16 out. */
+moe_status moe_dispatch(const moe_shape *shape, const moe_bf16 *X,
+                        const moe_plan_bufs *plan, moe_bf16 *Xperm, moe_stream stream);
+
+/* Forward of the layer (§2.1 equation).
+ *   X [T, d], weights, topk_idx/topk_w from moe_route, plan from moe_plan.
+ *   Y [T, d] bf16 out: Ysh[t] + sum over the token's experts in ascending
+ *   id of w * f_e(x_t), accumulated in fp32 and rounded once.
+ *   save_for_backward: keep A and B (gate/up pre-activations) in ws. */
+moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
+                       const int32_t *topk_idx, const float *topk_w,
+                       const moe_plan_bufs *plan, moe_bf16 *Y, int save_for_backward,
+                       void *ws, size_t ws_bytes, moe_stream stream);
+
+/* Backward of the layer for upstream gradient dY [T, d] bf16, with the
+ * selection held fixed.  Needs the same ws as a preceding moe_forward with
+ * save_for_backward = 1 and the same inputs.  The router-weight gradient
+ * uses <dY, f_e(x)> = <dY W_down[e]^T, h> (§3.4 "Router Weight Gradient
+ * Computation"), fused into the gated-activation backward.
+ *   dX [T, d] bf16 out; grads out (fp32). */
+moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf16 *X,
+                        const moe_bf16 *W_r, const moe_weights *weights,
+                        const int32_t *topk_idx, const float *topk_w,
+                        const moe_plan_bufs *plan, moe_bf16 *dX, const moe_grads *grads,
+                        void *ws, size_t ws_bytes, moe_stream stream);
+
+/* Static strings; never NULL. */
+const char *moe_status_string(moe_status status);
+const char *moe_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_H */

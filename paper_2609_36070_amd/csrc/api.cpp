@@ -1,0 +1,388 @@
+// C ABI of the MoE layer library: argument validation, workspace layout and
+// the launch sequence of each entry point.  Pure host code; every kernel is
+// enqueued on the caller's stream and nothing here synchronises.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+
+#include "../../include/moe.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr size_t ALIGN = 256;
+
+size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+// Byte offsets of every workspace region; depends only on the shape.
+struct Layout {
+    size_t err, blockcounts, blockbase, blockflags, wrt, rowidx, wperm;
+    size_t A, B, H, Yexp, As, Bs, Hs, Ysh;
+    size_t fwd_total;
+    size_t dA, dB, dgpart, dg, dZ, dXperm, dAs, dBs, dXsh, dwr_part;
+    size_t bwd_total;
+    int dg_parts;
+};
+
+Layout make_layout(const moe_shape &s) {
+    const size_t T = s.T, d = s.d, E = s.E, f = s.f, fs = s.f_shared;
+    const size_t R = T * (size_t)s.k;
+    const size_t nb = (size_t)plan_nblocks((long)R);
+    const size_t epad = (size_t)route_epad((int)E);
+    Layout L{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) { const size_t at = o; o += up(bytes > 0 ? bytes : 1); return at; };
+    L.err = take(4);
+    L.blockcounts = take(nb * E * 4);
+    L.blockbase = take(nb * E * 4);
+    L.blockflags = take(nb * 4);
+    L.wrt = take(epad * d * 2);
+    L.rowidx = take(R * 4);
+    L.wperm = take(R * 4);
+    L.A = take(R * f * 2);
+    L.B = take(R * f * 2);
+    L.H = take(R * f * 2);
+    L.Yexp = take(R * d * 2);
+    L.As = take(T * fs * 2);
+    L.Bs = take(T * fs * 2);
+    L.Hs = take(T * fs * 2);
+    L.Ysh = take(T * d * 2);
+    L.fwd_total = o;
+    L.dg_parts = (int)(f / (size_t)gemm_tile_n());
+    L.dA = take(R * f * 2);
+    L.dB = take(R * f * 2);
+    L.dgpart = take(R * (size_t)L.dg_parts * 4);
+    L.dg = take(R * 4);
+    L.dZ = take(T * E * 4);
+    L.dXperm = take(R * d * 2);
+    L.dAs = take(T * fs * 2);
+    L.dBs = take(T * fs * 2);
+    L.dXsh = take(T * d * 2);
+    L.dwr_part = take((size_t)dwr_nchunks((long)T) * d * E * 4);
+    L.bwd_total = o;
+    return L;
+}
+
+bool aligned(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool ptr_ok(const void *p) { return p != nullptr && aligned(p); }
+bool opt_ok(const void *p) { return p == nullptr || aligned(p); }
+
+moe_status check_shape(const moe_shape *s) {
+    if (!s) return MOE_EINVAL;
+    if (s->T < 0 || s->d <= 0 || s->E <= 0 || s->k <= 0 || s->f <= 0 || s->f_shared < 0)
+        return MOE_EINVAL;
+    if (s->k > s->E) return MOE_EINVAL;
+    if (s->d % 256 || s->f % 256 || s->f_shared % 256) return MOE_EUNSUPPORTED;
+    if (s->k > 16 || s->E > 256) return MOE_EUNSUPPORTED;
+    if (s->T * s->k >= (int64_t(1) << 31)) return MOE_EUNSUPPORTED;
+    if (s->d > (int64_t(1) << 20) || s->f > (int64_t(1) << 20) || s->f_shared > (int64_t(1) << 20))
+        return MOE_EUNSUPPORTED;
+    return MOE_OK;
+}
+
+moe_status check_weights(const moe_shape *s, const moe_weights *w) {
+    if (!w) return MOE_EINVAL;
+    if (!ptr_ok(w->W_gate) || !ptr_ok(w->W_up) || !ptr_ok(w->W_down)) return MOE_EINVAL;
+    const bool shared = s->f_shared > 0;
+    const bool any = w->Wg_s || w->Wu_s || w->Wd_s;
+    if (shared) {
+        if (!ptr_ok(w->Wg_s) || !ptr_ok(w->Wu_s) || !ptr_ok(w->Wd_s)) return MOE_EINVAL;
+    } else if (any) {
+        return MOE_EINVAL;
+    }
+    return MOE_OK;
+}
+
+moe_status check_plan(const moe_plan_bufs *p) {
+    if (!p) return MOE_EINVAL;
+    if (!ptr_ok(p->counts) || !ptr_ok(p->offsets) || !ptr_ok(p->perm) || !ptr_ok(p->route_pos))
+        return MOE_EINVAL;
+    return MOE_OK;
+}
+
+moe_status check_ws(const moe_shape *s, const void *ws, size_t ws_bytes, int with_backward) {
+    if (!ptr_ok(ws)) return MOE_EINVAL;
+    const Layout L = make_layout(*s);
+    if (ws_bytes < (with_backward ? L.bwd_total : L.fwd_total)) return MOE_ENOSPACE;
+    return MOE_OK;
+}
+
+template <typename T>
+T *at(void *ws, size_t off) { return reinterpret_cast<T *>(static_cast<char *>(ws) + off); }
+
+#define MOE_TRY(expr)                                      \
+    do {                                                   \
+        if ((expr) != hipSuccess) return MOE_EHIP;         \
+    } while (0)
+
+}  // namespace
+
+extern "C" {
+
+size_t moe_workspace_bytes(const moe_shape *shape, int with_backward) {
+    if (check_shape(shape) != MOE_OK) return 0;
+    const Layout L = make_layout(*shape);
+    return with_backward ? L.bwd_total : L.fwd_total;
+}
+
+moe_status moe_workspace_region(const moe_shape *shape, int with_backward, moe_ws_tensor which,
+                                size_t *offset, size_t *bytes) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if (!offset || !bytes) return MOE_EINVAL;
+    const Layout L = make_layout(*shape);
+    const size_t R = (size_t)(shape->T * shape->k);
+    const size_t T = shape->T, d = shape->d, f = shape->f;
+    switch (which) {
+        case MOE_WS_ERROR: *offset = L.err; *bytes = 4; break;
+        case MOE_WS_A: *offset = L.A; *bytes = R * f * 2; break;
+        case MOE_WS_B: *offset = L.B; *bytes = R * f * 2; break;
+        case MOE_WS_H: *offset = L.H; *bytes = R * f * 2; break;
+        case MOE_WS_YEXP: *offset = L.Yexp; *bytes = R * d * 2; break;
+        case MOE_WS_YSH: *offset = L.Ysh; *bytes = T * d * 2; break;
+        case MOE_WS_DG: *offset = L.dg; *bytes = R * 4; break;
+        case MOE_WS_DA: *offset = L.dA; *bytes = R * f * 2; break;
+        case MOE_WS_DB: *offset = L.dB; *bytes = R * f * 2; break;
+        case MOE_WS_DXPERM: *offset = L.dXperm; *bytes = R * d * 2; break;
+        default: return MOE_EINVAL;
+    }
+    if (!with_backward && *offset >= L.fwd_total) return MOE_EINVAL;
+    return MOE_OK;
+}
+
+moe_status moe_route(const moe_shape *shape, const moe_bf16 *X, const moe_bf16 *W_r,
+                     const float *bias, float *logits, int32_t *topk_idx, float *topk_w, void *ws,
+                     size_t ws_bytes, moe_stream stream) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if (!ptr_ok(X) || !ptr_ok(W_r) || !opt_ok(bias) || !ptr_ok(logits) || !ptr_ok(topk_idx) ||
+        !ptr_ok(topk_w))
+        return MOE_EINVAL;
+    if ((st = check_ws(shape, ws, ws_bytes, 0)) != MOE_OK) return st;
+    const Layout L = make_layout(*shape);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    MOE_TRY(launch_route(X, W_r, bias, logits, topk_idx, topk_w, at<uint16_t>(ws, L.wrt),
+                         (int)shape->T, (int)shape->d, (int)shape->E, (int)shape->k, s));
+    return MOE_OK;
+}
+
+moe_status moe_plan(const moe_shape *shape, const int32_t *topk_idx, const moe_plan_bufs *plan,
+                    void *ws, size_t ws_bytes, moe_stream stream) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if (!ptr_ok(topk_idx)) return MOE_EINVAL;
+    if ((st = check_plan(plan)) != MOE_OK) return st;
+    if ((st = check_ws(shape, ws, ws_bytes, 0)) != MOE_OK) return st;
+    const Layout L = make_layout(*shape);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int R = (int)(shape->T * shape->k);
+    MOE_TRY(launch_plan(topk_idx, R, (int)shape->E, plan->counts, plan->offsets, plan->perm,
+                        plan->route_pos, at<int>(ws, L.blockcounts), at<int>(ws, L.blockbase),
+                        at<int>(ws, L.blockflags), at<int>(ws, L.err), s));
+    return MOE_OK;
+}
+
+moe_status moe_dispatch(const moe_shape *shape, const moe_bf16 *X, const moe_plan_bufs *plan,
+                        moe_bf16 *Xperm, moe_stream stream) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if (!ptr_ok(X) || !ptr_ok(Xperm)) return MOE_EINVAL;
+    if ((st = check_plan(plan)) != MOE_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    MOE_TRY(launch_gather(X, plan->perm, plan->offsets, (int)shape->E, (int)shape->k,
+                          (int)shape->T, (int)shape->d, Xperm, s));
+    return MOE_OK;
+}
+
+moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
+                       const int32_t *topk_idx, const float *topk_w, const moe_plan_bufs *plan,
+                       moe_bf16 *Y, int save_for_backward, void *ws, size_t ws_bytes,
+                       moe_stream stream) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if (!ptr_ok(X) || !ptr_ok(topk_idx) || !ptr_ok(topk_w) || !ptr_ok(Y)) return MOE_EINVAL;
+    if ((st = check_weights(shape, weights)) != MOE_OK) return st;
+    if ((st = check_plan(plan)) != MOE_OK) return st;
+    if ((st = check_ws(shape, ws, ws_bytes, 0)) != MOE_OK) return st;
+    const Layout L = make_layout(*shape);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int T = (int)shape->T, d = (int)shape->d, E = (int)shape->E, k = (int)shape->k;
+    const int f = (int)shape->f, fs = (int)shape->f_shared;
+    const long R = (long)T * k;
+    int *rowidx = at<int>(ws, L.rowidx);
+    float *wperm = at<float>(ws, L.wperm);
+    uint16_t *H = at<uint16_t>(ws, L.H);
+
+    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, rowidx, wperm, s));
+    {   // routed up/gate + SwiGLU
+        GemmArgs g;
+        g.A = X; g.lda = d; g.a_rows = rowidx; g.a_nrows = T > 0 ? T : 1;
+        g.B = weights->W_gate; g.B2 = weights->W_up; g.ldb = f; g.b_estride = (long)d * f;
+        g.N = f; g.K = d; g.offsets = plan->offsets; g.E = E;
+        g.C = H; g.ldc = f;
+        if (save_for_backward) { g.C2 = at<uint16_t>(ws, L.A); g.C3 = at<uint16_t>(ws, L.B); }
+        MOE_TRY(launch_gemm_fwd_up(g, R, E, s));
+    }
+    if (fs > 0) {   // shared up/gate + SwiGLU
+        GemmArgs g;
+        g.A = X; g.lda = d; g.a_nrows = T > 0 ? T : 1; g.M = T;
+        g.B = weights->Wg_s; g.B2 = weights->Wu_s; g.ldb = fs;
+        g.N = fs; g.K = d;
+        g.C = at<uint16_t>(ws, L.Hs); g.ldc = fs;
+        if (save_for_backward) { g.C2 = at<uint16_t>(ws, L.As); g.C3 = at<uint16_t>(ws, L.Bs); }
+        MOE_TRY(launch_gemm_fwd_up(g, T, 1, s));
+    }
+    {   // routed down
+        GemmArgs g;
+        g.A = H; g.lda = f; g.a_nrows = R > 0 ? (int)R : 1;
+        g.B = weights->W_down; g.ldb = d; g.b_estride = (long)f * d;
+        g.N = d; g.K = f; g.offsets = plan->offsets; g.E = E;
+        g.C = at<uint16_t>(ws, L.Yexp); g.ldc = d;
+        MOE_TRY(launch_gemm_fwd_down(g, R, E, s));
+    }
+    if (fs > 0) {   // shared down
+        GemmArgs g;
+        g.A = at<uint16_t>(ws, L.Hs); g.lda = fs; g.a_nrows = T > 0 ? T : 1; g.M = T;
+        g.B = weights->Wd_s; g.ldb = d;
+        g.N = d; g.K = fs;
+        g.C = at<uint16_t>(ws, L.Ysh); g.ldc = d;
+        MOE_TRY(launch_gemm_fwd_down(g, T, 1, s));
+    }
+    MOE_TRY(launch_combine(at<uint16_t>(ws, L.Yexp), fs > 0 ? at<uint16_t>(ws, L.Ysh) : nullptr,
+                           topk_w, plan->route_pos, T, d, k, Y, s));
+    return MOE_OK;
+}
+
+moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf16 *X,
+                        const moe_bf16 *W_r, const moe_weights *weights, const int32_t *topk_idx,
+                        const float *topk_w, const moe_plan_bufs *plan, moe_bf16 *dX,
+                        const moe_grads *grads, void *ws, size_t ws_bytes, moe_stream stream) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if (!ptr_ok(dY) || !ptr_ok(X) || !ptr_ok(W_r) || !ptr_ok(topk_idx) || !ptr_ok(topk_w) ||
+        !ptr_ok(dX))
+        return MOE_EINVAL;
+    if ((st = check_weights(shape, weights)) != MOE_OK) return st;
+    if ((st = check_plan(plan)) != MOE_OK) return st;
+    if (!grads || !ptr_ok(grads->dW_gate) || !ptr_ok(grads->dW_up) || !ptr_ok(grads->dW_down) ||
+        !ptr_ok(grads->dW_r) || !opt_ok(grads->dZ))
+        return MOE_EINVAL;
+    const bool shared = shape->f_shared > 0;
+    if (shared) {
+        if (!ptr_ok(grads->dWg_s) || !ptr_ok(grads->dWu_s) || !ptr_ok(grads->dWd_s)) return MOE_EINVAL;
+    } else if (grads->dWg_s || grads->dWu_s || grads->dWd_s) {
+        return MOE_EINVAL;
+    }
+    if ((st = check_ws(shape, ws, ws_bytes, 1)) != MOE_OK) return st;
+    const Layout L = make_layout(*shape);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int T = (int)shape->T, d = (int)shape->d, E = (int)shape->E, k = (int)shape->k;
+    const int f = (int)shape->f, fs = (int)shape->f_shared;
+    const long R = (long)T * k;
+    const int Tn = T > 0 ? T : 1;
+    const int Rn = R > 0 ? (int)R : 1;
+    int *rowidx = at<int>(ws, L.rowidx);
+    float *wperm = at<float>(ws, L.wperm);
+    uint16_t *dA = at<uint16_t>(ws, L.dA), *dB = at<uint16_t>(ws, L.dB);
+    float *dgpart = at<float>(ws, L.dgpart);
+    float *dZ = grads->dZ ? grads->dZ : at<float>(ws, L.dZ);
+
+    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, rowidx, wperm, s));
+    {   // dh' = dY W_down^T with SwiGLU backward and dg partials
+        GemmArgs g;
+        g.A = dY; g.lda = d; g.a_rows = rowidx; g.a_nrows = Tn;
+        g.B = weights->W_down; g.ldb = d; g.b_estride = (long)f * d;
+        g.N = f; g.K = d; g.offsets = plan->offsets; g.E = E;
+        g.E1 = at<uint16_t>(ws, L.A); g.E2 = at<uint16_t>(ws, L.B); g.ldc = f;
+        g.rowscale = wperm; g.C = dA; g.C2 = dB; g.dgpart = dgpart; g.dg_ld = L.dg_parts;
+        MOE_TRY(launch_gemm_bwd_dgrad(g, R, E, s));
+    }
+    MOE_TRY(launch_softmax_bwd(dgpart, L.dg_parts, plan->route_pos, topk_w, topk_idx, T, k, E,
+                               at<float>(ws, L.dg), dZ, s));
+    {   // dXperm = dA W_gate^T + dB W_up^T
+        GemmArgs g;
+        g.A = dA; g.A2 = dB; g.lda = f; g.a_nrows = Rn;
+        g.B = weights->W_gate; g.B2 = weights->W_up; g.ldb = f; g.b_estride = (long)d * f;
+        g.N = d; g.K = f; g.offsets = plan->offsets; g.E = E;
+        g.C = at<uint16_t>(ws, L.dXperm); g.ldc = d;
+        MOE_TRY(launch_gemm_bwd_dx(g, R, E, s));
+    }
+    {   // dW_gate[e] = Xperm_e^T dA_e, dW_up[e] = Xperm_e^T dB_e
+        GemmArgs g;
+        g.A = X; g.lda = d; g.a_rows = rowidx; g.a_nrows = Tn;
+        g.B = dA; g.ldb = f; g.b_nrows = Rn;
+        g.M = d; g.N = f; g.offsets = plan->offsets; g.E = E;
+        g.Cf = grads->dW_gate; g.c_estride = (long)d * f; g.ldc = f;
+        MOE_TRY(launch_gemm_wgrad(g, E, s));
+        g.B = dB; g.Cf = grads->dW_up;
+        MOE_TRY(launch_gemm_wgrad(g, E, s));
+    }
+    {   // dW_down[e] = (w H_e)^T dYperm_e
+        GemmArgs g;
+        g.A = at<uint16_t>(ws, L.H); g.lda = f; g.a_nrows = Rn; g.a_kscale = wperm;
+        g.B = dY; g.ldb = d; g.b_rows = rowidx; g.b_nrows = Tn;
+        g.M = f; g.N = d; g.offsets = plan->offsets; g.E = E;
+        g.Cf = grads->dW_down; g.c_estride = (long)f * d; g.ldc = d;
+        MOE_TRY(launch_gemm_wgrad(g, E, s));
+    }
+    uint16_t *dXsh = nullptr;
+    if (shared) {
+        uint16_t *dAs = at<uint16_t>(ws, L.dAs), *dBs = at<uint16_t>(ws, L.dBs);
+        dXsh = at<uint16_t>(ws, L.dXsh);
+        {
+            GemmArgs g;
+            g.A = dY; g.lda = d; g.a_nrows = Tn; g.M = T;
+            g.B = weights->Wd_s; g.ldb = d;
+            g.N = fs; g.K = d;
+            g.E1 = at<uint16_t>(ws, L.As); g.E2 = at<uint16_t>(ws, L.Bs); g.ldc = fs;
+            g.C = dAs; g.C2 = dBs;
+            MOE_TRY(launch_gemm_bwd_dgrad(g, T, 1, s));
+        }
+        {
+            GemmArgs g;
+            g.A = dAs; g.A2 = dBs; g.lda = fs; g.a_nrows = Tn; g.M = T;
+            g.B = weights->Wg_s; g.B2 = weights->Wu_s; g.ldb = fs;
+            g.N = d; g.K = fs;
+            g.C = dXsh; g.ldc = d;
+            MOE_TRY(launch_gemm_bwd_dx(g, T, 1, s));
+        }
+        {
+            GemmArgs g;
+            g.A = X; g.lda = d; g.a_nrows = Tn;
+            g.B = dAs; g.ldb = fs; g.b_nrows = Tn;
+            g.M = d; g.N = fs; g.K = T;
+            g.Cf = grads->dWg_s; g.ldc = fs;
+            MOE_TRY(launch_gemm_wgrad(g, 1, s));
+            g.B = dBs; g.Cf = grads->dWu_s;
+            MOE_TRY(launch_gemm_wgrad(g, 1, s));
+        }
+        {
+            GemmArgs g;
+            g.A = at<uint16_t>(ws, L.Hs); g.lda = fs; g.a_nrows = Tn;
+            g.B = dY; g.ldb = d; g.b_nrows = Tn;
+            g.M = fs; g.N = d; g.K = T;
+            g.Cf = grads->dWd_s; g.ldc = d;
+            MOE_TRY(launch_gemm_wgrad(g, 1, s));
+        }
+    }
+    MOE_TRY(launch_dwr(X, dZ, T, d, E, at<float>(ws, L.dwr_part), grads->dW_r, s));
+    MOE_TRY(launch_reverse_combine(at<uint16_t>(ws, L.dXperm), dXsh, dZ, W_r, plan->route_pos, T, d,
+                                   k, E, dX, s));
+    return MOE_OK;
+}
+
+const char *moe_status_string(moe_status status) {
+    switch (status) {
+        case MOE_OK: return "ok";
+        case MOE_EINVAL: return "invalid argument";
+        case MOE_EUNSUPPORTED: return "unsupported shape";
+        case MOE_ENOSPACE: return "workspace too small";
+        case MOE_EHIP: return "HIP launch failed";
+        default: return "unknown status";
+    }
+}
+
+const char *moe_version(void) { return "moe-mi355x 0.1 (gfx950)"; }
+
+}  // extern "C"

@@ -1,0 +1,39 @@
+// Shared device helpers for the gfx950 MoE kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+#define DEV __device__ __forceinline__
+
+// bf16 bits -> fp32 (exact)
+DEV float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+DEV float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+DEV float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16 bits, round to nearest even (gfx950 converts natively).
+DEV uint16_t f2bf(float x) {
+    __bf16 b = (__bf16)x;
+    return __builtin_bit_cast(uint16_t, b);
+}
+DEV uint32_t pack_bf2(float lo, float hi) {
+    return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+}
+
+DEV float silu_f(float a) { return a / (1.0f + expf(-a)); }
+
+DEV int wave_lane() { return threadIdx.x & 63; }
+
+// 32-bit wave shuffles
+DEV float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, 64); }
+DEV int shfl_xor_i(int v, int m) { return __shfl_xor(v, m, 64); }
+
+DEV u32x4_t ld_u32x4(const void *p) { return *reinterpret_cast<const u32x4_t *>(p); }
+DEV void st_u32x4(void *p, u32x4_t v) { *reinterpret_cast<u32x4_t *>(p) = v; }
+DEV u32x2_t ld_u32x2(const void *p) { return *reinterpret_cast<const u32x2_t *>(p); }

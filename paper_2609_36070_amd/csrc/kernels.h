@@ -1,0 +1,72 @@
+// Internal launcher declarations of the gfx950 MoE kernels (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+constexpr int PLAN_CHUNK = 1024;  // routes per plan block
+
+// Grouped-GEMM problem description (see gemm.hip for the five modes).
+struct GemmArgs {
+    // operand A
+    const uint16_t *A = nullptr;
+    const uint16_t *A2 = nullptr;      // second K half (BWD_DX)
+    long lda = 0;
+    const int *a_rows = nullptr;       // row gather (MK rows / KM k-rows)
+    int a_nrows = 1;                   // rows addressable through A (clamp bound)
+    const float *a_kscale = nullptr;   // KM: per-k-row scale
+    // operand B
+    const uint16_t *B = nullptr;
+    const uint16_t *B2 = nullptr;      // W_up (FWD_UP, BWD_DX)
+    long ldb = 0;
+    long b_estride = 0;                // elements between experts' weights
+    const int *b_rows = nullptr;       // WGRAD: k-row gather
+    int b_nrows = 1;
+    // problem
+    int M = 0, N = 0, K = 0;
+    const int *offsets = nullptr;      // per-expert row ranges (device), or null
+    int E = 0;
+    // outputs
+    uint16_t *C = nullptr, *C2 = nullptr, *C3 = nullptr;
+    long ldc = 0;
+    float *Cf = nullptr;
+    long c_estride = 0;
+    const uint16_t *E1 = nullptr, *E2 = nullptr;  // BWD_DGRAD: saved A, B
+    const float *rowscale = nullptr;              // BWD_DGRAD: router weight per row
+    float *dgpart = nullptr;
+    int dg_ld = 0;
+};
+
+int gemm_tile_m();
+int gemm_tile_n();
+hipError_t launch_gemm_fwd_up(const GemmArgs &g, long rows, int groups, hipStream_t st);
+hipError_t launch_gemm_fwd_down(const GemmArgs &g, long rows, int groups, hipStream_t st);
+hipError_t launch_gemm_bwd_dgrad(const GemmArgs &g, long rows, int groups, hipStream_t st);
+hipError_t launch_gemm_bwd_dx(const GemmArgs &g, long rows, int groups, hipStream_t st);
+hipError_t launch_gemm_wgrad(const GemmArgs &g, int groups, hipStream_t st);
+
+int route_epad(int E);
+hipError_t launch_route(const uint16_t *X, const uint16_t *W_r, const float *bias, float *logits,
+                        int *topk_idx, float *topk_w, uint16_t *WrT, int T, int d, int E, int k,
+                        hipStream_t st);
+
+int plan_nblocks(long R);
+hipError_t launch_plan(const int *topk_idx, int R, int E, int *counts, int *offsets, int *perm,
+                       int *route_pos, int *blockcounts, int *blockbase, int *blockflags, int *err,
+                       hipStream_t st);
+
+int dwr_nchunks(long T);
+hipError_t launch_gather(const uint16_t *X, const int *perm, const int *offsets, int E, int k, int T,
+                         int d, uint16_t *Xperm, hipStream_t st);
+hipError_t launch_prep(const int *perm, const int *offsets, int E, const float *topk_w, int k, int T,
+                       int *rowidx, float *wperm, hipStream_t st);
+hipError_t launch_combine(const uint16_t *Yexp, const uint16_t *Ysh, const float *topk_w,
+                          const int *route_pos, int T, int d, int k, uint16_t *Y, hipStream_t st);
+hipError_t launch_softmax_bwd(const float *dgpart, int nparts, const int *route_pos,
+                              const float *topk_w, const int *topk_idx, int T, int k, int E,
+                              float *dg_out, float *dZ, hipStream_t st);
+hipError_t launch_reverse_combine(const uint16_t *dXperm, const uint16_t *dXsh, const float *dZ,
+                                  const uint16_t *W_r, const int *route_pos, int T, int d, int k,
+                                  int E, uint16_t *dX, hipStream_t st);
+hipError_t launch_dwr(const uint16_t *X, const float *dZ, int T, int d, int E, float *part,
+                      float *dWr, hipStream_t st);

@@ -1,0 +1,345 @@
+// HBM-bound steps around the expert GEMMs: dispatch gather, plan-order
+// prologue, the fixed-order weighted combine and its backward counterpart,
+// the restricted-softmax backward and the router-weight gradient.
+//
+// Every row copy moves 16-byte vectors; every sum over a token's routes runs
+// in slot order (ascending expert id) in fp32, so results are bitwise
+// repeatable (§3.4 "Determinism").
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+// Xperm[p] = X[perm[p] / k]; rows past the placed total are zero-filled.
+__global__ __launch_bounds__(256) void gather_rows_kernel(const uint16_t *__restrict__ X,
+                                                          const int *__restrict__ perm,
+                                                          const int *__restrict__ offsets, int E,
+                                                          int k, int T, int d, int R,
+                                                          uint16_t *__restrict__ out) {
+    const int total = offsets[E];
+    const int nc = d / 8;
+    for (int p = blockIdx.x; p < R; p += gridDim.x) {
+        int t = -1;
+        if (p < total) {
+            const int j = perm[p];
+            t = (j >= 0 && j < R) ? j / k : -1;
+        }
+        u32x4_t *dst = reinterpret_cast<u32x4_t *>(out + (long)p * d);
+        if (t < 0 || t >= T) {
+            for (int c = threadIdx.x; c < nc; c += 256) dst[c] = u32x4_t{0, 0, 0, 0};
+        } else {
+            const u32x4_t *src = reinterpret_cast<const u32x4_t *>(X + (long)t * d);
+            for (int c = threadIdx.x; c < nc; c += 256) dst[c] = src[c];
+        }
+    }
+}
+
+// Plan-order prologue: token row and router weight of every buffer position.
+__global__ __launch_bounds__(256) void prep_kernel(const int *__restrict__ perm,
+                                                   const int *__restrict__ offsets, int E,
+                                                   const float *__restrict__ topk_w, int k, int T,
+                                                   int R, int *__restrict__ rowidx,
+                                                   float *__restrict__ wperm) {
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    if (p >= R) return;
+    const int total = offsets[E];
+    int t = 0;
+    float wv = 0.f;
+    if (p < total) {
+        const int j = perm[p];
+        if (j >= 0 && j < R) {
+            t = j / k;
+            wv = topk_w[j];
+        }
+    }
+    rowidx[p] = t < T ? t : 0;
+    wperm[p] = wv;
+}
+
+// Y[t] = Ysh[t] + sum_slot w[t,slot] * Yexp[route_pos[t*k+slot]]  (fp32, one rounding)
+__global__ __launch_bounds__(256) void combine_kernel(const uint16_t *__restrict__ Yexp,
+                                                      const uint16_t *__restrict__ Ysh,
+                                                      const float *__restrict__ topk_w,
+                                                      const int *__restrict__ route_pos, int T,
+                                                      int d, int k, int R,
+                                                      uint16_t *__restrict__ Y) {
+    const int nc = d / 8;
+    for (int t = blockIdx.x; t < T; t += gridDim.x) {
+        int pos[16];
+        float wt[16];
+#pragma unroll
+        for (int s = 0; s < 16; ++s) {
+            pos[s] = -1;
+            wt[s] = 0.f;
+            if (s < k) {
+                const int p = route_pos[(long)t * k + s];
+                pos[s] = (p >= 0 && p < R) ? p : -1;
+                wt[s] = topk_w[(long)t * k + s];
+            }
+        }
+        for (int c = threadIdx.x; c < nc; c += 256) {
+            float acc[8];
+            if (Ysh) {
+                const u32x4_t v = ld_u32x4(Ysh + (long)t * d + 8 * c);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    acc[2 * q] = bf_lo(v[q]);
+                    acc[2 * q + 1] = bf_hi(v[q]);
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+            }
+#pragma unroll
+            for (int s = 0; s < 16; ++s) {
+                if (s < k && pos[s] >= 0) {
+                    const u32x4_t v = ld_u32x4(Yexp + (long)pos[s] * d + 8 * c);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        acc[2 * q] = acc[2 * q] + wt[s] * bf_lo(v[q]);
+                        acc[2 * q + 1] = acc[2 * q + 1] + wt[s] * bf_hi(v[q]);
+                    }
+                }
+            }
+            u32x4_t o;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) o[q] = pack_bf2(acc[2 * q], acc[2 * q + 1]);
+            st_u32x4(Y + (long)t * d + 8 * c, o);
+        }
+    }
+}
+
+// dg[p] = sum over n-tiles of the partial <dh', h> (fixed order), then the
+// restricted-softmax backward per token:
+//   dZ[t,e_s] = w_s (dg_s - sum_s' w_s' dg_s'),  zero for unselected experts.
+__global__ __launch_bounds__(256) void softmax_bwd_kernel(const float *__restrict__ dgpart,
+                                                          int nparts,
+                                                          const int *__restrict__ route_pos,
+                                                          const float *__restrict__ topk_w,
+                                                          const int *__restrict__ topk_idx, int T,
+                                                          int k, int E, int R,
+                                                          float *__restrict__ dg_out,
+                                                          float *__restrict__ dZ) {
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    if (t >= T) return;
+    float dg[16], wt[16];
+    float swdg = 0.f;
+#pragma unroll
+    for (int s = 0; s < 16; ++s) {
+        dg[s] = 0.f;
+        wt[s] = 0.f;
+        if (s < k) {
+            const int p = route_pos[(long)t * k + s];
+            wt[s] = topk_w[(long)t * k + s];
+            if (p >= 0 && p < R) {
+                float acc = 0.f;
+                for (int q = 0; q < nparts; ++q) acc = acc + dgpart[(long)p * nparts + q];
+                dg[s] = acc;
+                dg_out[p] = acc;
+            }
+            swdg = swdg + wt[s] * dg[s];
+        }
+    }
+    for (int e = 0; e < E; ++e) dZ[(long)t * E + e] = 0.f;
+#pragma unroll
+    for (int s = 0; s < 16; ++s) {
+        if (s < k) {
+            const int e = topk_idx[(long)t * k + s];
+            if (e >= 0 && e < E) dZ[(long)t * E + e] = wt[s] * (dg[s] - swdg);
+        }
+    }
+}
+
+// dX[t] = dXsh[t] + sum_slot dXperm[route_pos[t*k+slot]] + sum_e dZ[t,e] W_r[:,e]
+__global__ __launch_bounds__(256) void reverse_combine_kernel(const uint16_t *__restrict__ dXperm,
+                                                              const uint16_t *__restrict__ dXsh,
+                                                              const float *__restrict__ dZ,
+                                                              const uint16_t *__restrict__ Wr,
+                                                              const int *__restrict__ route_pos,
+                                                              int T, int d, int k, int E, int R,
+                                                              uint16_t *__restrict__ dX) {
+    __shared__ float dz[256];
+    const int nc = d / 8;
+    for (int t = blockIdx.x; t < T; t += gridDim.x) {
+        __syncthreads();
+        for (int e = threadIdx.x; e < E; e += 256) dz[e] = dZ[(long)t * E + e];
+        __syncthreads();
+        int pos[16];
+#pragma unroll
+        for (int s = 0; s < 16; ++s) {
+            pos[s] = -1;
+            if (s < k) {
+                const int p = route_pos[(long)t * k + s];
+                pos[s] = (p >= 0 && p < R) ? p : -1;
+            }
+        }
+        for (int c = threadIdx.x; c < nc; c += 256) {
+            float acc[8];
+            if (dXsh) {
+                const u32x4_t v = ld_u32x4(dXsh + (long)t * d + 8 * c);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    acc[2 * q] = bf_lo(v[q]);
+                    acc[2 * q + 1] = bf_hi(v[q]);
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+            }
+#pragma unroll
+            for (int s = 0; s < 16; ++s) {
+                if (s < k && pos[s] >= 0) {
+                    const u32x4_t v = ld_u32x4(dXperm + (long)pos[s] * d + 8 * c);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        acc[2 * q] = acc[2 * q] + bf_lo(v[q]);
+                        acc[2 * q + 1] = acc[2 * q + 1] + bf_hi(v[q]);
+                    }
+                }
+            }
+            // router term: rows 8c..8c+7 of W_r, all experts
+            float racc[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) racc[q] = 0.f;
+            if ((E & 7) == 0) {
+                for (int e0 = 0; e0 < E; e0 += 8) {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        const u32x4_t wv = ld_u32x4(Wr + (long)(8 * c + q) * E + e0);
+#pragma unroll
+                        for (int h = 0; h < 4; ++h) {
+                            racc[q] = racc[q] + dz[e0 + 2 * h] * bf_lo(wv[h]);
+                            racc[q] = racc[q] + dz[e0 + 2 * h + 1] * bf_hi(wv[h]);
+                        }
+                    }
+                }
+            } else {
+                for (int e = 0; e < E; ++e) {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q)
+                        racc[q] = racc[q] + dz[e] * bf2f(Wr[(long)(8 * c + q) * E + e]);
+                }
+            }
+            u32x4_t o;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                o[q] = pack_bf2(acc[2 * q] + racc[2 * q], acc[2 * q + 1] + racc[2 * q + 1]);
+            st_u32x4(dX + (long)t * d + 8 * c, o);
+        }
+    }
+}
+
+// dW_r = X^T dZ in two fixed-order stages.  Stage 1: block (column block,
+// token chunk) -> part[chunk][i][e]; stage 2 sums the chunks in order.
+constexpr int DWR_TC = 256;   // tokens per chunk
+constexpr int DWR_EG = 16;    // experts per register group
+
+__global__ __launch_bounds__(256) void dwr_partial_kernel(const uint16_t *__restrict__ X,
+                                                          const float *__restrict__ dZ, int T,
+                                                          int d, int E,
+                                                          float *__restrict__ part) {
+    __shared__ float dzs[DWR_TC][DWR_EG];
+    const int i = (blockIdx.x * 256 + threadIdx.x) * 2;  // two columns per thread
+    const int ch = blockIdx.y;
+    const int t0 = ch * DWR_TC;
+    const int t1 = min(T, t0 + DWR_TC);
+    for (int e0 = 0; e0 < E; e0 += DWR_EG) {
+        __syncthreads();
+        for (int q = threadIdx.x; q < DWR_TC * DWR_EG; q += 256) {
+            const int tt = q / DWR_EG, ee = q % DWR_EG;
+            dzs[tt][ee] = (t0 + tt < t1 && e0 + ee < E) ? dZ[(long)(t0 + tt) * E + e0 + ee] : 0.f;
+        }
+        __syncthreads();
+        float a0[DWR_EG], a1[DWR_EG];
+#pragma unroll
+        for (int ee = 0; ee < DWR_EG; ++ee) { a0[ee] = 0.f; a1[ee] = 0.f; }
+        if (i < d) {
+            for (int t = t0; t < t1; ++t) {
+                const uint32_t xv = *reinterpret_cast<const uint32_t *>(X + (long)t * d + i);
+                const float x0 = bf_lo(xv), x1 = bf_hi(xv);
+#pragma unroll
+                for (int ee = 0; ee < DWR_EG; ++ee) {
+                    a0[ee] = a0[ee] + x0 * dzs[t - t0][ee];
+                    a1[ee] = a1[ee] + x1 * dzs[t - t0][ee];
+                }
+            }
+#pragma unroll
+            for (int ee = 0; ee < DWR_EG; ++ee) {
+                if (e0 + ee < E) {
+                    part[((long)ch * d + i) * E + e0 + ee] = a0[ee];
+                    part[((long)ch * d + i + 1) * E + e0 + ee] = a1[ee];
+                }
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void dwr_reduce_kernel(const float *__restrict__ part, int nch,
+                                                         long n, float *__restrict__ dWr) {
+    const long q = (long)blockIdx.x * 256 + threadIdx.x;
+    if (q >= n) return;
+    float acc = 0.f;
+    for (int c = 0; c < nch; ++c) acc = acc + part[(long)c * n + q];
+    dWr[q] = acc;
+}
+
+inline unsigned rows_grid(long rows) { return (unsigned)(rows < 16384 ? (rows > 0 ? rows : 1) : 16384); }
+
+}  // namespace
+
+int dwr_nchunks(long T) { return (int)((T + DWR_TC - 1) / DWR_TC); }
+
+hipError_t launch_gather(const uint16_t *X, const int *perm, const int *offsets, int E, int k, int T,
+                         int d, uint16_t *Xperm, hipStream_t st) {
+    const long R = (long)T * k;
+    if (R == 0) return hipSuccess;
+    gather_rows_kernel<<<dim3(rows_grid(R)), dim3(256), 0, st>>>(X, perm, offsets, E, k, T, d, (int)R, Xperm);
+    return hipGetLastError();
+}
+
+hipError_t launch_prep(const int *perm, const int *offsets, int E, const float *topk_w, int k, int T,
+                       int *rowidx, float *wperm, hipStream_t st) {
+    const long R = (long)T * k;
+    if (R == 0) return hipSuccess;
+    prep_kernel<<<dim3((unsigned)((R + 255) / 256)), dim3(256), 0, st>>>(perm, offsets, E, topk_w, k, T,
+                                                                         (int)R, rowidx, wperm);
+    return hipGetLastError();
+}
+
+hipError_t launch_combine(const uint16_t *Yexp, const uint16_t *Ysh, const float *topk_w,
+                          const int *route_pos, int T, int d, int k, uint16_t *Y, hipStream_t st) {
+    if (T == 0) return hipSuccess;
+    combine_kernel<<<dim3(rows_grid(T)), dim3(256), 0, st>>>(Yexp, Ysh, topk_w, route_pos, T, d, k,
+                                                              T * k, Y);
+    return hipGetLastError();
+}
+
+hipError_t launch_softmax_bwd(const float *dgpart, int nparts, const int *route_pos,
+                              const float *topk_w, const int *topk_idx, int T, int k, int E,
+                              float *dg_out, float *dZ, hipStream_t st) {
+    if (T == 0) return hipSuccess;
+    softmax_bwd_kernel<<<dim3((unsigned)((T + 255) / 256)), dim3(256), 0, st>>>(
+        dgpart, nparts, route_pos, topk_w, topk_idx, T, k, E, T * k, dg_out, dZ);
+    return hipGetLastError();
+}
+
+hipError_t launch_reverse_combine(const uint16_t *dXperm, const uint16_t *dXsh, const float *dZ,
+                                  const uint16_t *W_r, const int *route_pos, int T, int d, int k,
+                                  int E, uint16_t *dX, hipStream_t st) {
+    if (T == 0) return hipSuccess;
+    reverse_combine_kernel<<<dim3(rows_grid(T)), dim3(256), 0, st>>>(dXperm, dXsh, dZ, W_r, route_pos,
+                                                                      T, d, k, E, T * k, dX);
+    return hipGetLastError();
+}
+
+hipError_t launch_dwr(const uint16_t *X, const float *dZ, int T, int d, int E, float *part,
+                      float *dWr, hipStream_t st) {
+    const int nch = dwr_nchunks(T);
+    const long n = (long)d * E;
+    if (nch > 0) {
+        dim3 grid((unsigned)((d / 2 + 255) / 256), (unsigned)nch);
+        dwr_partial_kernel<<<grid, dim3(256), 0, st>>>(X, dZ, T, d, E, part);
+    }
+    dwr_reduce_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st>>>(part, nch, n, dWr);
+    return hipGetLastError();
+}

@@ -1,0 +1,136 @@
+"""Host-side checks of the C ABI (CPU only: no kernel is ever launched here).
+
+The library must load, export every function include/moe.h declares, size
+its workspace from the shape alone, and reject bad arguments before touching
+the GPU.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_36070_amd import binding as B
+from paper_2609_36070_amd.workloads import WORKLOADS
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "moe.h")
+
+FAKE = 0x10000          # 16-byte aligned non-null address; never dereferenced on these paths
+MISALIGNED = 0x10008
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(moe_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    L = B.lib()
+    names = declared_functions()
+    assert names, "no declarations parsed"
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(B.EXPORTS)
+    assert "gfx950" in B.version()
+
+
+def test_status_strings():
+    for s in range(5):
+        assert B.status_string(s)
+    assert B.status_string(99) == "unknown status"
+
+
+@pytest.mark.parametrize("name", sorted(WORKLOADS))
+def test_workspace_sizes(name):
+    w = WORKLOADS[name]
+    sh = B.make_shape(w.T, w.d, w.E, w.k, w.f, w.f_s)
+    fwd = B.moe_workspace_bytes(sh, False)
+    bwd = B.moe_workspace_bytes(sh, True)
+    R = w.T * w.k
+    assert fwd >= R * w.f * 2 * 3 + R * w.d * 2           # A, B, H, Yexp at least
+    assert bwd >= fwd + R * w.d * 2                       # plus dXperm
+    for which in range(B.WS_DXPERM + 1):
+        off, nb = B.moe_workspace_region(sh, True, which)
+        assert off % 256 == 0 and off + nb <= bwd
+
+
+def test_workspace_zero_for_bad_shapes():
+    assert B.moe_workspace_bytes(B.make_shape(16, 100, 8, 2, 256), False) == 0   # d % 256
+    assert B.moe_workspace_bytes(B.make_shape(16, 256, 4, 5, 256), False) == 0   # k > E
+    assert B.moe_workspace_bytes(B.make_shape(16, 256, 300, 2, 256), False) == 0  # E > 256
+
+
+def _route(shape, **kw):
+    args = dict(X=FAKE, W_r=FAKE, bias=None, logits=FAKE, topk_idx=FAKE, topk_w=FAKE, ws=FAKE,
+                ws_bytes=1 << 40)
+    args.update(kw)
+    return B.lib().moe_route(ctypes.byref(shape), args["X"], args["W_r"], args["bias"],
+                             args["logits"], args["topk_idx"], args["topk_w"], args["ws"],
+                             args["ws_bytes"], None)
+
+
+def test_route_validation():
+    ok = B.make_shape(64, 256, 8, 2, 256)
+    assert _route(ok, X=None) == B.MOE_EINVAL
+    assert _route(ok, logits=MISALIGNED) == B.MOE_EINVAL
+    assert _route(ok, bias=MISALIGNED) == B.MOE_EINVAL
+    assert _route(ok, ws=None) == B.MOE_EINVAL
+    assert _route(ok, ws_bytes=16) == B.MOE_ENOSPACE
+    assert _route(B.make_shape(64, 256, 4, 5, 256)) == B.MOE_EINVAL          # k > E
+    assert _route(B.make_shape(64, 0, 8, 2, 256)) == B.MOE_EINVAL            # d <= 0
+    assert _route(B.make_shape(-1, 256, 8, 2, 256)) == B.MOE_EINVAL          # T < 0
+    assert _route(B.make_shape(64, 192, 8, 2, 256)) == B.MOE_EUNSUPPORTED    # d % 256
+    assert _route(B.make_shape(64, 256, 32, 17, 256)) == B.MOE_EUNSUPPORTED  # k > 16
+    assert _route(B.make_shape(64, 256, 8, 2, 320)) == B.MOE_EUNSUPPORTED    # f % 256
+    assert _route(B.make_shape(1 << 28, 256, 64, 16, 256)) == B.MOE_EUNSUPPORTED  # T*k >= 2^31
+    assert B.lib().moe_route(None, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, 1 << 40, None) \
+        == B.MOE_EINVAL
+
+
+def test_plan_forward_backward_validation():
+    L = B.lib()
+    sh = B.make_shape(64, 256, 8, 2, 256)
+    plan = B.MoePlanBufs(FAKE, FAKE, FAKE, FAKE)
+    bad_plan = B.MoePlanBufs(FAKE, None, FAKE, FAKE)
+    big = 1 << 40
+    assert L.moe_plan(ctypes.byref(sh), FAKE, ctypes.byref(bad_plan), FAKE, big, None) == B.MOE_EINVAL
+    assert L.moe_plan(ctypes.byref(sh), FAKE, ctypes.byref(plan), FAKE, 8, None) == B.MOE_ENOSPACE
+    assert L.moe_plan(ctypes.byref(sh), None, ctypes.byref(plan), FAKE, big, None) == B.MOE_EINVAL
+    assert L.moe_dispatch(ctypes.byref(sh), FAKE, ctypes.byref(plan), None, None) == B.MOE_EINVAL
+
+    w = B.MoeWeights(FAKE, FAKE, FAKE, None, None, None)
+    w_shared_extra = B.MoeWeights(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+    assert L.moe_forward(ctypes.byref(sh), FAKE, ctypes.byref(w_shared_extra), FAKE, FAKE,
+                         ctypes.byref(plan), FAKE, 1, FAKE, big, None) == B.MOE_EINVAL
+    sh_s = B.make_shape(64, 256, 8, 2, 256, 256)
+    assert L.moe_forward(ctypes.byref(sh_s), FAKE, ctypes.byref(w), FAKE, FAKE,
+                         ctypes.byref(plan), FAKE, 1, FAKE, big, None) == B.MOE_EINVAL
+    assert L.moe_forward(ctypes.byref(sh), FAKE, ctypes.byref(w), FAKE, FAKE,
+                         ctypes.byref(plan), FAKE, 1, FAKE, 64, None) == B.MOE_ENOSPACE
+    fwd_bytes = B.moe_workspace_bytes(sh, False)
+    g = B.MoeGrads(FAKE, FAKE, FAKE, FAKE, None, None, None, None)
+    # backward needs the larger workspace
+    assert L.moe_backward(ctypes.byref(sh), FAKE, FAKE, FAKE, ctypes.byref(w), FAKE, FAKE,
+                          ctypes.byref(plan), FAKE, ctypes.byref(g), FAKE, fwd_bytes,
+                          None) == B.MOE_ENOSPACE
+    g_bad = B.MoeGrads(FAKE, FAKE, None, FAKE, None, None, None, None)
+    assert L.moe_backward(ctypes.byref(sh), FAKE, FAKE, FAKE, ctypes.byref(w), FAKE, FAKE,
+                          ctypes.byref(plan), FAKE, ctypes.byref(g_bad), FAKE, big,
+                          None) == B.MOE_EINVAL
+    assert L.moe_backward(ctypes.byref(sh), FAKE, FAKE, FAKE, ctypes.byref(w), FAKE, FAKE,
+                          ctypes.byref(plan), MISALIGNED, ctypes.byref(g), FAKE, big,
+                          None) == B.MOE_EINVAL
+
+
+def test_oracle_is_not_imported_by_the_package():
+    import sys
+    import importlib
+    for mod in ("paper_2609_36070_amd", "paper_2609_36070_amd.binding",
+                "paper_2609_36070_amd.layer", "paper_2609_36070_amd.workloads"):
+        importlib.import_module(mod)
+    pkg_dir = os.path.dirname(B.__file__)
+    for fn in os.listdir(pkg_dir):
+        if fn.endswith(".py"):
+            src = open(os.path.join(pkg_dir, fn)).read()
+            assert "import oracle" not in src and "from oracle" not in src, fn
