@@ -1,0 +1,248 @@
+"""Benchmark one pass of the MoE-layer hot path on one MI355X.
+
+A step is route -> plan -> forward -> backward (training workload) over one
+batch of seeded synthetic input already resident in HBM.  Prints ONE JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+Throughput follows the paper's accounting (§4.1): forward FLOPs
+6*T*(k*f + f_shared)*d, backward twice that.  Per-stage times come from HIP
+events the library records on the stream the kernels run on.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MoE layer fwd+bwd TFLOP/s and tokens/s on 1 MI355X; % of bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class HipEvents:
+    """Minimal hipEvent API through ctypes (the library records them itself)."""
+
+    def __init__(self):
+        self.h = ctypes.CDLL("libamdhip64.so")
+        self.h.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.h.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                               ctypes.c_void_p]
+        self.h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self):
+        e = ctypes.c_void_p()
+        assert self.h.hipEventCreate(ctypes.byref(e)) == 0
+        return e.value
+
+    def record(self, e, stream):
+        assert self.h.hipEventRecord(e, stream) == 0
+
+    def ms(self, a, b):
+        out = ctypes.c_float()
+        assert self.h.hipEventElapsedTime(ctypes.byref(out), a, b) == 0
+        return out.value
+
+    def sync(self, e):
+        assert self.h.hipEventSynchronize(e) == 0
+
+    def destroy(self, e):
+        self.h.hipEventDestroy(e)
+
+
+def stage_flops(w):
+    """Algorithmic FLOPs of each timed stage and launches per stage."""
+    R, d, f, fs, T = w.T * w.k, w.d, w.f, w.f_s, w.T
+    fwd = {"up_routed": (4.0 * R * d * f, 1), "up_shared": (4.0 * T * d * fs, 1),
+           "down_routed": (2.0 * R * f * d, 1), "down_shared": (2.0 * T * fs * d, 1)}
+    bwd = {"dgrad_routed": (2.0 * R * d * f, 1), "dx_routed": (4.0 * R * f * d, 1),
+           "wgrad_gate_up": (4.0 * R * d * f, 2), "wgrad_down": (2.0 * R * f * d, 1),
+           "dgrad_shared": (2.0 * T * d * fs, 1), "dx_shared": (4.0 * T * fs * d, 1),
+           "wgrad_shared": (6.0 * T * d * fs, 3)}
+    return fwd, bwd
+
+
+def cpu_baseline(w, inputs, sample_tokens):
+    """Time the CPU oracle on the first `sample_tokens` tokens of the workload."""
+    import numpy as np
+    from oracle import moe_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = len(os.sched_getaffinity(0))
+    n = min(sample_tokens, w.T)
+    X = inputs["X"][:n]
+    W = {key: inputs.get(key) for key in ("W_gate", "W_up", "W_down", "Wg_s", "Wu_s", "Wd_s")}
+    t0 = time.perf_counter()
+    Z = O.router_logits(X, inputs["W_r"], inputs.get("bias"))
+    idx = O.topk_select(Z, w.k)
+    wts = O.gate_weights(Z, idx)
+    O.plan(idx, w.E)
+    O.moe_forward(X, W, idx, wts)
+    flops = w.scaled(T=n).fwd_flops()
+    if w.backward:
+        O.moe_backward(X, inputs["W_r"], W, idx, wts, inputs["dY"][:n])
+        flops += w.scaled(T=n).bwd_flops()
+    dt = time.perf_counter() - t0
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {n} of {w.T} tokens, all {w.k} routes each, full weights; "
+                      f"route+plan+forward{'+backward' if w.backward else ''} in fp64 numpy; "
+                      f"{dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="large_shared_train")
+    ap.add_argument("--cpu-sample-tokens", type=int, default=512)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no "
+              f"multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_36070_amd import binding as B
+    from paper_2609_36070_amd.layer import DeviceLayer
+    from paper_2609_36070_amd.workloads import WORKLOADS, make_inputs
+
+    w = WORKLOADS[args.workload]
+    log(f"[bench] workload {w.name}: T={w.T} d={w.d} E={w.E} k={w.k} f={w.f} f_s={w.f_s} "
+        f"backward={w.backward}")
+    t_in = time.perf_counter()
+    inputs = make_inputs(w, seed=0)
+    log(f"[bench] inputs drawn in {time.perf_counter() - t_in:.1f} s")
+    L = DeviceLayer(w, inputs)
+    stream = torch.cuda.current_stream().cuda_stream
+    H = HipEvents()
+
+    for i in range(args.warmup):
+        L.step()
+    torch.cuda.synchronize()
+    log(f"[bench] {args.warmup} warm-up steps done")
+
+    nf, nb = len(B.FWD_STAGES) + 1, len(B.BWD_STAGES) + 1
+    per_step = []
+    for _ in range(args.steps):
+        ev = {"route": H.create(), "plan": H.create(),
+              "fwd": [H.create() for _ in range(nf)],
+              "bwd": [H.create() for _ in range(nb)] if w.backward else [],
+              "end": H.create()}
+        per_step.append(ev)
+    t_start, t_stop = H.create(), H.create()
+
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    H.record(t_start, stream)
+    for ev in per_step:
+        fe = B.MoeStageEvents()
+        for i, e in enumerate(ev["fwd"]):
+            fe.ev[i] = e
+        be = None
+        if w.backward:
+            be = B.MoeStageEvents()
+            for i, e in enumerate(ev["bwd"]):
+                be.ev[i] = e
+        H.record(ev["route"], stream)
+        L.route()
+        H.record(ev["plan"], stream)
+        L.plan()
+        L.forward(events=fe)
+        if w.backward:
+            L.backward(events=be)
+        H.record(ev["end"], stream)
+    H.record(t_stop, stream)
+    H.sync(t_stop)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_total = H.ms(t_start, t_stop)
+    ms_step = ms_total / args.steps
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step (events), wall {1e3 * wall / args.steps:.3f}")
+
+    # per-stage averages
+    stages = {"route": 0.0, "plan": 0.0}
+    for ev in per_step:
+        stages["route"] += H.ms(ev["route"], ev["plan"])
+        stages["plan"] += H.ms(ev["plan"], ev["fwd"][0])
+        for i, name in enumerate(B.FWD_STAGES):
+            stages["fwd." + name] = stages.get("fwd." + name, 0.0) + H.ms(ev["fwd"][i], ev["fwd"][i + 1])
+        if w.backward:
+            for i, name in enumerate(B.BWD_STAGES):
+                stages["bwd." + name] = stages.get("bwd." + name, 0.0) + H.ms(ev["bwd"][i], ev["bwd"][i + 1])
+    stages = {k: v / args.steps for k, v in stages.items()}
+
+    fwd_fl, bwd_fl = stage_flops(w)
+    # kernels that run as exactly one instance per launch shape, with their FLOPs per launch
+    kern = {
+        "gemm up/gate+SwiGLU (routed)": (stages["fwd.up_routed"], 1, fwd_fl["up_routed"][0]),
+        "gemm down (routed)": (stages["fwd.down_routed"], 1, fwd_fl["down_routed"][0]),
+    }
+    if w.backward:
+        kern["gemm dgrad+SwiGLU bwd (routed)"] = (stages["bwd.dgrad_routed"], 1,
+                                                  bwd_fl["dgrad_routed"][0])
+        kern["gemm dX (routed)"] = (stages["bwd.dx_routed"], 1, bwd_fl["dx_routed"][0])
+        kern["gemm weight grad (routed)"] = (stages["bwd.wgrad_gate_up"] + stages["bwd.wgrad_down"],
+                                             3, 2.0 * w.T * w.k * w.d * w.f)
+    dom = max(kern, key=lambda k: kern[k][0])
+    t_ms, n_launch, fl = kern[dom]
+    avg_ms = t_ms / n_launch
+    achieved = fl / (avg_ms * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "avg_launch_ms": round(avg_ms, 4), "flops_per_launch": fl}
+
+    step_flops = w.fwd_flops() + (w.bwd_flops() if w.backward else 0.0)
+    value = step_flops / (ms_step * 1e-3) / 1e12
+    stage_report = {}
+    for name, ms in stages.items():
+        key = name.split(".", 1)[-1]
+        fl = (fwd_fl if name.startswith("fwd.") else bwd_fl).get(key, (0.0, 1))[0] \
+            if "." in name else 0.0
+        stage_report[name] = {"ms": round(ms, 4)}
+        if fl:
+            stage_report[name]["tflops"] = round(fl / (ms * 1e-3) / 1e12, 1) if ms > 0 else None
+    for name, v in stage_report.items():
+        log(f"   {name:28s} {v['ms']:9.4f} ms  {v.get('tflops', '')}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a token sample ...")
+        cpu = cpu_baseline(w, inputs, args.cpu_sample_tokens)
+        log(f"[bench] cpu baseline {cpu}")
+
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "T": w.T, "d": w.d, "E": w.E, "k": w.k, "f": w.f,
+                   "f_shared": w.f_s, "passes": "fwd+bwd" if w.backward else "fwd",
+                   "step": "route+plan+forward" + ("+backward" if w.backward else "")},
+        "tokens_per_s": round(w.T / (ms_step * 1e-3), 1),
+        "frac_of_bf16_peak": round(value / PEAK_BF16_TFLOPS, 4),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "stages": stage_report,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

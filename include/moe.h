@@ -113,6 +113,24 @@ typedef enum {
     MOE_WS_COUNT = 10
 } moe_ws_tensor;
 
+/* Optional per-stage timing.  When a moe_stage_events pointer is passed to
+ * moe_forward / moe_backward, ev[i] (a hipEvent_t, or NULL to skip) is
+ * recorded on the stream just before stage i is enqueued and ev[n] after the
+ * last stage, so the elapsed time between ev[i] and ev[i+1] is stage i.
+ * Stages that do not apply (no shared expert) still record their events.
+ *   forward  (n = 6): 0 plan-order prologue, 1 routed up/gate + SwiGLU,
+ *                     2 shared up/gate + SwiGLU, 3 routed down, 4 shared down,
+ *                     5 combine.
+ *   backward (n = 11): 0 prologue, 1 routed dgrad + SwiGLU backward,
+ *                     2 softmax backward, 3 routed dX GEMM, 4 routed dW_gate
+ *                     and dW_up, 5 routed dW_down, 6 shared dgrad, 7 shared
+ *                     dX GEMM, 8 shared weight gradients, 9 dW_r,
+ *                     10 reverse combine. */
+#define MOE_MAX_STAGE_EVENTS 16
+typedef struct {
+    void *ev[MOE_MAX_STAGE_EVENTS];
+} moe_stage_events;
+
 /* Workspace bytes needed by moe_route/moe_plan/moe_forward (with_backward=0)
  * or additionally moe_backward (with_backward=1).  Pure host function;
  * returns 0 for an invalid or unsupported shape. */
@@ -159,7 +177,8 @@ moe_status moe_dispatch(const moe_shape *shape, const moe_bf16 *X,
 moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
                        const int32_t *topk_idx, const float *topk_w,
                        const moe_plan_bufs *plan, moe_bf16 *Y, int save_for_backward,
-                       void *ws, size_t ws_bytes, moe_stream stream);
+                       void *ws, size_t ws_bytes, moe_stream stream,
+                       const moe_stage_events *events /* NULL = no timing */);
 
 /* Backward of the layer for upstream gradient dY [T, d] bf16, with the
  * selection held fixed.  Needs the same ws as a preceding moe_forward with
@@ -171,7 +190,8 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
                         const moe_bf16 *W_r, const moe_weights *weights,
                         const int32_t *topk_idx, const float *topk_w,
                         const moe_plan_bufs *plan, moe_bf16 *dX, const moe_grads *grads,
-                        void *ws, size_t ws_bytes, moe_stream stream);
+                        void *ws, size_t ws_bytes, moe_stream stream,
+                        const moe_stage_events *events /* NULL = no timing */);
 
 /* Static strings; never NULL. */
 const char *moe_status_string(moe_status status);

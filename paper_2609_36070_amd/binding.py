@@ -43,6 +43,17 @@ class MoeGrads(ctypes.Structure):
                                         "dWg_s", "dWu_s", "dWd_s")]
 
 
+MAX_STAGE_EVENTS = 16
+FWD_STAGES = ("prologue", "up_routed", "up_shared", "down_routed", "down_shared", "combine")
+BWD_STAGES = ("prologue", "dgrad_routed", "softmax_bwd", "dx_routed", "wgrad_gate_up",
+              "wgrad_down", "dgrad_shared", "dx_shared", "wgrad_shared", "dw_router",
+              "reverse_combine")
+
+
+class MoeStageEvents(ctypes.Structure):
+    _fields_ = [("ev", c_void_p * MAX_STAGE_EVENTS)]
+
+
 class MoeError(RuntimeError):
     def __init__(self, fn, status):
         super().__init__(f"{fn} failed: {status_string(status)} ({status})")
@@ -68,10 +79,11 @@ def lib():
         L.moe_plan.argtypes = [P(MoeShape), c_void_p, P(MoePlanBufs), c_void_p, c_size_t, c_void_p]
         L.moe_dispatch.argtypes = [P(MoeShape), c_void_p, P(MoePlanBufs), c_void_p, c_void_p]
         L.moe_forward.argtypes = [P(MoeShape), c_void_p, P(MoeWeights), c_void_p, c_void_p,
-                                  P(MoePlanBufs), c_void_p, c_int, c_void_p, c_size_t, c_void_p]
+                                  P(MoePlanBufs), c_void_p, c_int, c_void_p, c_size_t, c_void_p,
+                                  P(MoeStageEvents)]
         L.moe_backward.argtypes = [P(MoeShape), c_void_p, c_void_p, c_void_p, P(MoeWeights),
                                    c_void_p, c_void_p, P(MoePlanBufs), c_void_p, P(MoeGrads),
-                                   c_void_p, c_size_t, c_void_p]
+                                   c_void_p, c_size_t, c_void_p, P(MoeStageEvents)]
         for fn in ("moe_route", "moe_plan", "moe_dispatch", "moe_forward", "moe_backward",
                    "moe_workspace_region"):
             getattr(L, fn).restype = c_int
@@ -97,6 +109,9 @@ def _p(t):
         return None
     if isinstance(t, int):
         return t
+    if t.numel() == 0:
+        # torch reports NULL for empty tensors; pass the (non-empty) storage instead
+        return t.untyped_storage().data_ptr()
     return t.data_ptr()
 
 
@@ -166,18 +181,22 @@ def moe_dispatch(shape, X, plan: MoePlanBufs, Xperm, stream=None, raise_on_error
 
 
 def moe_forward(shape, X, weights: MoeWeights, topk_idx, topk_w, plan: MoePlanBufs, Y,
-                save_for_backward, ws, ws_bytes=None, stream=None, raise_on_error=True):
+                save_for_backward, ws, ws_bytes=None, stream=None, raise_on_error=True,
+                events: MoeStageEvents = None):
     nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
     st = lib().moe_forward(ctypes.byref(shape), _p(X), ctypes.byref(weights), _p(topk_idx),
                            _p(topk_w), ctypes.byref(plan), _p(Y), int(bool(save_for_backward)),
-                           _p(ws), nbytes, _stream(stream))
+                           _p(ws), nbytes, _stream(stream),
+                           None if events is None else ctypes.byref(events))
     return _check("moe_forward", st, raise_on_error)
 
 
 def moe_backward(shape, dY, X, W_r, weights: MoeWeights, topk_idx, topk_w, plan: MoePlanBufs, dX,
-                 grads: MoeGrads, ws, ws_bytes=None, stream=None, raise_on_error=True):
+                 grads: MoeGrads, ws, ws_bytes=None, stream=None, raise_on_error=True,
+                 events: MoeStageEvents = None):
     nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
     st = lib().moe_backward(ctypes.byref(shape), _p(dY), _p(X), _p(W_r), ctypes.byref(weights),
                             _p(topk_idx), _p(topk_w), ctypes.byref(plan), _p(dX),
-                            ctypes.byref(grads), _p(ws), nbytes, _stream(stream))
+                            ctypes.byref(grads), _p(ws), nbytes, _stream(stream),
+                            None if events is None else ctypes.byref(events))
     return _check("moe_backward", st, raise_on_error)

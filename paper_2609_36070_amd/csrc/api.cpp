@@ -111,6 +111,16 @@ moe_status check_ws(const moe_shape *s, const void *ws, size_t ws_bytes, int wit
 template <typename T>
 T *at(void *ws, size_t off) { return reinterpret_cast<T *>(static_cast<char *>(ws) + off); }
 
+// Records stage event i (if requested) on the stream.
+struct StageMarks {
+    const moe_stage_events *ev;
+    hipStream_t s;
+    hipError_t mark(int i) const {
+        if (!ev || i >= MOE_MAX_STAGE_EVENTS || !ev->ev[i]) return hipSuccess;
+        return hipEventRecord(static_cast<hipEvent_t>(ev->ev[i]), s);
+    }
+};
+
 #define MOE_TRY(expr)                                      \
     do {                                                   \
         if ((expr) != hipSuccess) return MOE_EHIP;         \
@@ -198,7 +208,7 @@ moe_status moe_dispatch(const moe_shape *shape, const moe_bf16 *X, const moe_pla
 moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
                        const int32_t *topk_idx, const float *topk_w, const moe_plan_bufs *plan,
                        moe_bf16 *Y, int save_for_backward, void *ws, size_t ws_bytes,
-                       moe_stream stream) {
+                       moe_stream stream, const moe_stage_events *events) {
     moe_status st = check_shape(shape);
     if (st != MOE_OK) return st;
     if (!ptr_ok(X) || !ptr_ok(topk_idx) || !ptr_ok(topk_w) || !ptr_ok(Y)) return MOE_EINVAL;
@@ -213,8 +223,11 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
     int *rowidx = at<int>(ws, L.rowidx);
     float *wperm = at<float>(ws, L.wperm);
     uint16_t *H = at<uint16_t>(ws, L.H);
+    const StageMarks mk{events, s};
 
+    MOE_TRY(mk.mark(0));
     MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, rowidx, wperm, s));
+    MOE_TRY(mk.mark(1));
     {   // routed up/gate + SwiGLU
         GemmArgs g;
         g.A = X; g.lda = d; g.a_rows = rowidx; g.a_nrows = T > 0 ? T : 1;
@@ -224,6 +237,7 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
         if (save_for_backward) { g.C2 = at<uint16_t>(ws, L.A); g.C3 = at<uint16_t>(ws, L.B); }
         MOE_TRY(launch_gemm_fwd_up(g, R, E, s));
     }
+    MOE_TRY(mk.mark(2));
     if (fs > 0) {   // shared up/gate + SwiGLU
         GemmArgs g;
         g.A = X; g.lda = d; g.a_nrows = T > 0 ? T : 1; g.M = T;
@@ -233,6 +247,7 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
         if (save_for_backward) { g.C2 = at<uint16_t>(ws, L.As); g.C3 = at<uint16_t>(ws, L.Bs); }
         MOE_TRY(launch_gemm_fwd_up(g, T, 1, s));
     }
+    MOE_TRY(mk.mark(3));
     {   // routed down
         GemmArgs g;
         g.A = H; g.lda = f; g.a_nrows = R > 0 ? (int)R : 1;
@@ -241,6 +256,7 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
         g.C = at<uint16_t>(ws, L.Yexp); g.ldc = d;
         MOE_TRY(launch_gemm_fwd_down(g, R, E, s));
     }
+    MOE_TRY(mk.mark(4));
     if (fs > 0) {   // shared down
         GemmArgs g;
         g.A = at<uint16_t>(ws, L.Hs); g.lda = fs; g.a_nrows = T > 0 ? T : 1; g.M = T;
@@ -249,15 +265,18 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
         g.C = at<uint16_t>(ws, L.Ysh); g.ldc = d;
         MOE_TRY(launch_gemm_fwd_down(g, T, 1, s));
     }
+    MOE_TRY(mk.mark(5));
     MOE_TRY(launch_combine(at<uint16_t>(ws, L.Yexp), fs > 0 ? at<uint16_t>(ws, L.Ysh) : nullptr,
                            topk_w, plan->route_pos, T, d, k, Y, s));
+    MOE_TRY(mk.mark(6));
     return MOE_OK;
 }
 
 moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf16 *X,
                         const moe_bf16 *W_r, const moe_weights *weights, const int32_t *topk_idx,
                         const float *topk_w, const moe_plan_bufs *plan, moe_bf16 *dX,
-                        const moe_grads *grads, void *ws, size_t ws_bytes, moe_stream stream) {
+                        const moe_grads *grads, void *ws, size_t ws_bytes, moe_stream stream,
+                        const moe_stage_events *events) {
     moe_status st = check_shape(shape);
     if (st != MOE_OK) return st;
     if (!ptr_ok(dY) || !ptr_ok(X) || !ptr_ok(W_r) || !ptr_ok(topk_idx) || !ptr_ok(topk_w) ||
@@ -287,8 +306,11 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
     uint16_t *dA = at<uint16_t>(ws, L.dA), *dB = at<uint16_t>(ws, L.dB);
     float *dgpart = at<float>(ws, L.dgpart);
     float *dZ = grads->dZ ? grads->dZ : at<float>(ws, L.dZ);
+    const StageMarks mk{events, s};
 
+    MOE_TRY(mk.mark(0));
     MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, rowidx, wperm, s));
+    MOE_TRY(mk.mark(1));
     {   // dh' = dY W_down^T with SwiGLU backward and dg partials
         GemmArgs g;
         g.A = dY; g.lda = d; g.a_rows = rowidx; g.a_nrows = Tn;
@@ -298,8 +320,10 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
         g.rowscale = wperm; g.C = dA; g.C2 = dB; g.dgpart = dgpart; g.dg_ld = L.dg_parts;
         MOE_TRY(launch_gemm_bwd_dgrad(g, R, E, s));
     }
+    MOE_TRY(mk.mark(2));
     MOE_TRY(launch_softmax_bwd(dgpart, L.dg_parts, plan->route_pos, topk_w, topk_idx, T, k, E,
                                at<float>(ws, L.dg), dZ, s));
+    MOE_TRY(mk.mark(3));
     {   // dXperm = dA W_gate^T + dB W_up^T
         GemmArgs g;
         g.A = dA; g.A2 = dB; g.lda = f; g.a_nrows = Rn;
@@ -308,6 +332,7 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
         g.C = at<uint16_t>(ws, L.dXperm); g.ldc = d;
         MOE_TRY(launch_gemm_bwd_dx(g, R, E, s));
     }
+    MOE_TRY(mk.mark(4));
     {   // dW_gate[e] = Xperm_e^T dA_e, dW_up[e] = Xperm_e^T dB_e
         GemmArgs g;
         g.A = X; g.lda = d; g.a_rows = rowidx; g.a_nrows = Tn;
@@ -318,6 +343,7 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
         g.B = dB; g.Cf = grads->dW_up;
         MOE_TRY(launch_gemm_wgrad(g, E, s));
     }
+    MOE_TRY(mk.mark(5));
     {   // dW_down[e] = (w H_e)^T dYperm_e
         GemmArgs g;
         g.A = at<uint16_t>(ws, L.H); g.lda = f; g.a_nrows = Rn; g.a_kscale = wperm;
@@ -326,6 +352,7 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
         g.Cf = grads->dW_down; g.c_estride = (long)f * d; g.ldc = d;
         MOE_TRY(launch_gemm_wgrad(g, E, s));
     }
+    MOE_TRY(mk.mark(6));
     uint16_t *dXsh = nullptr;
     if (shared) {
         uint16_t *dAs = at<uint16_t>(ws, L.dAs), *dBs = at<uint16_t>(ws, L.dBs);
@@ -339,6 +366,7 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
             g.C = dAs; g.C2 = dBs;
             MOE_TRY(launch_gemm_bwd_dgrad(g, T, 1, s));
         }
+        MOE_TRY(mk.mark(7));
         {
             GemmArgs g;
             g.A = dAs; g.A2 = dBs; g.lda = fs; g.a_nrows = Tn; g.M = T;
@@ -347,6 +375,7 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
             g.C = dXsh; g.ldc = d;
             MOE_TRY(launch_gemm_bwd_dx(g, T, 1, s));
         }
+        MOE_TRY(mk.mark(8));
         {
             GemmArgs g;
             g.A = X; g.lda = d; g.a_nrows = Tn;
@@ -365,10 +394,16 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
             g.Cf = grads->dWd_s; g.ldc = d;
             MOE_TRY(launch_gemm_wgrad(g, 1, s));
         }
+    } else {
+        MOE_TRY(mk.mark(7));
+        MOE_TRY(mk.mark(8));
     }
+    MOE_TRY(mk.mark(9));
     MOE_TRY(launch_dwr(X, dZ, T, d, E, at<float>(ws, L.dwr_part), grads->dW_r, s));
+    MOE_TRY(mk.mark(10));
     MOE_TRY(launch_reverse_combine(at<uint16_t>(ws, L.dXperm), dXsh, dZ, W_r, plan->route_pos, T, d,
                                    k, E, dX, s));
+    MOE_TRY(mk.mark(11));
     return MOE_OK;
 }
 

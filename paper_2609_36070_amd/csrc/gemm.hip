@@ -67,7 +67,7 @@ struct Traits {
     static constexpr bool GROUPED_ROWS = (MODE != WGRAD);
 };
 
-template <int MODE>
+template <int MODE, bool GROUPED>
 __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g) {
     using Tr = Traits<MODE>;
     __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][TILE_ELEMS];  // [stage][A/B]
@@ -85,7 +85,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g) {
         ntile = blockIdx.x % ntn;
         const int mt = blockIdx.x / ntn;
         n0 = ntile * ((MODE == FWD_UP) ? BN / 2 : BN);
-        if (g.offsets) {
+        if constexpr (GROUPED) {
             if (tid == 0) s_info[0] = -1;
             __syncthreads();
             if (tid < 64) {
@@ -126,7 +126,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g) {
         m0 = (rest % ntm) * BM;
         e = rest / ntm;
         n0 = ntile * BN;
-        if (g.offsets) {
+        if constexpr (GROUPED) {
             kbeg = g.offsets[e];
             klen = g.offsets[e + 1] - kbeg;
         } else {
@@ -415,7 +415,10 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g) {
 template <int MODE>
 hipError_t launch_mode(const GemmArgs &g, unsigned grid, hipStream_t st) {
     if (grid == 0) return hipSuccess;
-    gemm_kernel<MODE><<<dim3(grid), dim3(NTHREADS), 0, st>>>(g);
+    if (g.offsets)
+        gemm_kernel<MODE, true><<<dim3(grid), dim3(NTHREADS), 0, st>>>(g);
+    else
+        gemm_kernel<MODE, false><<<dim3(grid), dim3(NTHREADS), 0, st>>>(g);
     return hipGetLastError();
 }
 

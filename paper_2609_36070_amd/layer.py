@@ -91,22 +91,23 @@ class DeviceLayer:
     def plan(self, stream=None):
         B.moe_plan(self.shape, self.topk_idx, self.plan_bufs, self.ws, stream=stream)
 
-    def forward(self, save_for_backward=None, stream=None):
+    def forward(self, save_for_backward=None, stream=None, events=None):
         save = self.with_backward if save_for_backward is None else save_for_backward
         B.moe_forward(self.shape, self.X, self.weights, self.topk_idx, self.topk_w,
-                      self.plan_bufs, self.Y, save, self.ws, stream=stream)
+                      self.plan_bufs, self.Y, save, self.ws, stream=stream, events=events)
 
-    def backward(self, stream=None):
+    def backward(self, stream=None, events=None):
         B.moe_backward(self.shape, self.dY, self.X, self.W_r, self.weights, self.topk_idx,
-                       self.topk_w, self.plan_bufs, self.dX, self.grads, self.ws, stream=stream)
+                       self.topk_w, self.plan_bufs, self.dX, self.grads, self.ws, stream=stream,
+                       events=events)
 
-    def step(self, stream=None):
+    def step(self, stream=None, fwd_events=None, bwd_events=None):
         """One pass of the whole path: route, plan, forward (and backward)."""
         self.route(stream)
         self.plan(stream)
-        self.forward(stream=stream)
+        self.forward(stream=stream, events=fwd_events)
         if self.with_backward:
-            self.backward(stream)
+            self.backward(stream, events=bwd_events)
 
     # -- inspection -------------------------------------------------------
     def ws_tensor(self, which, dtype, shape):

@@ -102,25 +102,25 @@ def test_plan_forward_backward_validation():
     w = B.MoeWeights(FAKE, FAKE, FAKE, None, None, None)
     w_shared_extra = B.MoeWeights(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
     assert L.moe_forward(ctypes.byref(sh), FAKE, ctypes.byref(w_shared_extra), FAKE, FAKE,
-                         ctypes.byref(plan), FAKE, 1, FAKE, big, None) == B.MOE_EINVAL
+                         ctypes.byref(plan), FAKE, 1, FAKE, big, None, None) == B.MOE_EINVAL
     sh_s = B.make_shape(64, 256, 8, 2, 256, 256)
     assert L.moe_forward(ctypes.byref(sh_s), FAKE, ctypes.byref(w), FAKE, FAKE,
-                         ctypes.byref(plan), FAKE, 1, FAKE, big, None) == B.MOE_EINVAL
+                         ctypes.byref(plan), FAKE, 1, FAKE, big, None, None) == B.MOE_EINVAL
     assert L.moe_forward(ctypes.byref(sh), FAKE, ctypes.byref(w), FAKE, FAKE,
-                         ctypes.byref(plan), FAKE, 1, FAKE, 64, None) == B.MOE_ENOSPACE
+                         ctypes.byref(plan), FAKE, 1, FAKE, 64, None, None) == B.MOE_ENOSPACE
     fwd_bytes = B.moe_workspace_bytes(sh, False)
     g = B.MoeGrads(FAKE, FAKE, FAKE, FAKE, None, None, None, None)
     # backward needs the larger workspace
     assert L.moe_backward(ctypes.byref(sh), FAKE, FAKE, FAKE, ctypes.byref(w), FAKE, FAKE,
                           ctypes.byref(plan), FAKE, ctypes.byref(g), FAKE, fwd_bytes,
-                          None) == B.MOE_ENOSPACE
+                          None, None) == B.MOE_ENOSPACE
     g_bad = B.MoeGrads(FAKE, FAKE, None, FAKE, None, None, None, None)
     assert L.moe_backward(ctypes.byref(sh), FAKE, FAKE, FAKE, ctypes.byref(w), FAKE, FAKE,
                           ctypes.byref(plan), FAKE, ctypes.byref(g_bad), FAKE, big,
-                          None) == B.MOE_EINVAL
+                          None, None) == B.MOE_EINVAL
     assert L.moe_backward(ctypes.byref(sh), FAKE, FAKE, FAKE, ctypes.byref(w), FAKE, FAKE,
                           ctypes.byref(plan), MISALIGNED, ctypes.byref(g), FAKE, big,
-                          None) == B.MOE_EINVAL
+                          None, None) == B.MOE_EINVAL
 
 
 def test_oracle_is_not_imported_by_the_package():
