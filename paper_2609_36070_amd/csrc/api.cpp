@@ -17,10 +17,10 @@ size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 // Byte offsets of every workspace region; depends only on the shape.
 struct Layout {
-    size_t err, blockcounts, blockbase, blockflags, wrt, rowidx, wperm;
+    size_t err, blockcounts, blockbase, blockflags, wrt, rowidx, wperm, zeros;
     size_t A, B, H, Yexp, As, Bs, Hs, Ysh;
     size_t fwd_total;
-    size_t dA, dB, dgpart, dg, dZ, dXperm, dAs, dBs, dXsh, dwr_part;
+    size_t dA, dB, Hw, dgpart, dg, dZ, dXperm, dAs, dBs, dXsh, dwr_part;
     size_t bwd_total;
     int dg_parts;
 };
@@ -40,6 +40,7 @@ Layout make_layout(const moe_shape &s) {
     L.wrt = take(epad * d * 2);
     L.rowidx = take(R * 4);
     L.wperm = take(R * 4);
+    L.zeros = take(ZERO_PAGE_ELEMS * 2);
     L.A = take(R * f * 2);
     L.B = take(R * f * 2);
     L.H = take(R * f * 2);
@@ -51,6 +52,7 @@ Layout make_layout(const moe_shape &s) {
     L.fwd_total = o;
     L.dg_parts = (int)(f / (size_t)gemm_tile_n());
     L.dA = take(R * f * 2);
+    L.Hw = take(R * f * 2);
     L.dB = take(R * f * 2);
     L.dgpart = take(R * (size_t)L.dg_parts * 4);
     L.dg = take(R * 4);
@@ -226,10 +228,12 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
     const StageMarks mk{events, s};
 
     MOE_TRY(mk.mark(0));
-    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, rowidx, wperm, s));
+    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, rowidx, wperm,
+                        at<uint16_t>(ws, L.zeros), s));
     MOE_TRY(mk.mark(1));
     {   // routed up/gate + SwiGLU
         GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
         g.A = X; g.lda = d; g.a_rows = rowidx; g.a_nrows = T > 0 ? T : 1;
         g.B = weights->W_gate; g.B2 = weights->W_up; g.ldb = f; g.b_estride = (long)d * f;
         g.N = f; g.K = d; g.offsets = plan->offsets; g.E = E;
@@ -240,6 +244,7 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
     MOE_TRY(mk.mark(2));
     if (fs > 0) {   // shared up/gate + SwiGLU
         GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
         g.A = X; g.lda = d; g.a_nrows = T > 0 ? T : 1; g.M = T;
         g.B = weights->Wg_s; g.B2 = weights->Wu_s; g.ldb = fs;
         g.N = fs; g.K = d;
@@ -250,6 +255,7 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
     MOE_TRY(mk.mark(3));
     {   // routed down
         GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
         g.A = H; g.lda = f; g.a_nrows = R > 0 ? (int)R : 1;
         g.B = weights->W_down; g.ldb = d; g.b_estride = (long)f * d;
         g.N = d; g.K = f; g.offsets = plan->offsets; g.E = E;
@@ -259,6 +265,7 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
     MOE_TRY(mk.mark(4));
     if (fs > 0) {   // shared down
         GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
         g.A = at<uint16_t>(ws, L.Hs); g.lda = fs; g.a_nrows = T > 0 ? T : 1; g.M = T;
         g.B = weights->Wd_s; g.ldb = d;
         g.N = d; g.K = fs;
@@ -309,15 +316,18 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
     const StageMarks mk{events, s};
 
     MOE_TRY(mk.mark(0));
-    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, rowidx, wperm, s));
+    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, rowidx, wperm,
+                        at<uint16_t>(ws, L.zeros), s));
     MOE_TRY(mk.mark(1));
     {   // dh' = dY W_down^T with SwiGLU backward and dg partials
         GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
         g.A = dY; g.lda = d; g.a_rows = rowidx; g.a_nrows = Tn;
         g.B = weights->W_down; g.ldb = d; g.b_estride = (long)f * d;
         g.N = f; g.K = d; g.offsets = plan->offsets; g.E = E;
         g.E1 = at<uint16_t>(ws, L.A); g.E2 = at<uint16_t>(ws, L.B); g.ldc = f;
-        g.rowscale = wperm; g.C = dA; g.C2 = dB; g.dgpart = dgpart; g.dg_ld = L.dg_parts;
+        g.rowscale = wperm; g.C = dA; g.C2 = dB; g.C3 = at<uint16_t>(ws, L.Hw);
+        g.dgpart = dgpart; g.dg_ld = L.dg_parts;
         MOE_TRY(launch_gemm_bwd_dgrad(g, R, E, s));
     }
     MOE_TRY(mk.mark(2));
@@ -326,6 +336,7 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
     MOE_TRY(mk.mark(3));
     {   // dXperm = dA W_gate^T + dB W_up^T
         GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
         g.A = dA; g.A2 = dB; g.lda = f; g.a_nrows = Rn;
         g.B = weights->W_gate; g.B2 = weights->W_up; g.ldb = f; g.b_estride = (long)d * f;
         g.N = d; g.K = f; g.offsets = plan->offsets; g.E = E;
@@ -335,6 +346,7 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
     MOE_TRY(mk.mark(4));
     {   // dW_gate[e] = Xperm_e^T dA_e, dW_up[e] = Xperm_e^T dB_e
         GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
         g.A = X; g.lda = d; g.a_rows = rowidx; g.a_nrows = Tn;
         g.B = dA; g.ldb = f; g.b_nrows = Rn;
         g.M = d; g.N = f; g.offsets = plan->offsets; g.E = E;
@@ -346,7 +358,8 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
     MOE_TRY(mk.mark(5));
     {   // dW_down[e] = (w H_e)^T dYperm_e
         GemmArgs g;
-        g.A = at<uint16_t>(ws, L.H); g.lda = f; g.a_nrows = Rn; g.a_kscale = wperm;
+        g.zeros = at<uint16_t>(ws, L.zeros);
+        g.A = at<uint16_t>(ws, L.Hw); g.lda = f; g.a_nrows = Rn;
         g.B = dY; g.ldb = d; g.b_rows = rowidx; g.b_nrows = Tn;
         g.M = f; g.N = d; g.offsets = plan->offsets; g.E = E;
         g.Cf = grads->dW_down; g.c_estride = (long)f * d; g.ldc = d;
@@ -359,6 +372,7 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
         dXsh = at<uint16_t>(ws, L.dXsh);
         {
             GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
             g.A = dY; g.lda = d; g.a_nrows = Tn; g.M = T;
             g.B = weights->Wd_s; g.ldb = d;
             g.N = fs; g.K = d;
@@ -369,6 +383,7 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
         MOE_TRY(mk.mark(7));
         {
             GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
             g.A = dAs; g.A2 = dBs; g.lda = fs; g.a_nrows = Tn; g.M = T;
             g.B = weights->Wg_s; g.B2 = weights->Wu_s; g.ldb = fs;
             g.N = d; g.K = fs;
@@ -378,6 +393,7 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
         MOE_TRY(mk.mark(8));
         {
             GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
             g.A = X; g.lda = d; g.a_nrows = Tn;
             g.B = dAs; g.ldb = fs; g.b_nrows = Tn;
             g.M = d; g.N = fs; g.K = T;
@@ -388,6 +404,7 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
         }
         {
             GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
             g.A = at<uint16_t>(ws, L.Hs); g.lda = fs; g.a_nrows = Tn;
             g.B = dY; g.ldb = d; g.b_nrows = Tn;
             g.M = fs; g.N = d; g.K = T;

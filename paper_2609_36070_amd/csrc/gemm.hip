@@ -10,7 +10,7 @@
 //              H = silu(A) * B                         (A, B kept for backward)
 //   FWD_DOWN   Yexp = H W_down[e]
 //   BWD_DGRAD  dh' = dY[tok(p)] W_down[e]^T, then dg partials <dh', h>,
-//              dA = w dh' * B * silu'(A), dB = w dh' * silu(A)
+//              dA = w dh' * B * silu'(A), dB = w dh' * silu(A), Hw = w * h
 //   BWD_DX     dXperm = dA W_gate[e]^T + dB W_up[e]^T  (one K loop over both)
 //   WGRAD      dW[e] = P_e^T Q_e, K = the expert's ragged route count
 //
@@ -19,62 +19,128 @@
 // copy of X or dY is ever written.  The shared expert runs through the same
 // kernel as one ungrouped problem of T rows.
 //
-// Tiling: 256 x 256 x 64 block tile, 8 waves as 2 (M) x 4 (N), 128 x 64 per
-// wave (4 x 2 MFMA tiles), double-buffered LDS (2 x 64 KB).  Operands live in
-// LDS K-contiguous, 128-byte rows with the 16-byte chunk index XOR-swizzled
-// by (row >> 1) & 7, so fragment reads and staging writes hit distinct banks.
-// Operands stored N- or M-contiguous in HBM (W_gate/W_up/W_down in the
-// forward, both operands of WGRAD) are transposed in registers during
-// staging (8 k-rows x 4 columns per thread, v_perm byte selects).
+// Pipeline: 256 x 256 block tile, K step 32, a 4-stage LDS ring (4 x 32 KB)
+// filled by direct global->LDS loads (global_load_lds_dwordx4, no staging
+// registers), prefetch distance 3, one barrier per K step.  8 waves as
+// 2 (M) x 4 (N), 128 x 64 per wave (4 x 2 MFMA tiles).
 //
-// Tile order: n-tile fastest, so the blocks resident together share A panels
-// and the whole B panel set of one expert stays cache-resident.  Each output
-// element is owned by exactly one block and its K loop runs in a fixed
-// order: results are bitwise deterministic (§3.4 "Determinism").
+// LDS tile formats:
+//   K-contiguous ("row" tiles: A rows, B rows of an [N][K] weight): 64-byte
+//     rows, the 16-byte chunk index XOR (row >> 2) & 3; fragments are read
+//     with ds_read_b128.
+//   MN-contiguous ("col" tiles: [K][N] weights, both WGRAD operands): 512-byte
+//     k rows, the 32-byte block index XOR 2 * (k & 3); fragments are read
+//     with ds_read_b64_tr_b16, which hands each lane one column of a 4 x 16
+//     block, so no operand is ever transposed in registers.
+// Both swizzles keep fragment reads free of bank conflicts and are applied
+// on the global side of the direct loads.
+//
+// Each output element is owned by exactly one block and its K loop runs in
+// a fixed order: results are bitwise deterministic (§3.4 "Determinism").
 #include "common.h"
 #include "kernels.h"
 
+#define LDSP __attribute__((address_space(3)))
+
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int BM = 256, BN = 256, BK = 32, STAGES = 4;
 constexpr int NTHREADS = 512;
 constexpr int WAVES_N = 4;
 constexpr int WM = 128, WN = 64;
 constexpr int TM = WM / 32, TN = WN / 32;
-constexpr int TILE_ELEMS = BM * BK;  // per operand per stage (bf16 elements)
+constexpr int TILE_ELEMS = BM * BK;  // per operand per stage (bf16 elements) = 16 KB
+constexpr int LOADS_PER_K = 4;       // direct-load instructions per thread per K step
 
 enum Mode { FWD_UP = 0, FWD_DOWN = 1, BWD_DGRAD = 2, BWD_DX = 3, WGRAD = 4 };
 
-DEV int swz(int row, int c) { return c ^ ((row >> 1) & 7); }
-
-// 8 k-rows x 4 columns (2 dwords per row) -> 4 columns x 8 k (16 bytes each).
-DEV void transpose_8x4(const u32x2_t (&v)[8], u32x4_t (&o)[4]) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const uint32_t lo0 = v[2 * q][0], hi0 = v[2 * q + 1][0];
-        const uint32_t lo1 = v[2 * q][1], hi1 = v[2 * q + 1][1];
-        o[0][q] = __builtin_amdgcn_perm(hi0, lo0, 0x05040100u);
-        o[1][q] = __builtin_amdgcn_perm(hi0, lo0, 0x07060302u);
-        o[2][q] = __builtin_amdgcn_perm(hi1, lo1, 0x05040100u);
-        o[3][q] = __builtin_amdgcn_perm(hi1, lo1, 0x07060302u);
-    }
-}
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 
 template <int MODE>
 struct Traits {
-    static constexpr bool A_KM = (MODE == WGRAD);                       // A transposed in staging
-    static constexpr bool B_KN = (MODE == FWD_UP || MODE == FWD_DOWN || MODE == WGRAD);
+    static constexpr bool A_COL = (MODE == WGRAD);                       // A stored [K][M]
+    static constexpr bool B_COL = (MODE == FWD_UP || MODE == FWD_DOWN || MODE == WGRAD);
     static constexpr bool GROUPED_ROWS = (MODE != WGRAD);
 };
 
+// Row tiles: 16-byte chunk c of row r lives at chunk c ^ ((r >> 2) & 3).
+DEV int row_swz(int r, int c) { return c ^ ((r >> 2) & 3); }
+// Col tiles: 32-byte block b of k row kr lives at block b ^ (2 * (kr & 3)).
+DEV int col_swz(int kr, int b) { return b ^ (2 * (kr & 3)); }
+
+DEV void load_lds16(const uint16_t *src, uint16_t *lds_dst) {
+    __builtin_amdgcn_global_load_lds(src, (LDSP void *)lds_dst, 16, 0, 0);
+}
+
+DEV int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Workgroup barrier without the memory fence __syncthreads() carries: the
+// fence would wait for every in-flight direct load (vmcnt(0)) and undo the
+// prefetch.  Ordering is explicit instead: each wave waits for its own tile
+// loads (wait_vmcnt) before the barrier, and every LDS read of the previous
+// K step has been consumed by an MFMA before the wave reaches it.
+DEV void barrier_no_fence() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// s_waitcnt vmcnt(n) leaving lgkm/exp counters alone (gfx9 encoding).
+template <int N>
+DEV void wait_vmcnt() {
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Fragment for MFMA operand rows [r0, r0+32) from a row tile, k step ks.
+DEV bf16x8_t frag_row(const uint16_t *t, int r0, int ks, int lane) {
+    const int r = r0 + (lane & 31);
+    const int c = 2 * ks + (lane >> 5);
+    return __builtin_bit_cast(bf16x8_t, ld_u32x4(t + r * BK + 8 * row_swz(r, c)));
+}
+
+// Fragment for MFMA operand columns [n0, n0+32) from a col tile, k step ks.
+// Lane l gets column n0 + (l & 31) at k = 16 ks + 8 (l >> 5) + 0..7, built
+// from two transposing reads of 4 k rows each.
+DEV bf16x8_t frag_col(const uint16_t *t, int n0, int ks, int lane) {
+    const int i = lane & 15, grp = lane >> 4;
+    const int n = n0 + 16 * (grp & 1) + 4 * (i & 3);
+    const int kb = 16 * ks + 8 * (grp >> 1) + (i >> 2);
+    bf16x4_t v[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int kr = kb + 4 * q;
+        const int off = kr * BN + 16 * col_swz(kr, n >> 4) + (n & 15);
+        v[q] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDSP bf16x4_t *)(t + off));
+    }
+    return bf16x8_t{v[0][0], v[0][1], v[0][2], v[0][3], v[1][0], v[1][1], v[1][2], v[1][3]};
+}
+
+// Physical row of the k row a lane loads in a col tile.  The two k rows of one
+// load instruction (kk0, kk0 + 1, picked by lane / 32) are wave-uniform, so
+// their gather indices come through scalar loads and never wait on the
+// vector-memory counter that tracks the in-flight tile loads.  Rows past the
+// expert's count clamp to its last row (the caller points them at zeros).
+DEV int krow_phys(const int *rows, int kbeg, int kk0, int klen, int nrows, int lane) {
+    const int p0 = kbeg + min(kk0, klen - 1);
+    const int p1 = kbeg + min(kk0 + 1, klen - 1);
+    int r0 = p0, r1 = p1;
+    if (rows) {
+        r0 = rows[p0];
+        r1 = rows[p1];
+    }
+    const int r = (lane >> 5) ? r1 : r0;
+    return min(max(r, 0), nrows - 1);
+}
+
 template <int MODE, bool GROUPED>
-__global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g) {
+__global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int *__restrict__ a_rows, const int *__restrict__ b_rows) {
     using Tr = Traits<MODE>;
-    __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][TILE_ELEMS];  // [stage][A/B]
+    __shared__ __attribute__((aligned(16))) uint16_t lds[STAGES][2][TILE_ELEMS];  // [stage][A/B]
     __shared__ int s_info[2];
 
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
     // ---------------- tile assignment ----------------
@@ -109,10 +175,10 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g) {
                 }
             }
             __syncthreads();
-            if (s_info[0] < 0) return;
-            e = s_info[0];
-            row0 = g.offsets[e] + s_info[1] * BM;
-            row_end = g.offsets[e + 1];
+            e = uniform(s_info[0]);
+            if (e < 0) return;
+            row0 = uniform(g.offsets[e] + uniform(s_info[1]) * BM);
+            row_end = uniform(g.offsets[e + 1]);
         } else {
             row0 = mt * BM;
             row_end = g.M;
@@ -127,156 +193,121 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g) {
         e = rest / ntm;
         n0 = ntile * BN;
         if constexpr (GROUPED) {
-            kbeg = g.offsets[e];
-            klen = g.offsets[e + 1] - kbeg;
+            kbeg = uniform(g.offsets[e]);
+            klen = uniform(g.offsets[e + 1]) - kbeg;
         } else {
             kbeg = 0;
             klen = g.K;
         }
     }
 
-    // ---------------- staging set-up ----------------
-    // MK / NK operands: thread -> chunk c = tid % 8 of rows tid/8 + 64*i.
-    const int st_c = tid & 7, st_r = tid >> 3;
-    // KN / KM operands: thread -> k-group kg = tid / 64 (8 k rows), column group cg = tid % 64.
-    const int kg = tid >> 6, cg = tid & 63;
-
-    const uint16_t *a_ptr[4];
-    const uint16_t *a2_ptr[4];
-    bool a_ok[4];
-    const uint16_t *b_ptr[4];
-    const uint16_t *b2_ptr[4];
-    const uint16_t *bkn_base = nullptr;   // KN: column base of this thread (row 0)
-    const uint16_t *akm_base = nullptr;   // KM: column base of this thread (row 0)
-
-    if constexpr (!Tr::A_KM) {
+    // ---------------- direct-load set-up ----------------
+    // Each thread issues 2 loads per operand per K step.  Load i of wave w is
+    // wave-instruction q = 2 w + i (0..15), writing 1 KB of the stage's tile.
+    //   row tile: instruction q covers rows 16 q .. 16 q + 15; lane -> row
+    //             16 q + lane / 4, physical chunk lane & 3.
+    //   col tile: instruction q covers k rows 2 q, 2 q + 1; lane -> k row
+    //             2 q + lane / 32, physical 16-byte slot lane & 31.
+    const uint16_t *a_row[2] = {nullptr, nullptr};   // row tile: row base (+ chunk), K offset added per step
+    const uint16_t *a2_row[2] = {nullptr, nullptr};
+    const uint16_t *b_row[2] = {nullptr, nullptr};
+    const uint16_t *b2_row[2] = {nullptr, nullptr};
+    long a_col_off = 0, b_col_off = 0;              // col tile: column offset of this lane
+    const uint16_t *b_col_base = nullptr;
+    int lds_off[2];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int p = row0 + st_r + 64 * i;
-            a_ok[i] = p < row_end;
-            int phys = a_ok[i] ? (g.a_rows ? g.a_rows[p] : p) : 0;
+    for (int i = 0; i < 2; ++i) lds_off[i] = (2 * wave + i) * 512;   // bf16 elements (1 KB)
+
+    if constexpr (!Tr::A_COL) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int r = 16 * (2 * wave + i) + (lane >> 2);
+            const int c = row_swz(r, lane & 3);
+            // rows past the region's end load its last row; their results are never stored
+            const int p = min(row0 + r, row_end - 1);
+            int phys = a_rows ? a_rows[p] : p;
             phys = min(max(phys, 0), g.a_nrows - 1);
-            a_ptr[i] = g.A + (long)phys * g.lda + 8 * st_c;
-            a2_ptr[i] = (MODE == BWD_DX) ? g.A2 + (long)phys * g.lda + 8 * st_c : nullptr;
+            a_row[i] = g.A + (long)phys * g.lda + 8 * c;
+            if (MODE == BWD_DX) a2_row[i] = g.A2 + (long)phys * g.lda + 8 * c;
         }
     } else {
-        akm_base = g.A + m0 + 4 * cg;
+        a_col_off = m0;
     }
-    if constexpr (!Tr::B_KN) {
-        // NK: row n of B is output column n0 + n, K contiguous.
+    if constexpr (!Tr::B_COL) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int n = n0 + st_r + 64 * i;
-            b_ptr[i] = g.B + (long)e * g.b_estride + (long)n * g.ldb + 8 * st_c;
-            b2_ptr[i] = (MODE == BWD_DX) ? g.B2 + (long)e * g.b_estride + (long)n * g.ldb + 8 * st_c
-                                         : nullptr;
+        for (int i = 0; i < 2; ++i) {
+            const int r = 16 * (2 * wave + i) + (lane >> 2);
+            const int c = row_swz(r, lane & 3);
+            const long n = n0 + r;
+            b_row[i] = g.B + (long)e * g.b_estride + n * g.ldb + 8 * c;
+            if (MODE == BWD_DX) b2_row[i] = g.B2 + (long)e * g.b_estride + n * g.ldb + 8 * c;
         }
     } else {
-        if constexpr (MODE == FWD_UP) {
-            const int nn = 4 * cg;                       // B tile row (0..255)
-            const int which = (nn >> 5) & 1;             // 0 gate, 1 up
-            const int fcol = n0 + (nn >> 6) * 32 + (nn & 31);
-            bkn_base = (which ? g.B2 : g.B) + (long)e * g.b_estride + fcol;
-        } else {
-            bkn_base = g.B + (long)e * g.b_estride + n0 + 4 * cg;
-        }
+        b_col_base = g.B + (long)e * g.b_estride;
+        b_col_off = n0;
     }
 
-    u32x4_t ra[4];
-    u32x2_t rkm[8];
-    u32x4_t rb[4];
-    u32x2_t rkn[8];
+    // column (within the 256-wide tile) that this lane's 16-byte col-tile load covers
+    auto col_of = [&](int kr) {
+        const int slot = lane & 31;
+        const int b = col_swz(kr, slot >> 1);       // logical 32-byte block
+        return 16 * b + 8 * (slot & 1);
+    };
 
     const int nk = (MODE == BWD_DX) ? 2 * (g.K / BK) : (klen + BK - 1) / BK;
     const int nk_half = g.K / BK;
 
-    auto load_global = [&](int kt) {
-        if constexpr (!Tr::A_KM) {
+    auto issue = [&](int kt) {
+        uint16_t *la = lds[kt % STAGES][0];
+        uint16_t *lb = lds[kt % STAGES][1];
+        // ---- operand A ----
+        if constexpr (!Tr::A_COL) {
             const bool second = (MODE == BWD_DX) && kt >= nk_half;
             const int kk = (second ? kt - nk_half : kt) * BK;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const uint16_t *src = (second ? a2_ptr[i] : a_ptr[i]) + kk;
-                ra[i] = a_ok[i] ? ld_u32x4(src) : u32x4_t{0, 0, 0, 0};
-            }
+            for (int i = 0; i < 2; ++i)
+                load_lds16((second ? a2_row[i] : a_row[i]) + kk, la + lds_off[i]);
         } else {
 #pragma unroll
-            for (int r = 0; r < 8; ++r) {
-                const int kr = kt * BK + 8 * kg + r;
-                if (kr < klen) {
-                    const int p = kbeg + kr;
-                    int phys = g.a_rows ? g.a_rows[p] : p;
-                    phys = min(max(phys, 0), g.a_nrows - 1);
-                    u32x2_t v = ld_u32x2(akm_base + (long)phys * g.lda);
-                    if (g.a_kscale) {
-                        const float s = g.a_kscale[p];
-                        v[0] = pack_bf2(bf_lo(v[0]) * s, bf_hi(v[0]) * s);
-                        v[1] = pack_bf2(bf_lo(v[1]) * s, bf_hi(v[1]) * s);
-                    }
-                    rkm[r] = v;
-                } else {
-                    rkm[r] = u32x2_t{0, 0};
-                }
+            for (int i = 0; i < 2; ++i) {
+                const int kr = 2 * (2 * wave + i) + (lane >> 5);
+                const int kk = kt * BK + kr;
+                const int phys = krow_phys(a_rows, kbeg, kt * BK + 2 * (2 * wave + i), klen,
+                                           g.a_nrows, lane);
+                const int col = col_of(kr);
+                const uint16_t *src = kk < klen ? g.A + (long)phys * g.lda + a_col_off + col
+                                                : g.zeros + col;
+                load_lds16(src, la + lds_off[i]);
             }
         }
-        if constexpr (!Tr::B_KN) {
+        // ---- operand B ----
+        if constexpr (!Tr::B_COL) {
             const bool second = (MODE == BWD_DX) && kt >= nk_half;
             const int kk = (second ? kt - nk_half : kt) * BK;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) rb[i] = ld_u32x4((second ? b2_ptr[i] : b_ptr[i]) + kk);
+            for (int i = 0; i < 2; ++i)
+                load_lds16((second ? b2_row[i] : b_row[i]) + kk, lb + lds_off[i]);
         } else {
 #pragma unroll
-            for (int r = 0; r < 8; ++r) {
-                const int kr = kt * BK + 8 * kg + r;
+            for (int i = 0; i < 2; ++i) {
+                const int kr = 2 * (2 * wave + i) + (lane >> 5);
+                const int kk = kt * BK + kr;
+                const int col = col_of(kr);
+                const uint16_t *src;
                 if constexpr (MODE == WGRAD) {
-                    if (kr < klen) {
-                        const int p = kbeg + kr;
-                        int phys = g.b_rows ? g.b_rows[p] : p;
-                        phys = min(max(phys, 0), g.b_nrows - 1);
-                        rkn[r] = ld_u32x2(bkn_base + (long)phys * g.ldb);
-                    } else {
-                        rkn[r] = u32x2_t{0, 0};
-                    }
+                    const int phys = krow_phys(b_rows, kbeg, kt * BK + 2 * (2 * wave + i), klen,
+                                               g.b_nrows, lane);
+                    src = kk < klen ? b_col_base + (long)phys * g.ldb + b_col_off + col
+                                    : g.zeros + col;
+                } else if constexpr (MODE == FWD_UP) {
+                    // tile columns: 32-column groups alternate gate / up over the same f range
+                    const int which = (col >> 5) & 1;
+                    const int fcol = (int)b_col_off + (col >> 6) * 32 + (col & 31);
+                    src = (which ? g.B2 : g.B) + (long)e * g.b_estride + (long)kk * g.ldb + fcol;
                 } else {
-                    rkn[r] = ld_u32x2(bkn_base + (long)kr * g.ldb);
+                    src = b_col_base + (long)kk * g.ldb + b_col_off + col;
                 }
-            }
-        }
-    };
-
-    auto store_lds = [&](int stage) {
-        uint16_t *la = lds[stage][0];
-        uint16_t *lb = lds[stage][1];
-        if constexpr (!Tr::A_KM) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int row = st_r + 64 * i;
-                st_u32x4(la + row * BK + 8 * swz(row, st_c), ra[i]);
-            }
-        } else {
-            u32x4_t o[4];
-            transpose_8x4(rkm, o);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int j = (q + (cg >> 2)) & 3;
-                const int row = 4 * cg + j;
-                st_u32x4(la + row * BK + 8 * swz(row, kg), o[j]);
-            }
-        }
-        if constexpr (!Tr::B_KN) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int row = st_r + 64 * i;
-                st_u32x4(lb + row * BK + 8 * swz(row, st_c), rb[i]);
-            }
-        } else {
-            u32x4_t o[4];
-            transpose_8x4(rkn, o);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int j = (q + (cg >> 2)) & 3;
-                const int row = 4 * cg + j;
-                st_u32x4(lb + row * BK + 8 * swz(row, kg), o[j]);
+                load_lds16(src, lb + lds_off[i]);
             }
         }
     };
@@ -289,30 +320,32 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g) {
 #pragma unroll
             for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
-    if (nk > 0) {
-        load_global(0);
-        store_lds(0);
-        __syncthreads();
-    }
-    const int lrow = lane & 31, lhalf = lane >> 5;
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+        if (s < nk) issue(s);
+
     for (int kt = 0; kt < nk; ++kt) {
-        const int stage = kt & 1;
-        if (kt + 1 < nk) load_global(kt + 1);
-        const uint16_t *la = lds[stage][0];
-        const uint16_t *lb = lds[stage][1];
+        // tile kt has landed once at most (tiles issued after it) x LOADS_PER_K loads remain
+        const int ahead = min(STAGES - 2, nk - 1 - kt);
+        if (ahead >= 2) wait_vmcnt<2 * LOADS_PER_K>();
+        else if (ahead == 1) wait_vmcnt<LOADS_PER_K>();
+        else wait_vmcnt<0>();
+        barrier_no_fence();
+        if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+        const uint16_t *la = lds[kt % STAGES][0];
+        const uint16_t *lb = lds[kt % STAGES][1];
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
-            const int c = 2 * ks + lhalf;
             bf16x8_t af[TM], bfr[TN];
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
-                const int row = wm * WM + 32 * i + lrow;
-                af[i] = __builtin_bit_cast(bf16x8_t, ld_u32x4(la + row * BK + 8 * swz(row, c)));
+                if constexpr (Tr::A_COL) af[i] = frag_col(la, wm * WM + 32 * i, ks, lane);
+                else af[i] = frag_row(la, wm * WM + 32 * i, ks, lane);
             }
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
-                const int row = wn * WN + 32 * j + lrow;
-                bfr[j] = __builtin_bit_cast(bf16x8_t, ld_u32x4(lb + row * BK + 8 * swz(row, c)));
+                if constexpr (Tr::B_COL) bfr[j] = frag_col(lb, wn * WN + 32 * j, ks, lane);
+                else bfr[j] = frag_row(lb, wn * WN + 32 * j, ks, lane);
             }
 #pragma unroll
             for (int i = 0; i < TM; ++i)
@@ -320,12 +353,12 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g) {
                 for (int j = 0; j < TN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
         }
-        if (kt + 1 < nk) store_lds(stage ^ 1);
-        __syncthreads();
     }
+    __syncthreads();
 
     // ---------------- epilogues ----------------
     // 32x32 accumulator layout: lane l, register q -> row 8*(q/4) + 4*(l/32) + q%4, column l%32.
+    const int lrow = lane & 31, lhalf = lane >> 5;
     if constexpr (MODE == FWD_UP) {
         const int fcol = n0 + wn * 32 + lrow;
 #pragma unroll
@@ -374,11 +407,13 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g) {
                         const float a = bf2f(g.E1[o]), b = bf2f(g.E2[o]);
                         const float sg = 1.0f / (1.0f + expf(-a));
                         const float sl = a * sg;
+                        const float h = sl * b;
                         const float dhp = acc[i][j][q];
-                        prod = prod + dhp * (sl * b);
+                        prod = prod + dhp * h;
                         const float dh = wv * dhp;
                         g.C[o] = f2bf(dh * b * (sg * (1.0f + a * (1.0f - sg))));
                         g.C2[o] = f2bf(dh * sl);
+                        if (g.C3) g.C3[o] = f2bf(wv * h);
                     }
                 }
                 // sum over the 32 columns held by this half-wave (fixed butterfly order)
@@ -416,9 +451,9 @@ template <int MODE>
 hipError_t launch_mode(const GemmArgs &g, unsigned grid, hipStream_t st) {
     if (grid == 0) return hipSuccess;
     if (g.offsets)
-        gemm_kernel<MODE, true><<<dim3(grid), dim3(NTHREADS), 0, st>>>(g);
+        gemm_kernel<MODE, true><<<dim3(grid), dim3(NTHREADS), 0, st>>>(g, g.a_rows, g.b_rows);
     else
-        gemm_kernel<MODE, false><<<dim3(grid), dim3(NTHREADS), 0, st>>>(g);
+        gemm_kernel<MODE, false><<<dim3(grid), dim3(NTHREADS), 0, st>>>(g, g.a_rows, g.b_rows);
     return hipGetLastError();
 }
 

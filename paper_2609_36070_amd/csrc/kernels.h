@@ -14,7 +14,7 @@ struct GemmArgs {
     long lda = 0;
     const int *a_rows = nullptr;       // row gather (MK rows / KM k-rows)
     int a_nrows = 1;                   // rows addressable through A (clamp bound)
-    const float *a_kscale = nullptr;   // KM: per-k-row scale
+    const uint16_t *zeros = nullptr;   // >= 512 zero bytes: source of k rows past a WGRAD count
     // operand B
     const uint16_t *B = nullptr;
     const uint16_t *B2 = nullptr;      // W_up (FWD_UP, BWD_DX)
@@ -27,7 +27,7 @@ struct GemmArgs {
     const int *offsets = nullptr;      // per-expert row ranges (device), or null
     int E = 0;
     // outputs
-    uint16_t *C = nullptr, *C2 = nullptr, *C3 = nullptr;
+    uint16_t *C = nullptr, *C2 = nullptr, *C3 = nullptr;   // BWD_DGRAD: dA, dB, w*h
     long ldc = 0;
     float *Cf = nullptr;
     long c_estride = 0;
@@ -59,7 +59,8 @@ int dwr_nchunks(long T);
 hipError_t launch_gather(const uint16_t *X, const int *perm, const int *offsets, int E, int k, int T,
                          int d, uint16_t *Xperm, hipStream_t st);
 hipError_t launch_prep(const int *perm, const int *offsets, int E, const float *topk_w, int k, int T,
-                       int *rowidx, float *wperm, hipStream_t st);
+                       int *rowidx, float *wperm, uint16_t *zeros, hipStream_t st);
+constexpr int ZERO_PAGE_ELEMS = 512;  // bf16 elements of the zero page (1 KB)
 hipError_t launch_combine(const uint16_t *Yexp, const uint16_t *Ysh, const float *topk_w,
                           const int *route_pos, int T, int d, int k, uint16_t *Y, hipStream_t st);
 hipError_t launch_softmax_bwd(const float *dgpart, int nparts, const int *route_pos,

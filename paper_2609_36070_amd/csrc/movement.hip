@@ -34,13 +34,16 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const uint16_t *__rest
     }
 }
 
-// Plan-order prologue: token row and router weight of every buffer position.
+// Plan-order prologue: token row and router weight of every buffer position,
+// and the zero page the weight-gradient GEMMs read past an expert's count.
 __global__ __launch_bounds__(256) void prep_kernel(const int *__restrict__ perm,
                                                    const int *__restrict__ offsets, int E,
                                                    const float *__restrict__ topk_w, int k, int T,
                                                    int R, int *__restrict__ rowidx,
-                                                   float *__restrict__ wperm) {
+                                                   float *__restrict__ wperm,
+                                                   uint16_t *__restrict__ zeros) {
     const int p = blockIdx.x * 256 + threadIdx.x;
+    if (p < ZERO_PAGE_ELEMS) zeros[p] = 0;
     if (p >= R) return;
     const int total = offsets[E];
     int t = 0;
@@ -298,11 +301,11 @@ hipError_t launch_gather(const uint16_t *X, const int *perm, const int *offsets,
 }
 
 hipError_t launch_prep(const int *perm, const int *offsets, int E, const float *topk_w, int k, int T,
-                       int *rowidx, float *wperm, hipStream_t st) {
+                       int *rowidx, float *wperm, uint16_t *zeros, hipStream_t st) {
     const long R = (long)T * k;
-    if (R == 0) return hipSuccess;
-    prep_kernel<<<dim3((unsigned)((R + 255) / 256)), dim3(256), 0, st>>>(perm, offsets, E, topk_w, k, T,
-                                                                         (int)R, rowidx, wperm);
+    const long n = R > ZERO_PAGE_ELEMS ? R : ZERO_PAGE_ELEMS;
+    prep_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st>>>(perm, offsets, E, topk_w, k, T,
+                                                                         (int)R, rowidx, wperm, zeros);
     return hipGetLastError();
 }
 
