@@ -44,13 +44,27 @@
 
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 32, STAGES = 4;
-constexpr int NTHREADS = 512;
-constexpr int WAVES_N = 4;
-constexpr int WM = 128, WN = 64;
+#ifndef MOE_GEMM_BK
+#define MOE_GEMM_BK 64
+#endif
+constexpr int BM = 256, BN = 256, BK = MOE_GEMM_BK;
+static_assert(BK == 32 || BK == 64, "K step is 32 or 64");
+#ifndef MOE_GEMM_WAVES_M
+#define MOE_GEMM_WAVES_M 2
+#endif
+#ifndef MOE_GEMM_WAVES_N
+#define MOE_GEMM_WAVES_N 4
+#endif
+constexpr int WAVES_M = MOE_GEMM_WAVES_M, WAVES_N = MOE_GEMM_WAVES_N;
+constexpr int NWAVES = WAVES_M * WAVES_N;
+constexpr int NTHREADS = 64 * NWAVES;
+constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
 constexpr int TM = WM / 32, TN = WN / 32;
-constexpr int TILE_ELEMS = BM * BK;  // per operand per stage (bf16 elements) = 16 KB
-constexpr int LOADS_PER_K = 4;       // direct-load instructions per thread per K step
+constexpr int TILE_ELEMS = BM * BK;        // per operand per stage (bf16 elements)
+constexpr int ROWS_PER_LD = 512 / BK;      // row-tile rows covered by one 1 KB wave load
+constexpr int LD_PER_OP = (BK / 2) / NWAVES;  // 1 KB direct loads per operand per wave per K step
+constexpr int LOADS_PER_K = 2 * LD_PER_OP; // direct-load instructions per thread per K step
+static_assert(WN % 64 == 0, "gate/up column pairs need 64-column wave tiles");
 
 enum Mode { FWD_UP = 0, FWD_DOWN = 1, BWD_DGRAD = 2, BWD_DX = 3, WGRAD = 4 };
 
@@ -63,8 +77,9 @@ struct Traits {
     static constexpr bool GROUPED_ROWS = (MODE != WGRAD);
 };
 
-// Row tiles: 16-byte chunk c of row r lives at chunk c ^ ((r >> 2) & 3).
-DEV int row_swz(int r, int c) { return c ^ ((r >> 2) & 3); }
+// Row tiles: 16-byte chunk c of row r lives at chunk c ^ ((r >> 2) & 3)
+// (64-byte rows) or c ^ ((r >> 1) & 7) (128-byte rows).
+DEV int row_swz(int r, int c) { return BK == 32 ? c ^ ((r >> 2) & 3) : c ^ ((r >> 1) & 7); }
 // Col tiles: 32-byte block b of k row kr lives at block b ^ (2 * (kr & 3)).
 DEV int col_swz(int kr, int b) { return b ^ (2 * (kr & 3)); }
 
@@ -135,7 +150,13 @@ DEV int krow_phys(const int *rows, int kbeg, int kk0, int klen, int nrows, int l
 template <int MODE, bool GROUPED>
 __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int *__restrict__ a_rows, const int *__restrict__ b_rows) {
     using Tr = Traits<MODE>;
-    __shared__ __attribute__((aligned(16))) uint16_t lds[STAGES][2][TILE_ELEMS];  // [stage][A/B]
+    // Two LDS stages, each operand its own object: the compiler then knows the
+    // tile being read never aliases the tile being filled and does not stall
+    // the reads on the in-flight direct loads.
+    __shared__ __attribute__((aligned(16))) uint16_t lds_a0[TILE_ELEMS];
+    __shared__ __attribute__((aligned(16))) uint16_t lds_b0[TILE_ELEMS];
+    __shared__ __attribute__((aligned(16))) uint16_t lds_a1[TILE_ELEMS];
+    __shared__ __attribute__((aligned(16))) uint16_t lds_b1[TILE_ELEMS];
     __shared__ int s_info[2];
 
     const int tid = threadIdx.x;
@@ -208,21 +229,21 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
     //             16 q + lane / 4, physical chunk lane & 3.
     //   col tile: instruction q covers k rows 2 q, 2 q + 1; lane -> k row
     //             2 q + lane / 32, physical 16-byte slot lane & 31.
-    const uint16_t *a_row[2] = {nullptr, nullptr};   // row tile: row base (+ chunk), K offset added per step
-    const uint16_t *a2_row[2] = {nullptr, nullptr};
-    const uint16_t *b_row[2] = {nullptr, nullptr};
-    const uint16_t *b2_row[2] = {nullptr, nullptr};
+    const uint16_t *a_row[LD_PER_OP];   // row tile: row base (+ chunk), K offset added per step
+    const uint16_t *a2_row[LD_PER_OP];
+    const uint16_t *b_row[LD_PER_OP];
+    const uint16_t *b2_row[LD_PER_OP];
     long a_col_off = 0, b_col_off = 0;              // col tile: column offset of this lane
     const uint16_t *b_col_base = nullptr;
-    int lds_off[2];
+    int lds_off[LD_PER_OP];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) lds_off[i] = (2 * wave + i) * 512;   // bf16 elements (1 KB)
+    for (int i = 0; i < LD_PER_OP; ++i) lds_off[i] = (LD_PER_OP * wave + i) * 512;   // bf16 elements (1 KB)
 
     if constexpr (!Tr::A_COL) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int r = 16 * (2 * wave + i) + (lane >> 2);
-            const int c = row_swz(r, lane & 3);
+        for (int i = 0; i < LD_PER_OP; ++i) {
+            const int r = ROWS_PER_LD * (LD_PER_OP * wave + i) + lane / (BK / 8);
+            const int c = row_swz(r, lane % (BK / 8));
             // rows past the region's end load its last row; their results are never stored
             const int p = min(row0 + r, row_end - 1);
             int phys = a_rows ? a_rows[p] : p;
@@ -235,9 +256,9 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
     }
     if constexpr (!Tr::B_COL) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int r = 16 * (2 * wave + i) + (lane >> 2);
-            const int c = row_swz(r, lane & 3);
+        for (int i = 0; i < LD_PER_OP; ++i) {
+            const int r = ROWS_PER_LD * (LD_PER_OP * wave + i) + lane / (BK / 8);
+            const int c = row_swz(r, lane % (BK / 8));
             const long n = n0 + r;
             b_row[i] = g.B + (long)e * g.b_estride + n * g.ldb + 8 * c;
             if (MODE == BWD_DX) b2_row[i] = g.B2 + (long)e * g.b_estride + n * g.ldb + 8 * c;
@@ -257,22 +278,20 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
     const int nk = (MODE == BWD_DX) ? 2 * (g.K / BK) : (klen + BK - 1) / BK;
     const int nk_half = g.K / BK;
 
-    auto issue = [&](int kt) {
-        uint16_t *la = lds[kt % STAGES][0];
-        uint16_t *lb = lds[kt % STAGES][1];
+    auto issue = [&](int kt, uint16_t *la, uint16_t *lb) {
         // ---- operand A ----
         if constexpr (!Tr::A_COL) {
             const bool second = (MODE == BWD_DX) && kt >= nk_half;
             const int kk = (second ? kt - nk_half : kt) * BK;
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < LD_PER_OP; ++i)
                 load_lds16((second ? a2_row[i] : a_row[i]) + kk, la + lds_off[i]);
         } else {
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int kr = 2 * (2 * wave + i) + (lane >> 5);
+            for (int i = 0; i < LD_PER_OP; ++i) {
+                const int kr = 2 * (LD_PER_OP * wave + i) + (lane >> 5);
                 const int kk = kt * BK + kr;
-                const int phys = krow_phys(a_rows, kbeg, kt * BK + 2 * (2 * wave + i), klen,
+                const int phys = krow_phys(a_rows, kbeg, kt * BK + 2 * (LD_PER_OP * wave + i), klen,
                                            g.a_nrows, lane);
                 const int col = col_of(kr);
                 const uint16_t *src = kk < klen ? g.A + (long)phys * g.lda + a_col_off + col
@@ -285,17 +304,17 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
             const bool second = (MODE == BWD_DX) && kt >= nk_half;
             const int kk = (second ? kt - nk_half : kt) * BK;
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < LD_PER_OP; ++i)
                 load_lds16((second ? b2_row[i] : b_row[i]) + kk, lb + lds_off[i]);
         } else {
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int kr = 2 * (2 * wave + i) + (lane >> 5);
+            for (int i = 0; i < LD_PER_OP; ++i) {
+                const int kr = 2 * (LD_PER_OP * wave + i) + (lane >> 5);
                 const int kk = kt * BK + kr;
                 const int col = col_of(kr);
                 const uint16_t *src;
                 if constexpr (MODE == WGRAD) {
-                    const int phys = krow_phys(b_rows, kbeg, kt * BK + 2 * (2 * wave + i), klen,
+                    const int phys = krow_phys(b_rows, kbeg, kt * BK + 2 * (LD_PER_OP * wave + i), klen,
                                                g.b_nrows, lane);
                     src = kk < klen ? b_col_base + (long)phys * g.ldb + b_col_off + col
                                     : g.zeros + col;
@@ -320,20 +339,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
 #pragma unroll
             for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
-#pragma unroll
-    for (int s = 0; s < STAGES - 1; ++s)
-        if (s < nk) issue(s);
-
-    for (int kt = 0; kt < nk; ++kt) {
-        // tile kt has landed once at most (tiles issued after it) x LOADS_PER_K loads remain
-        const int ahead = min(STAGES - 2, nk - 1 - kt);
-        if (ahead >= 2) wait_vmcnt<2 * LOADS_PER_K>();
-        else if (ahead == 1) wait_vmcnt<LOADS_PER_K>();
-        else wait_vmcnt<0>();
-        barrier_no_fence();
-        if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
-        const uint16_t *la = lds[kt % STAGES][0];
-        const uint16_t *lb = lds[kt % STAGES][1];
+    auto compute = [&](const uint16_t *la, const uint16_t *lb) {
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
             bf16x8_t af[TM], bfr[TN];
@@ -353,6 +359,30 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
                 for (int j = 0; j < TN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
         }
+    };
+
+    // Double-buffered K loop, unrolled by two so each half names its stages:
+    // wait for this wave's loads of the tile about to be read, barrier (all
+    // waves' loads landed, all reads of the other stage done), start filling
+    // the other stage with the next tile, then compute on this one.
+    if (nk > 0) issue(0, lds_a0, lds_b0);
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+        wait_vmcnt<0>();
+        barrier_no_fence();
+        issue(kt + 1, lds_a1, lds_b1);
+        asm volatile("" ::: "memory");   // keep the loads ahead of this step's LDS reads
+        compute(lds_a0, lds_b0);
+        wait_vmcnt<0>();
+        barrier_no_fence();
+        if (kt + 2 < nk) issue(kt + 2, lds_a0, lds_b0);
+        asm volatile("" ::: "memory");
+        compute(lds_a1, lds_b1);
+    }
+    if (kt < nk) {
+        wait_vmcnt<0>();
+        barrier_no_fence();
+        compute(lds_a0, lds_b0);
     }
     __syncthreads();
 
@@ -360,22 +390,26 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
     // 32x32 accumulator layout: lane l, register q -> row 8*(q/4) + 4*(l/32) + q%4, column l%32.
     const int lrow = lane & 31, lhalf = lane >> 5;
     if constexpr (MODE == FWD_UP) {
-        const int fcol = n0 + wn * 32 + lrow;
+        // wave columns hold (gate, up) MFMA tile pairs over the same 32 f columns
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+        for (int jp = 0; jp < TN / 2; ++jp) {
+            const int fcol = n0 + (wn * WN / 64 + jp) * 32 + lrow;
 #pragma unroll
-            for (int q = 0; q < 16; ++q) {
-                const int p = row0 + wm * WM + 32 * i + 8 * (q >> 2) + 4 * lhalf + (q & 3);
-                if (p < row_end) {
-                    const float a = acc[i][0][q], b = acc[i][1][q];
-                    const long o = (long)p * g.ldc + fcol;
-                    g.C[o] = f2bf(silu_f(a) * b);
-                    if (g.C2) {
-                        g.C2[o] = f2bf(a);
-                        g.C3[o] = f2bf(b);
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    const int p = row0 + wm * WM + 32 * i + 8 * (q >> 2) + 4 * lhalf + (q & 3);
+                    if (p < row_end) {
+                        const float a = acc[i][2 * jp][q], b = acc[i][2 * jp + 1][q];
+                        const long o = (long)p * g.ldc + fcol;
+                        g.C[o] = f2bf(silu_f(a) * b);
+                        if (g.C2) {
+                            g.C2[o] = f2bf(a);
+                            g.C3[o] = f2bf(b);
+                        }
                     }
                 }
-            }
+        }
     } else if constexpr (MODE == FWD_DOWN || MODE == BWD_DX) {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -389,7 +423,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
                 }
             }
     } else if constexpr (MODE == BWD_DGRAD) {
-        float *red = reinterpret_cast<float *>(&lds[0][0][0]);  // [WAVES_N][BM]
+        float *red = reinterpret_cast<float *>(lds_a0);  // [WAVES_N][BM]
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -425,9 +459,9 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
         if (g.dgpart && tid < BM) {
             const int p = row0 + tid;
             if (p < row_end) {
-                float s = red[0 * BM + tid] + red[1 * BM + tid];
-                s = s + red[2 * BM + tid];
-                s = s + red[3 * BM + tid];
+                float s = red[tid];
+#pragma unroll
+                for (int w = 1; w < WAVES_N; ++w) s = s + red[w * BM + tid];
                 g.dgpart[(long)p * g.dg_ld + ntile] = s;
             }
         }
