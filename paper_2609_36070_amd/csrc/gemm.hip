@@ -147,6 +147,25 @@ DEV int krow_phys(const int *rows, int kbeg, int kk0, int klen, int nrows, int l
     return min(max(r, 0), nrows - 1);
 }
 
+// XCD-aware raster.  Workgroups are dealt to the 8 XCDs round-robin; each XCD
+// instead gets a contiguous run of the logical tile order, which walks groups
+// of GM m-tiles with the m-tile fastest.  The ~32 blocks an XCD runs at once
+// then share GM A panels and ~8 B panels in that XCD's L2.  The grid is a
+// multiple of 8; blocks past the tile count return at once.
+DEV bool map_tile(int b, int nblocks, int tiles_m, int ntn, int &mt, int &nt) {
+    constexpr int NX = 8, GM = 4;
+    const int per = nblocks / NX;
+    const int l = (b % NX) * per + b / NX;
+    if (l >= tiles_m * ntn) return false;
+    const int group = l / (GM * ntn);
+    const int first = group * GM;
+    const int gm = min(GM, tiles_m - first);
+    const int within = l - group * GM * ntn;
+    mt = first + within % gm;
+    nt = within / gm;
+    return true;
+}
+
 template <int MODE, bool GROUPED>
 __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int *__restrict__ a_rows, const int *__restrict__ b_rows) {
     using Tr = Traits<MODE>;
@@ -169,8 +188,8 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
     int m0 = 0, kbeg = 0, klen = 0;
     if constexpr (Tr::GROUPED_ROWS) {
         const int ntn = (MODE == FWD_UP) ? g.N / (BN / 2) : g.N / BN;
-        ntile = blockIdx.x % ntn;
-        const int mt = blockIdx.x / ntn;
+        int mt = 0;
+        if (!map_tile(blockIdx.x, gridDim.x, g.tiles_m, ntn, mt, ntile)) return;
         n0 = ntile * ((MODE == FWD_UP) ? BN / 2 : BN);
         if constexpr (GROUPED) {
             if (tid == 0) s_info[0] = -1;
@@ -208,10 +227,10 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
         klen = g.K;
     } else {
         const int ntn = g.N / BN, ntm = g.M / BM;
-        ntile = blockIdx.x % ntn;
-        const int rest = blockIdx.x / ntn;
-        m0 = (rest % ntm) * BM;
-        e = rest / ntm;
+        int cm = 0;   // (expert, m-tile) pair, m-tile fastest
+        if (!map_tile(blockIdx.x, gridDim.x, g.tiles_m, ntn, cm, ntile)) return;
+        m0 = (cm % ntm) * BM;
+        e = cm / ntm;
         n0 = ntile * BN;
         if constexpr (GROUPED) {
             kbeg = uniform(g.offsets[e]);
@@ -482,8 +501,11 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
 }
 
 template <int MODE>
-hipError_t launch_mode(const GemmArgs &g, unsigned grid, hipStream_t st) {
-    if (grid == 0) return hipSuccess;
+hipError_t launch_mode(GemmArgs g, int tiles_m, int ntn, hipStream_t st) {
+    const long tiles = (long)tiles_m * ntn;
+    if (tiles <= 0) return hipSuccess;
+    g.tiles_m = tiles_m;
+    const unsigned grid = (unsigned)((tiles + 7) / 8 * 8);
     if (g.offsets)
         gemm_kernel<MODE, true><<<dim3(grid), dim3(NTHREADS), 0, st>>>(g, g.a_rows, g.b_rows);
     else
@@ -496,29 +518,25 @@ hipError_t launch_mode(const GemmArgs &g, unsigned grid, hipStream_t st) {
 int gemm_tile_m() { return BM; }
 int gemm_tile_n() { return BN; }
 
-// Upper bound on the m-tiles of a grouped problem with `rows` total rows over
-// `groups` groups: sum_e ceil(M_e / BM) <= rows / BM + groups.
-static unsigned grouped_mtiles(long rows, int groups) {
-    return (unsigned)(rows / BM + (groups > 0 ? groups : 1));
+// m-tile slots of a row problem.  Grouped: an upper bound on
+// sum_e ceil(M_e / BM), which is at most rows / BM + groups; slots past the
+// actual tiles return at once.
+static int mtiles(const GemmArgs &g, long rows, int groups) {
+    return g.offsets ? (int)(rows / BM + (groups > 0 ? groups : 1)) : (int)((rows + BM - 1) / BM);
 }
 
 hipError_t launch_gemm_fwd_up(const GemmArgs &g, long rows, int groups, hipStream_t st) {
-    const unsigned mt = g.offsets ? grouped_mtiles(rows, groups) : (unsigned)((rows + BM - 1) / BM);
-    return launch_mode<FWD_UP>(g, mt * (unsigned)(g.N / (BN / 2)), st);
+    return launch_mode<FWD_UP>(g, mtiles(g, rows, groups), g.N / (BN / 2), st);
 }
 hipError_t launch_gemm_fwd_down(const GemmArgs &g, long rows, int groups, hipStream_t st) {
-    const unsigned mt = g.offsets ? grouped_mtiles(rows, groups) : (unsigned)((rows + BM - 1) / BM);
-    return launch_mode<FWD_DOWN>(g, mt * (unsigned)(g.N / BN), st);
+    return launch_mode<FWD_DOWN>(g, mtiles(g, rows, groups), g.N / BN, st);
 }
 hipError_t launch_gemm_bwd_dgrad(const GemmArgs &g, long rows, int groups, hipStream_t st) {
-    const unsigned mt = g.offsets ? grouped_mtiles(rows, groups) : (unsigned)((rows + BM - 1) / BM);
-    return launch_mode<BWD_DGRAD>(g, mt * (unsigned)(g.N / BN), st);
+    return launch_mode<BWD_DGRAD>(g, mtiles(g, rows, groups), g.N / BN, st);
 }
 hipError_t launch_gemm_bwd_dx(const GemmArgs &g, long rows, int groups, hipStream_t st) {
-    const unsigned mt = g.offsets ? grouped_mtiles(rows, groups) : (unsigned)((rows + BM - 1) / BM);
-    return launch_mode<BWD_DX>(g, mt * (unsigned)(g.N / BN), st);
+    return launch_mode<BWD_DX>(g, mtiles(g, rows, groups), g.N / BN, st);
 }
 hipError_t launch_gemm_wgrad(const GemmArgs &g, int groups, hipStream_t st) {
-    const unsigned tiles = (unsigned)(groups * (g.M / BM) * (g.N / BN));
-    return launch_mode<WGRAD>(g, tiles, st);
+    return launch_mode<WGRAD>(g, groups * (g.M / BM), g.N / BN, st);
 }

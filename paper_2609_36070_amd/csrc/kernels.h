@@ -35,6 +35,7 @@ struct GemmArgs {
     const float *rowscale = nullptr;              // BWD_DGRAD: router weight per row
     float *dgpart = nullptr;
     int dg_ld = 0;
+    int tiles_m = 0;                   // set by the launcher: m-tile slots of the raster
 };
 
 int gemm_tile_m();
