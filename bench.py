@@ -74,6 +74,33 @@ def stage_flops(w):
     return fwd, bwd
 
 
+def source_sha256():
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2609_36070_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch recorded under profiles/ for this kernel and workload.
+
+    Returns None unless the record was taken on the current kernel sources
+    (same hash of the csrc directory): counters of an older kernel say nothing
+    about this one.
+    """
+    import glob
+    for path in glob.glob(os.path.join(ROOT, "profiles", "traffic_*.json")):
+        with open(path) as fh:
+            rec = json.load(fh)
+        if rec.get("kernel") == kernel and rec.get("workload") == workload \
+                and rec.get("source_sha256") == source_sha256():
+            return rec["read_bytes_per_launch"] + rec["write_bytes_per_launch"]
+    return None
+
+
 def cpu_baseline(w, inputs, sample_tokens):
     """Time the CPU oracle on the first `sample_tokens` tokens of the workload."""
     import numpy as np
@@ -109,7 +136,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="large_shared_train")
-    ap.add_argument("--cpu-sample-tokens", type=int, default=512)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=2048)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (the reference "
@@ -218,7 +245,7 @@ def main():
     achieved = fl / (avg_ms * 1e-3) / 1e12
     roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic(dom, w.name),
                 "avg_launch_ms": round(avg_ms, 4), "flops_per_launch": fl}
 
     step_flops = w.fwd_flops() + (w.bwd_flops() if w.backward else 0.0)
