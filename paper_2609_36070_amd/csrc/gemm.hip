@@ -130,23 +130,6 @@ DEV bf16x8_t frag_col(const uint16_t *t, int n0, int ks, int lane) {
     return bf16x8_t{v[0][0], v[0][1], v[0][2], v[0][3], v[1][0], v[1][1], v[1][2], v[1][3]};
 }
 
-// Physical row of the k row a lane loads in a col tile.  The two k rows of one
-// load instruction (kk0, kk0 + 1, picked by lane / 32) are wave-uniform, so
-// their gather indices come through scalar loads and never wait on the
-// vector-memory counter that tracks the in-flight tile loads.  Rows past the
-// expert's count clamp to its last row (the caller points them at zeros).
-DEV int krow_phys(const int *rows, int kbeg, int kk0, int klen, int nrows, int lane) {
-    const int p0 = kbeg + min(kk0, klen - 1);
-    const int p1 = kbeg + min(kk0 + 1, klen - 1);
-    int r0 = p0, r1 = p1;
-    if (rows) {
-        r0 = rows[p0];
-        r1 = rows[p1];
-    }
-    const int r = (lane >> 5) ? r1 : r0;
-    return min(max(r, 0), nrows - 1);
-}
-
 // XCD-aware raster.  Workgroups are dealt to the 8 XCDs round-robin; each XCD
 // instead gets a contiguous run of the logical tile order, which walks groups
 // of GM m-tiles with the m-tile fastest.  The ~32 blocks an XCD runs at once
@@ -298,6 +281,27 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
     const int nk_half = g.K / BK;
 
     auto issue = [&](int kt, uint16_t *la, uint16_t *lb) {
+        // WGRAD k rows come through the plan's token index: fetch every index
+        // this K step needs first (scalar loads, one wait), then issue the
+        // direct loads.
+        int pa[LD_PER_OP], pb[LD_PER_OP];
+        if constexpr (MODE == WGRAD) {
+            int ia[2 * LD_PER_OP], ib[2 * LD_PER_OP];
+#pragma unroll
+            for (int i = 0; i < LD_PER_OP; ++i) {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int p = kbeg + min(kt * BK + 2 * (LD_PER_OP * wave + i) + h, klen - 1);
+                    ia[2 * i + h] = a_rows ? a_rows[p] : p;
+                    ib[2 * i + h] = b_rows ? b_rows[p] : p;
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < LD_PER_OP; ++i) {
+                pa[i] = min(max((lane >> 5) ? ia[2 * i + 1] : ia[2 * i], 0), g.a_nrows - 1);
+                pb[i] = min(max((lane >> 5) ? ib[2 * i + 1] : ib[2 * i], 0), g.b_nrows - 1);
+            }
+        }
         // ---- operand A ----
         if constexpr (!Tr::A_COL) {
             const bool second = (MODE == BWD_DX) && kt >= nk_half;
@@ -310,10 +314,8 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
             for (int i = 0; i < LD_PER_OP; ++i) {
                 const int kr = 2 * (LD_PER_OP * wave + i) + (lane >> 5);
                 const int kk = kt * BK + kr;
-                const int phys = krow_phys(a_rows, kbeg, kt * BK + 2 * (LD_PER_OP * wave + i), klen,
-                                           g.a_nrows, lane);
                 const int col = col_of(kr);
-                const uint16_t *src = kk < klen ? g.A + (long)phys * g.lda + a_col_off + col
+                const uint16_t *src = kk < klen ? g.A + (long)pa[i] * g.lda + a_col_off + col
                                                 : g.zeros + col;
                 load_lds16(src, la + lds_off[i]);
             }
@@ -333,9 +335,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
                 const int col = col_of(kr);
                 const uint16_t *src;
                 if constexpr (MODE == WGRAD) {
-                    const int phys = krow_phys(b_rows, kbeg, kt * BK + 2 * (LD_PER_OP * wave + i), klen,
-                                               g.b_nrows, lane);
-                    src = kk < klen ? b_col_base + (long)phys * g.ldb + b_col_off + col
+                    src = kk < klen ? b_col_base + (long)pb[i] * g.ldb + b_col_off + col
                                     : g.zeros + col;
                 } else if constexpr (MODE == FWD_UP) {
                     // tile columns: 32-column groups alternate gate / up over the same f range
