@@ -28,6 +28,8 @@ DEV uint32_t pack_bf2(float lo, float hi) {
 
 DEV float silu_f(float a) { return a / (1.0f + expf(-a)); }
 
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+
 DEV int wave_lane() { return threadIdx.x & 63; }
 
 // 32-bit wave shuffles
@@ -37,3 +39,9 @@ DEV int shfl_xor_i(int v, int m) { return __shfl_xor(v, m, 64); }
 DEV u32x4_t ld_u32x4(const void *p) { return *reinterpret_cast<const u32x4_t *>(p); }
 DEV void st_u32x4(void *p, u32x4_t v) { *reinterpret_cast<u32x4_t *>(p) = v; }
 DEV u32x2_t ld_u32x2(const void *p) { return *reinterpret_cast<const u32x2_t *>(p); }
+
+// 8 floats -> 8 bf16 (round to nearest even) packed in 16 bytes
+DEV u32x4_t pack_bf8(const f32x8 &v) {
+    return u32x4_t{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]),
+                   pack_bf2(v[6], v[7])};
+}

@@ -407,81 +407,112 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
 
     // ---------------- epilogues ----------------
     // 32x32 accumulator layout: lane l, register q -> row 8*(q/4) + 4*(l/32) + q%4, column l%32.
+    // Row-tile outputs go through a per-wave LDS scratch (32 rows x 64 fp32,
+    // pitch SP) so every global access of the epilogue is a 16-byte vector of
+    // 8 consecutive columns of one row.
     const int lrow = lane & 31, lhalf = lane >> 5;
+    constexpr int SP = 68;                       // scratch pitch in floats (16-byte rows, few bank conflicts)
+    static_assert(TN == 2 && WN == 64, "epilogue staging assumes 64-column wave tiles");
+    uint16_t *scr_base = (wave >> 1) == 0 ? lds_a0 : (wave >> 1) == 1 ? lds_b0
+                       : (wave >> 1) == 2 ? lds_a1 : lds_b1;
+    float *scr = reinterpret_cast<float *>(scr_base) + (wave & 1) * 32 * SP;
+    auto stage = [&](int i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+                scr[(8 * (q >> 2) + 4 * lhalf + (q & 3)) * SP + 32 * j + lrow] = acc[i][j][q];
+    };
+    auto read8 = [&](int row, int c) {
+        const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(scr + row * SP + c);
+        const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(scr + row * SP + c + 4);
+        return f32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    };
     if constexpr (MODE == FWD_UP) {
-        // wave columns hold (gate, up) MFMA tile pairs over the same 32 f columns
+        // staged columns 0..31 hold the gate, 32..63 the up projection of the same 32 f columns
+        const long fcol0 = n0 + wn * 32;
 #pragma unroll
-        for (int jp = 0; jp < TN / 2; ++jp) {
-            const int fcol = n0 + (wn * WN / 64 + jp) * 32 + lrow;
+        for (int i = 0; i < TM; ++i) {
+            stage(i);
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
+            for (int t = 0; t < 2; ++t) {
+                const int row = (lane >> 2) + 16 * t, c = 8 * (lane & 3);
+                const int p = row0 + wm * WM + 32 * i + row;
+                const f32x8 a = read8(row, c), b = read8(row, 32 + c);
+                if (p < row_end) {
+                    f32x8 h;
 #pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    const int p = row0 + wm * WM + 32 * i + 8 * (q >> 2) + 4 * lhalf + (q & 3);
-                    if (p < row_end) {
-                        const float a = acc[i][2 * jp][q], b = acc[i][2 * jp + 1][q];
-                        const long o = (long)p * g.ldc + fcol;
-                        g.C[o] = f2bf(silu_f(a) * b);
-                        if (g.C2) {
-                            g.C2[o] = f2bf(a);
-                            g.C3[o] = f2bf(b);
-                        }
+                    for (int k = 0; k < 8; ++k) h[k] = silu_f(a[k]) * b[k];
+                    const long o = (long)p * g.ldc + fcol0 + c;
+                    st_u32x4(g.C + o, pack_bf8(h));
+                    if (g.C2) {
+                        st_u32x4(g.C2 + o, pack_bf8(a));
+                        st_u32x4(g.C3 + o, pack_bf8(b));
                     }
                 }
+            }
         }
     } else if constexpr (MODE == FWD_DOWN || MODE == BWD_DX) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i) {
+            stage(i);
 #pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int col = n0 + wn * WN + 32 * j + lrow;
-#pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    const int p = row0 + wm * WM + 32 * i + 8 * (q >> 2) + 4 * lhalf + (q & 3);
-                    if (p < row_end) g.C[(long)p * g.ldc + col] = f2bf(acc[i][j][q]);
-                }
+            for (int t = 0; t < 4; ++t) {
+                const int row = (lane >> 3) + 8 * t, c = 8 * (lane & 7);
+                const int p = row0 + wm * WM + 32 * i + row;
+                const f32x8 v = read8(row, c);
+                if (p < row_end) st_u32x4(g.C + (long)p * g.ldc + n0 + wn * WN + c, pack_bf8(v));
             }
+        }
     } else if constexpr (MODE == BWD_DGRAD) {
-        float *red = reinterpret_cast<float *>(lds_a0);  // [WAVES_N][BM]
+        float *red = reinterpret_cast<float *>(lds_a0) + 2 * 32 * SP;  // [WAVES_N][BM]
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i) {
+            stage(i);
 #pragma unroll
-            for (int q = 0; q < 16; ++q) {
-                const int rl = wm * WM + 32 * i + 8 * (q >> 2) + 4 * lhalf + (q & 3);
+            for (int t = 0; t < 4; ++t) {
+                const int row = (lane >> 3) + 8 * t, c = 8 * (lane & 7);
+                const int rl = wm * WM + 32 * i + row;
                 const int p = row0 + rl;
-                const bool ok = p < row_end;
-                const float wv = (ok && g.rowscale) ? g.rowscale[p] : 1.0f;
+                const f32x8 dhp = read8(row, c);
                 float prod = 0.f;
+                if (p < row_end) {
+                    const float wv = g.rowscale ? g.rowscale[p] : 1.0f;
+                    const long o = (long)p * g.ldc + n0 + wn * WN + c;
+                    const u32x4_t av = ld_u32x4(g.E1 + o), bv = ld_u32x4(g.E2 + o);
+                    f32x8 da, db, hw;
 #pragma unroll
-                for (int j = 0; j < TN; ++j) {
-                    const int col = n0 + wn * WN + 32 * j + lrow;
-                    if (ok) {
-                        const long o = (long)p * g.ldc + col;
-                        const float a = bf2f(g.E1[o]), b = bf2f(g.E2[o]);
+                    for (int k = 0; k < 8; ++k) {
+                        const float a = (k & 1) ? bf_hi(av[k >> 1]) : bf_lo(av[k >> 1]);
+                        const float b = (k & 1) ? bf_hi(bv[k >> 1]) : bf_lo(bv[k >> 1]);
                         const float sg = 1.0f / (1.0f + expf(-a));
                         const float sl = a * sg;
                         const float h = sl * b;
-                        const float dhp = acc[i][j][q];
-                        prod = prod + dhp * h;
-                        const float dh = wv * dhp;
-                        g.C[o] = f2bf(dh * b * (sg * (1.0f + a * (1.0f - sg))));
-                        g.C2[o] = f2bf(dh * sl);
-                        if (g.C3) g.C3[o] = f2bf(wv * h);
+                        prod = prod + dhp[k] * h;
+                        const float dh = wv * dhp[k];
+                        da[k] = dh * b * (sg * (1.0f + a * (1.0f - sg)));
+                        db[k] = dh * sl;
+                        hw[k] = wv * h;
                     }
+                    st_u32x4(g.C + o, pack_bf8(da));
+                    st_u32x4(g.C2 + o, pack_bf8(db));
+                    if (g.C3) st_u32x4(g.C3 + o, pack_bf8(hw));
                 }
-                // sum over the 32 columns held by this half-wave (fixed butterfly order)
-#pragma unroll
-                for (int off = 16; off >= 1; off >>= 1) prod = prod + shfl_xor_f(prod, off);
-                if (lrow == 0) red[wn * BM + rl] = prod;
+                // sum over the 8 lanes holding this row's 64 columns (fixed butterfly order)
+                prod = prod + shfl_xor_f(prod, 1);
+                prod = prod + shfl_xor_f(prod, 2);
+                prod = prod + shfl_xor_f(prod, 4);
+                if ((lane & 7) == 0) red[wn * BM + rl] = prod;
             }
+        }
         __syncthreads();
         if (g.dgpart && tid < BM) {
             const int p = row0 + tid;
             if (p < row_end) {
-                float s = red[tid];
+                float sum = red[tid];
 #pragma unroll
-                for (int w = 1; w < WAVES_N; ++w) s = s + red[w * BM + tid];
-                g.dgpart[(long)p * g.dg_ld + ntile] = s;
+                for (int w = 1; w < WAVES_N; ++w) sum = sum + red[w * BM + tid];
+                g.dgpart[(long)p * g.dg_ld + ntile] = sum;
             }
         }
     } else {  // WGRAD
