@@ -19,14 +19,15 @@
 // copy of X or dY is ever written.  The shared expert runs through the same
 // kernel as one ungrouped problem of T rows.
 //
-// Pipeline: 256 x 256 block tile, K step 32, a 4-stage LDS ring (4 x 32 KB)
+// Pipeline: 256 x 256 block tile, K step 64, two LDS stages (2 x 64 KB)
 // filled by direct global->LDS loads (global_load_lds_dwordx4, no staging
-// registers), prefetch distance 3, one barrier per K step.  8 waves as
-// 2 (M) x 4 (N), 128 x 64 per wave (4 x 2 MFMA tiles).
+// registers): the next tile streams in while the current one is multiplied,
+// one fence-free barrier per K step.  8 waves as 2 (M) x 4 (N), 128 x 64 per
+// wave (4 x 2 MFMA tiles).  Tiles are rastered XCD-aware.
 //
 // LDS tile formats:
-//   K-contiguous ("row" tiles: A rows, B rows of an [N][K] weight): 64-byte
-//     rows, the 16-byte chunk index XOR (row >> 2) & 3; fragments are read
+//   K-contiguous ("row" tiles: A rows, B rows of an [N][K] weight): 128-byte
+//     rows, the 16-byte chunk index XOR (row >> 1) & 7; fragments are read
 //     with ds_read_b128.
 //   MN-contiguous ("col" tiles: [K][N] weights, both WGRAD operands): 512-byte
 //     k rows, the 32-byte block index XOR 2 * (k & 3); fragments are read
@@ -39,6 +40,8 @@
 // a fixed order: results are bitwise deterministic (§3.4 "Determinism").
 #include "common.h"
 #include "kernels.h"
+
+#include <type_traits>
 
 #define LDSP __attribute__((address_space(3)))
 
@@ -64,7 +67,7 @@ constexpr int TILE_ELEMS = BM * BK;        // per operand per stage (bf16 elemen
 constexpr int ROWS_PER_LD = 512 / BK;      // row-tile rows covered by one 1 KB wave load
 constexpr int LD_PER_OP = (BK / 2) / NWAVES;  // 1 KB direct loads per operand per wave per K step
 constexpr int LOADS_PER_K = 2 * LD_PER_OP; // direct-load instructions per thread per K step
-static_assert(WN % 64 == 0, "gate/up column pairs need 64-column wave tiles");
+static_assert(WN == 64 || WN == 128, "gate/up column pairs and the epilogue need 64- or 128-column wave tiles");
 
 enum Mode { FWD_UP = 0, FWD_DOWN = 1, BWD_DGRAD = 2, BWD_DX = 3, WGRAD = 4 };
 
@@ -358,6 +361,19 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
 #pragma unroll
             for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
+    auto load_frags = [&](const uint16_t *la, const uint16_t *lb, int ks, bf16x8_t (&af)[TM],
+                          bf16x8_t (&bfr)[TN]) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            if constexpr (Tr::A_COL) af[i] = frag_col(la, wm * WM + 32 * i, ks, lane);
+            else af[i] = frag_row(la, wm * WM + 32 * i, ks, lane);
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            if constexpr (Tr::B_COL) bfr[j] = frag_col(lb, wn * WN + 32 * j, ks, lane);
+            else bfr[j] = frag_row(lb, wn * WN + 32 * j, ks, lane);
+        }
+    };
     auto compute = [&](const uint16_t *la, const uint16_t *lb) {
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
@@ -407,15 +423,18 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
 
     // ---------------- epilogues ----------------
     // 32x32 accumulator layout: lane l, register q -> row 8*(q/4) + 4*(l/32) + q%4, column l%32.
-    // Row-tile outputs go through a per-wave LDS scratch (32 rows x 64 fp32,
+    // Row-tile outputs go through a per-wave LDS scratch (32 rows x WN fp32,
     // pitch SP) so every global access of the epilogue is a 16-byte vector of
     // 8 consecutive columns of one row.
     const int lrow = lane & 31, lhalf = lane >> 5;
-    constexpr int SP = 68;                       // scratch pitch in floats (16-byte rows, few bank conflicts)
-    static_assert(TN == 2 && WN == 64, "epilogue staging assumes 64-column wave tiles");
-    uint16_t *scr_base = (wave >> 1) == 0 ? lds_a0 : (wave >> 1) == 1 ? lds_b0
-                       : (wave >> 1) == 2 ? lds_a1 : lds_b1;
-    float *scr = reinterpret_cast<float *>(scr_base) + (wave & 1) * 32 * SP;
+    constexpr int SP = WN + 4;                   // scratch pitch in floats (16-byte rows, few bank conflicts)
+    constexpr int LPR = WN / 8;                  // lanes per staged row
+    constexpr int RPP = 64 / LPR;                // staged rows per pass
+    constexpr int WPA = NWAVES / 4;              // waves sharing one 32 KB stage array
+    static_assert(WPA * 32 * SP + WAVES_N * BM <= TILE_ELEMS / 2, "epilogue scratch fits a stage array");
+    uint16_t *scr_base = (wave / WPA) == 0 ? lds_a0 : (wave / WPA) == 1 ? lds_b0
+                       : (wave / WPA) == 2 ? lds_a1 : lds_b1;
+    float *scr = reinterpret_cast<float *>(scr_base) + (wave % WPA) * 32 * SP;
     auto stage = [&](int i) {
 #pragma unroll
         for (int j = 0; j < TN; ++j)
@@ -429,25 +448,29 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
         return f32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     };
     if constexpr (MODE == FWD_UP) {
-        // staged columns 0..31 hold the gate, 32..63 the up projection of the same 32 f columns
-        const long fcol0 = n0 + wn * 32;
+        // staged columns 64 jp + 0..31 hold the gate, 64 jp + 32..63 the up
+        // projection of the same 32 f columns
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             stage(i);
 #pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                const int row = (lane >> 2) + 16 * t, c = 8 * (lane & 3);
-                const int p = row0 + wm * WM + 32 * i + row;
-                const f32x8 a = read8(row, c), b = read8(row, 32 + c);
-                if (p < row_end) {
-                    f32x8 h;
+            for (int jp = 0; jp < TN / 2; ++jp) {
+                const long fcol0 = n0 + (wn * WN / 64 + jp) * 32;
 #pragma unroll
-                    for (int k = 0; k < 8; ++k) h[k] = silu_f(a[k]) * b[k];
-                    const long o = (long)p * g.ldc + fcol0 + c;
-                    st_u32x4(g.C + o, pack_bf8(h));
-                    if (g.C2) {
-                        st_u32x4(g.C2 + o, pack_bf8(a));
-                        st_u32x4(g.C3 + o, pack_bf8(b));
+                for (int t = 0; t < 2; ++t) {
+                    const int row = (lane >> 2) + 16 * t, c = 8 * (lane & 3);
+                    const int p = row0 + wm * WM + 32 * i + row;
+                    const f32x8 a = read8(row, 64 * jp + c), b = read8(row, 64 * jp + 32 + c);
+                    if (p < row_end) {
+                        f32x8 h;
+#pragma unroll
+                        for (int k = 0; k < 8; ++k) h[k] = silu_f(a[k]) * b[k];
+                        const long o = (long)p * g.ldc + fcol0 + c;
+                        st_u32x4(g.C + o, pack_bf8(h));
+                        if (g.C2) {
+                            st_u32x4(g.C2 + o, pack_bf8(a));
+                            st_u32x4(g.C3 + o, pack_bf8(b));
+                        }
                     }
                 }
             }
@@ -457,21 +480,21 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
         for (int i = 0; i < TM; ++i) {
             stage(i);
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const int row = (lane >> 3) + 8 * t, c = 8 * (lane & 7);
+            for (int t = 0; t < 32 / RPP; ++t) {
+                const int row = lane / LPR + RPP * t, c = 8 * (lane % LPR);
                 const int p = row0 + wm * WM + 32 * i + row;
                 const f32x8 v = read8(row, c);
                 if (p < row_end) st_u32x4(g.C + (long)p * g.ldc + n0 + wn * WN + c, pack_bf8(v));
             }
         }
     } else if constexpr (MODE == BWD_DGRAD) {
-        float *red = reinterpret_cast<float *>(lds_a0) + 2 * 32 * SP;  // [WAVES_N][BM]
+        float *red = reinterpret_cast<float *>(lds_a0) + WPA * 32 * SP;  // [WAVES_N][BM]
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             stage(i);
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const int row = (lane >> 3) + 8 * t, c = 8 * (lane & 7);
+            for (int t = 0; t < 32 / RPP; ++t) {
+                const int row = lane / LPR + RPP * t, c = 8 * (lane % LPR);
                 const int rl = wm * WM + 32 * i + row;
                 const int p = row0 + rl;
                 const f32x8 dhp = read8(row, c);
@@ -498,11 +521,10 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
                     st_u32x4(g.C2 + o, pack_bf8(db));
                     if (g.C3) st_u32x4(g.C3 + o, pack_bf8(hw));
                 }
-                // sum over the 8 lanes holding this row's 64 columns (fixed butterfly order)
-                prod = prod + shfl_xor_f(prod, 1);
-                prod = prod + shfl_xor_f(prod, 2);
-                prod = prod + shfl_xor_f(prod, 4);
-                if ((lane & 7) == 0) red[wn * BM + rl] = prod;
+                // sum over the LPR lanes holding this row's WN columns (fixed butterfly order)
+#pragma unroll
+                for (int m = 1; m < LPR; m <<= 1) prod = prod + shfl_xor_f(prod, m);
+                if (lane % LPR == 0) red[wn * BM + rl] = prod;
             }
         }
         __syncthreads();

@@ -154,3 +154,32 @@ def test_determinism_bitwise_repeat():
         torch.cuda.synchronize()
         for n in names:
             assert torch.equal(getattr(L, n), first[n]), (rep, n)
+
+
+def test_graph_capture_replays_match_eager():
+    """The whole step captured in a HIP graph; every replay equals the eager run bitwise."""
+    from paper_2609_36070_amd.workloads import make_inputs
+    w = RAGGED_TRAIN
+    L, _ = run_layer(w, inputs=make_inputs(w, 7))
+    names = ("logits", "topk_idx", "topk_w", "counts", "offsets", "perm", "route_pos", "Y", "dX",
+             "dW_gate", "dW_up", "dW_down", "dW_r", "dZ", "dWg_s", "dWu_s", "dWd_s")
+    eager = {n: getattr(L, n).clone() for n in names}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        L.step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        L.step()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for n in names:                     # eager work between replays: clobber every output
+            getattr(L, n).fill_(-7 if getattr(L, n).dtype == torch.int32 else 3.0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for n in names:
+            assert torch.equal(getattr(L, n), eager[n]), (rep, n)
+    say("  graph replays bitwise equal to eager")
