@@ -101,6 +101,47 @@ def measured_traffic(kernel, workload):
     return None
 
 
+def schedule_timing(H, stream, reps=20):
+    """Multi-rank dispatch schedule (moe_schedule) on each synthetic route table,
+    built for rank 0 (which owns the hot expert where there is one); GPU time
+    per call from a graph of back-to-back calls."""
+    import torch
+    from paper_2609_36070_amd import binding as B
+    from paper_2609_36070_amd.workloads import ROUTE_TABLES, make_route_table
+    res = {}
+    for name, t in ROUTE_TABLES.items():
+        A = torch.from_numpy(make_route_table(t, seed=0)).cuda()
+        R, NK, L = t.R, t.NK, t.L
+        M = torch.empty(R * L, dtype=torch.int32, device="cuda")
+        S = torch.empty(L + 1, dtype=torch.int32, device="cuda")
+        phi = torch.empty((R * NK, 2), dtype=torch.int32, device="cuda")
+        ws = torch.empty(B.moe_schedule_workspace_bytes(R, NK, L), dtype=torch.uint8, device="cuda")
+        for _ in range(3):
+            B.moe_schedule(R, NK, L, 0, A, M, S, phi, R * NK, ws)
+        torch.cuda.synchronize()
+        # reps calls captured in one HIP graph, so host launch cost is not timed
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(reps):
+                B.moe_schedule(R, NK, L, 0, A, M, S, phi, R * NK, ws)
+        graph.replay()
+        torch.cuda.synchronize()
+        a, b = H.create(), H.create()
+        H.record(a, stream)
+        graph.replay()
+        H.record(b, stream)
+        H.sync(b)
+        us = 1e3 * H.ms(a, b) / reps
+        P = int(S[L].item())
+        nbytes = 2 * 4 * R * NK + 8 * P + 4 * R * L      # A read twice, schedule rows, M
+        res[name] = {"R": R, "N": t.N, "K": t.K, "L": L, "rank": 0, "routes_received": P,
+                     "us": round(us, 2), "GB/s": round(nbytes / (us * 1e-6) / 1e9, 1)}
+        H.destroy(a)
+        H.destroy(b)
+        del A, phi, ws
+    return res
+
+
 def cpu_baseline(w, inputs, sample_tokens):
     """Time the CPU oracle on the first `sample_tokens` tokens of the workload."""
     import numpy as np
@@ -138,6 +179,8 @@ def main():
     ap.add_argument("--workload", default="large_shared_train")
     ap.add_argument("--cpu-sample-tokens", type=int, default=2048)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-schedule", action="store_true",
+                    help="skip timing the multi-rank dispatch schedule")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (the reference "
                          "kernel for scaling HBM byte counters)")
@@ -261,6 +304,13 @@ def main():
     for name, v in stage_report.items():
         log(f"   {name:28s} {v['ms']:9.4f} ms  {v.get('tflops', '')}")
 
+    sched = None
+    if not args.no_schedule:
+        sched = schedule_timing(H, stream)
+        for name, v in sched.items():
+            log(f"   schedule {name:8s} R={v['R']:3d} L={v['L']:3d} {v['us']:8.2f} us "
+                f"({100.0 * v['us'] * 1e-3 / ms_step:.3f}% of the layer step)")
+
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a token sample ...")
@@ -280,6 +330,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "stages": stage_report,
+        "schedule": sched,
     }
     print(json.dumps(out), flush=True)
 

@@ -162,6 +162,37 @@ moe_status moe_plan(const moe_shape *shape, const int32_t *topk_idx,
                     const moe_plan_bufs *plan, void *ws, size_t ws_bytes,
                     moe_stream stream);
 
+/* Pull-based dispatch schedule for R source ranks (§3.1, Algorithm 1, and
+ * its sort-key statement in "Scheduling").  Each of R ranks holds N tokens
+ * with K routes each; A is the all-gathered route table and the schedule is
+ * the one rank c builds for its L local experts (global ids c*L .. c*L+L-1).
+ *   A   [R, NK] int32 in: A[r*NK + j] = global expert id of route j of
+ *       source rank r, in [0, R*L).
+ *   M   [R, L] int32 out: M[r*L + l] = routes of rank r to local expert l.
+ *   S   [L+1] int32 out: S[l] = start of local expert l's region
+ *       (sum of M over all ranks and all experts before l); S[L] = P, the
+ *       number of routes this rank receives.
+ *   phi [phi_rows, 2] int32 out: row p < P holds (source rank r, route j):
+ *       buffer position p receives route j of rank r.  Within a region the
+ *       rows are ordered by (o, r), o = number of earlier routes of row r to
+ *       the same expert, so source ranks interleave round-robin.  Rows >= P
+ *       are not written.
+ * Error word (the first int32 of ws, readable after a synchronisation):
+ * bit 0 = some id outside [0, R*L) (such routes are never scheduled, the
+ * counts ignore them); bit 1 = P > phi_rows (rows past phi_rows are
+ * dropped).  Work per local route is O(R).  With R = 1 and c = 0 the
+ * schedule equals moe_plan's perm.
+ * Limits: 1 <= R <= 1024, 1 <= L <= 256, 0 <= c < R, 0 <= NK, R*NK < 2^31,
+ * L * (R rounded up to a multiple of 4) <= 8192; otherwise MOE_EINVAL
+ * (R, L < 1, NK < 0, c outside [0, R), phi_rows < 0, null or misaligned
+ * pointer), MOE_EUNSUPPORTED (outside the limits) or MOE_ENOSPACE (ws_bytes
+ * below moe_schedule_workspace_bytes, a pure host function that returns 0
+ * for invalid or unsupported dimensions). */
+size_t moe_schedule_workspace_bytes(int64_t R, int64_t NK, int64_t L);
+moe_status moe_schedule(int64_t R, int64_t NK, int64_t L, int64_t c, const int32_t *A,
+                        int32_t *M, int32_t *S, int32_t *phi, int64_t phi_rows, void *ws,
+                        size_t ws_bytes, moe_stream stream);
+
 /* Materialised dispatch (§3.1 "Scheduling", local part): Xperm[p] =
  * X[perm[p] / k] for p < T*k.  moe_forward does not need it (its GEMMs read
  * token rows through the plan); it exists for callers that want the

@@ -22,7 +22,8 @@ MOE_OK, MOE_EINVAL, MOE_EUNSUPPORTED, MOE_ENOSPACE, MOE_EHIP = range(5)
 WS_ERROR, WS_A, WS_B, WS_H, WS_YEXP, WS_YSH, WS_DG, WS_DA, WS_DB, WS_DXPERM = range(10)
 
 EXPORTS = ("moe_workspace_bytes", "moe_workspace_region", "moe_route", "moe_plan",
-           "moe_dispatch", "moe_forward", "moe_backward", "moe_status_string", "moe_version")
+           "moe_schedule_workspace_bytes", "moe_schedule", "moe_dispatch", "moe_forward",
+           "moe_backward", "moe_status_string", "moe_version")
 
 
 class MoeShape(ctypes.Structure):
@@ -78,14 +79,18 @@ def lib():
         L.moe_route.argtypes = [P(MoeShape)] + [c_void_p] * 7 + [c_size_t, c_void_p]
         L.moe_plan.argtypes = [P(MoeShape), c_void_p, P(MoePlanBufs), c_void_p, c_size_t, c_void_p]
         L.moe_dispatch.argtypes = [P(MoeShape), c_void_p, P(MoePlanBufs), c_void_p, c_void_p]
+        L.moe_schedule_workspace_bytes.argtypes = [ctypes.c_int64] * 3
+        L.moe_schedule_workspace_bytes.restype = c_size_t
+        L.moe_schedule.argtypes = ([ctypes.c_int64] * 4 + [c_void_p] * 4
+                                   + [ctypes.c_int64, c_void_p, c_size_t, c_void_p])
         L.moe_forward.argtypes = [P(MoeShape), c_void_p, P(MoeWeights), c_void_p, c_void_p,
                                   P(MoePlanBufs), c_void_p, c_int, c_void_p, c_size_t, c_void_p,
                                   P(MoeStageEvents)]
         L.moe_backward.argtypes = [P(MoeShape), c_void_p, c_void_p, c_void_p, P(MoeWeights),
                                    c_void_p, c_void_p, P(MoePlanBufs), c_void_p, P(MoeGrads),
                                    c_void_p, c_size_t, c_void_p, P(MoeStageEvents)]
-        for fn in ("moe_route", "moe_plan", "moe_dispatch", "moe_forward", "moe_backward",
-                   "moe_workspace_region"):
+        for fn in ("moe_route", "moe_plan", "moe_schedule", "moe_dispatch", "moe_forward",
+                   "moe_backward", "moe_workspace_region"):
             getattr(L, fn).restype = c_int
         L.moe_status_string.argtypes = [c_int]
         L.moe_status_string.restype = ctypes.c_char_p
@@ -172,6 +177,18 @@ def moe_plan(shape, topk_idx, plan: MoePlanBufs, ws, ws_bytes=None, stream=None,
     st = lib().moe_plan(ctypes.byref(shape), _p(topk_idx), ctypes.byref(plan), _p(ws), nbytes,
                         _stream(stream))
     return _check("moe_plan", st, raise_on_error)
+
+
+def moe_schedule_workspace_bytes(R: int, NK: int, L: int) -> int:
+    return int(lib().moe_schedule_workspace_bytes(R, NK, L))
+
+
+def moe_schedule(R, NK, L, c, A, M, S, phi, phi_rows, ws, ws_bytes=None, stream=None,
+                 raise_on_error=True):
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    st = lib().moe_schedule(R, NK, L, c, _p(A), _p(M), _p(S), _p(phi), phi_rows, _p(ws), nbytes,
+                            _stream(stream))
+    return _check("moe_schedule", st, raise_on_error)
 
 
 def moe_dispatch(shape, X, plan: MoePlanBufs, Xperm, stream=None, raise_on_error=True):

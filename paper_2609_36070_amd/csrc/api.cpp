@@ -110,6 +110,32 @@ moe_status check_ws(const moe_shape *s, const void *ws, size_t ws_bytes, int wit
     return MOE_OK;
 }
 
+// Multi-rank schedule: validation and workspace (error word, per-chunk
+// flags, per-(row, chunk, expert) counts that become ordinal bases).
+moe_status check_schedule_dims(int64_t R, int64_t NK, int64_t L, int64_t c) {
+    if (R <= 0 || L <= 0 || NK < 0 || c < 0 || c >= R) return MOE_EINVAL;
+    if (R > 1024 || L > 256) return MOE_EUNSUPPORTED;
+    if (L * sched_rpad((int)R) > SCHED_MAX_TABLE) return MOE_EUNSUPPORTED;
+    if (R * NK >= (int64_t(1) << 31)) return MOE_EUNSUPPORTED;
+    return MOE_OK;
+}
+
+struct SchedLayout {
+    size_t err, flags, counts, total;
+};
+
+SchedLayout schedule_layout(int64_t R, int64_t NK, int64_t L) {
+    const size_t C = (size_t)sched_nchunks((long)NK);
+    SchedLayout SL{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) { const size_t at = o; o += up(bytes > 0 ? bytes : 1); return at; };
+    SL.err = take(4);
+    SL.flags = take((size_t)R * C * 4);
+    SL.counts = take((size_t)R * C * (size_t)L * 4);
+    SL.total = o;
+    return SL;
+}
+
 template <typename T>
 T *at(void *ws, size_t off) { return reinterpret_cast<T *>(static_cast<char *>(ws) + off); }
 
@@ -192,6 +218,26 @@ moe_status moe_plan(const moe_shape *shape, const int32_t *topk_idx, const moe_p
     MOE_TRY(launch_plan(topk_idx, R, (int)shape->E, plan->counts, plan->offsets, plan->perm,
                         plan->route_pos, at<int>(ws, L.blockcounts), at<int>(ws, L.blockbase),
                         at<int>(ws, L.blockflags), at<int>(ws, L.err), s));
+    return MOE_OK;
+}
+
+size_t moe_schedule_workspace_bytes(int64_t R, int64_t NK, int64_t L) {
+    if (check_schedule_dims(R, NK, L, 0) != MOE_OK) return 0;
+    return schedule_layout(R, NK, L).total;
+}
+
+moe_status moe_schedule(int64_t R, int64_t NK, int64_t L, int64_t c, const int32_t *A, int32_t *M,
+                        int32_t *S, int32_t *phi, int64_t phi_rows, void *ws, size_t ws_bytes,
+                        moe_stream stream) {
+    moe_status st = check_schedule_dims(R, NK, L, c);
+    if (st != MOE_OK) return st;
+    if (!ptr_ok(A) || !ptr_ok(M) || !ptr_ok(S) || !ptr_ok(phi) || !ptr_ok(ws) || phi_rows < 0)
+        return MOE_EINVAL;
+    const SchedLayout SL = schedule_layout(R, NK, L);
+    if (ws_bytes < SL.total) return MOE_ENOSPACE;
+    MOE_TRY(launch_schedule(A, (int)R, (int)NK, (int)L, (int)c, M, S, phi, (long)phi_rows,
+                            at<int>(ws, SL.counts), at<int>(ws, SL.flags), at<int>(ws, SL.err),
+                            static_cast<hipStream_t>(stream)));
     return MOE_OK;
 }
 

@@ -5,6 +5,10 @@
 #include <stdint.h>
 
 constexpr int PLAN_CHUNK = 1024;  // routes per plan block
+#ifndef MOE_SCHED_CHUNK
+#define MOE_SCHED_CHUNK 512
+#endif
+constexpr int SCHED_CHUNK = MOE_SCHED_CHUNK;  // routes of one source rank per schedule block
 
 // Grouped-GEMM problem description (see gemm.hip for the five modes).
 struct GemmArgs {
@@ -55,6 +59,12 @@ int plan_nblocks(long R);
 hipError_t launch_plan(const int *topk_idx, int R, int E, int *counts, int *offsets, int *perm,
                        int *route_pos, int *blockcounts, int *blockbase, int *blockflags, int *err,
                        hipStream_t st);
+
+constexpr int SCHED_MAX_TABLE = 8192;  // L * (R rounded up to 4): the count table staged in LDS
+int sched_nchunks(long NK);
+int sched_rpad(int R);
+hipError_t launch_schedule(const int *A, int R, int NK, int L, int c, int *M, int *S, int *phi,
+                           long phi_rows, int *counts, int *flags, int *err, hipStream_t st);
 
 int dwr_nchunks(long T);
 hipError_t launch_gather(const uint16_t *X, const int *perm, const int *offsets, int E, int k, int T,

@@ -133,3 +133,58 @@ def make_inputs(w: Workload, seed: int = 0) -> dict:
         hot_tokens=hot,
     )
     return out
+
+
+# ---------------------------------------------------------------------------
+# All-gathered route tables for the multi-rank dispatch schedule
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class RouteTable:
+    name: str
+    R: int          # source ranks (expert-parallel degree)
+    N: int          # tokens per rank
+    K: int          # routes per token
+    L: int          # experts per rank (R*L experts in all)
+    bias_std: float = 0.5   # per-expert popularity skew: weight exp(bias), bias ~ N(0, std)
+    hot_frac: float = 0.0   # fraction of tokens that always take global expert 0
+    note: str = ""
+
+    @property
+    def NK(self) -> int:
+        return self.N * self.K
+
+
+ROUTE_TABLES = {
+    "ep4": RouteTable("ep4", R=4, N=16384, K=8, L=32, hot_frac=0.1,
+                      note="128 experts over 4 ranks (the hot-expert layer's global view)"),
+    "ep16": RouteTable("ep16", R=16, N=4096, K=8, L=16,
+                       note="256 experts over 16 ranks"),
+    "ep64": RouteTable("ep64", R=64, N=2048, K=8, L=4,
+                       note="256 experts over 64 ranks, 2048 tokens per rank"),
+}
+
+
+def make_route_table(t: RouteTable, seed: int = 0) -> np.ndarray:
+    """A[R, N*K] int32, token-major (route j = token*K + slot).
+
+    Each token draws K distinct experts out of R*L without replacement with
+    probabilities proportional to exp(bias) (Gumbel top-K sampling), lists
+    them in ascending id, and a seeded ``hot_frac`` of the tokens always
+    includes expert 0.  Draw order: bias[R*L], the hot-token subset, then
+    the Gumbel noise in blocks of 4096 tokens.
+    """
+    rng = np.random.default_rng(seed)
+    E, T = t.R * t.L, t.R * t.N
+    bias = rng.standard_normal(E) * t.bias_std
+    hot = np.zeros(T, bool)
+    if t.hot_frac > 0:
+        hot[rng.choice(T, size=int(np.floor(t.hot_frac * T)), replace=False)] = True
+    out = np.empty((T, t.K), np.int32)
+    for s in range(0, T, 4096):
+        e = min(T, s + 4096)
+        g = rng.gumbel(size=(e - s, E)) + bias
+        g[hot[s:e], 0] = np.inf
+        pick = np.argpartition(-g, t.K - 1, axis=1)[:, :t.K]
+        out[s:e] = np.sort(pick, axis=1)
+    return out.reshape(t.R, t.N * t.K)

@@ -123,6 +123,38 @@ def test_plan_forward_backward_validation():
                           None, None) == B.MOE_EINVAL
 
 
+def test_schedule_workspace_and_validation():
+    L = B.lib()
+    # error word + per-(rank, chunk) flags + per-(rank, chunk, expert) counts
+    ws = B.moe_schedule_workspace_bytes(64, 16384, 4)
+    assert ws >= 4 + 64 * 4 + 64 * 4 * 4
+    assert B.moe_schedule_workspace_bytes(64, 2 * 16384, 4) > ws    # grows with the row length
+    assert B.moe_schedule_workspace_bytes(4, 0, 32) > 0          # no routes is valid
+    assert B.moe_schedule_workspace_bytes(0, 16, 4) == 0         # R < 1
+    assert B.moe_schedule_workspace_bytes(2048, 16, 4) == 0      # R > 1024
+    assert B.moe_schedule_workspace_bytes(4, 16, 300) == 0       # L > 256
+    assert B.moe_schedule_workspace_bytes(1024, 1 << 21, 4) == 0  # R*NK >= 2^31
+    assert B.moe_schedule_workspace_bytes(1024, 16, 8) > 0       # count table of 8192
+    assert B.moe_schedule_workspace_bytes(1024, 16, 9) == 0      # count table above 8192
+    assert B.moe_schedule_workspace_bytes(1021, 16, 8) > 0       # R rounds up to 1024
+
+    def call(R=4, NK=64, Lx=8, c=1, A=FAKE, M=FAKE, S=FAKE, phi=FAKE, rows=256, w=FAKE,
+             nb=1 << 40):
+        return L.moe_schedule(R, NK, Lx, c, A, M, S, phi, rows, w, nb, None)
+
+    assert call(c=4) == B.MOE_EINVAL          # c >= R
+    assert call(c=-1) == B.MOE_EINVAL
+    assert call(NK=-1) == B.MOE_EINVAL
+    assert call(Lx=0) == B.MOE_EINVAL
+    assert call(A=None) == B.MOE_EINVAL
+    assert call(phi=MISALIGNED) == B.MOE_EINVAL
+    assert call(rows=-1) == B.MOE_EINVAL
+    assert call(w=None) == B.MOE_EINVAL
+    assert call(nb=8) == B.MOE_ENOSPACE
+    assert call(R=2000, c=0) == B.MOE_EUNSUPPORTED
+    assert call(Lx=512) == B.MOE_EUNSUPPORTED
+
+
 def test_oracle_is_not_imported_by_the_package():
     import sys
     import importlib
