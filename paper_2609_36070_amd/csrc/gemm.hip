@@ -374,25 +374,24 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
             else bfr[j] = frag_row(lb, wn * WN + 32 * j, ks, lane);
         }
     };
+    // Fragments are double-buffered in registers: the reads of k sub-step
+    // ks + 1 are issued before the MFMAs of sub-step ks (the scheduling
+    // barrier stops the compiler from sinking them to their uses), so LDS
+    // latency hides behind the matrix cores.
     auto compute = [&](const uint16_t *la, const uint16_t *lb) {
+        bf16x8_t af[2][TM], bfr[2][TN];
+        load_frags(la, lb, 0, af[0], bfr[0]);
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
-            bf16x8_t af[TM], bfr[TN];
-#pragma unroll
-            for (int i = 0; i < TM; ++i) {
-                if constexpr (Tr::A_COL) af[i] = frag_col(la, wm * WM + 32 * i, ks, lane);
-                else af[i] = frag_row(la, wm * WM + 32 * i, ks, lane);
-            }
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                if constexpr (Tr::B_COL) bfr[j] = frag_col(lb, wn * WN + 32 * j, ks, lane);
-                else bfr[j] = frag_row(lb, wn * WN + 32 * j, ks, lane);
-            }
+            const int cur = ks & 1;
+            if (ks + 1 < BK / 16) load_frags(la, lb, ks + 1, af[cur ^ 1], bfr[cur ^ 1]);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j],
+                                                                        acc[i][j], 0, 0, 0);
         }
     };
 
