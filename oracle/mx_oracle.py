@@ -1,0 +1,181 @@
+"""Plain CPU oracle of the MXFP8 routed-expert forward (float64 numpy).
+
+TEST INFRASTRUCTURE ONLY.  Only the test-suite, the package smoke check and the
+benchmark's CPU-baseline leg may import this module.  The GPU library never
+calls it and shares no code with it.
+
+The paper runs its routed experts in MXFP8 and keeps the shared expert in BF16
+(§3.4 "MXFP8 Support"): weights are quantised ahead of time by their own
+kernel, activations are quantised where they are produced (dispatch, the
+grouped GEMMs, the gated activation).  MXFP8 is the OCP microscaling format
+the paper cites: blocks of elements share one power-of-two scale.
+
+Readings of what the paper leaves open:
+
+* elements are OCP FP8 E4M3 (exponent bias 7, no infinities, largest finite
+  magnitude 448, S.1111.111 is NaN);
+* a block is 32 consecutive elements along the contraction (K) dimension of
+  the GEMM that consumes the tensor, with one E8M0 scale (a biased exponent,
+  bias 127) per block;
+* scale: the microscaling definition, shared_exp = floor(log2(amax)) - emax
+  with emax = 8 (the largest E4M3 exponent), clamped to [-127, 127]; an
+  all-zero block takes -127;
+* elements: v / 2**shared_exp rounded to the nearest E4M3 value (ties to the
+  even code), saturating at +-448 (the block maximum can exceed 448 after
+  scaling, since amax / 2**shared_exp lies in [256, 512));
+* quantised tensors: X per token along d (once per token, before the gather),
+  W_gate and W_up along d, W_down along f, and the gated activation H along f
+  (straight from its fp32 value); products are exact and accumulate in fp32 on
+  the GPU (here in float64); the expert output Yexp is rounded to bf16 as in
+  the BF16 path, and the shared expert and the combine are the BF16 path's.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import moe_oracle as O
+
+F64 = np.float64
+E4M3_EMAX = 8          # largest unbiased exponent of an E4M3 normal
+E4M3_MAX = 448.0       # 1.75 * 2**8
+E4M3_EMIN = -6         # exponent of the smallest normal; subnormals are k * 2**-9
+BLOCK = 32
+SCALE_BIAS = 127
+
+
+# ---------------------------------------------------------------------------
+# E4M3 elements
+# ---------------------------------------------------------------------------
+
+def e4m3_value(code):
+    """Value of E4M3 codes (float64; NaN for S.1111.111)."""
+    c = np.asarray(code, np.int64)
+    s = (c >> 7) & 1
+    e = (c >> 3) & 15
+    m = c & 7
+    mag = np.where(e == 0, m * 2.0 ** (E4M3_EMIN - 3), (8 + m) * np.exp2(e - 7 - 3.0))
+    mag = np.where((e == 15) & (m == 7), np.nan, mag)
+    return np.where(s == 1, -mag, mag)
+
+
+def e4m3_round(x):
+    """Nearest E4M3 code of each value (ties to the even code), saturating at
+    +-448.  Values must be finite."""
+    x = np.asarray(x, F64)
+    sign = (np.signbit(x)).astype(np.int64)
+    a = np.abs(x)
+    # binade exponent of |x| (the subnormal range shares the quantum of 2**-6)
+    _, ex = np.frexp(np.where(a > 0, a, 1.0))
+    e = np.maximum(ex - 1, E4M3_EMIN)
+    q = np.exp2(e - 3.0)                       # spacing of the grid in that binade
+    m = np.rint(a / q).astype(np.int64)        # round half to even
+    # rounding up to the next binade: m == 16 means (1.0) * 2**(e+1)
+    up = m == 16
+    e = np.where(up, e + 1, e)
+    m = np.where(up, 8, m)
+    normal = m >= 8
+    code = np.where(normal, ((e + 7) << 3) | (m - 8), m)
+    code = np.where(m * np.exp2(e - 3.0) > E4M3_MAX, 0x7E, code)   # saturate
+    code = np.where(a == 0, 0, code)
+    return ((sign << 7) | code).astype(np.uint8)
+
+
+# ---------------------------------------------------------------------------
+# Microscaling blocks
+# ---------------------------------------------------------------------------
+
+def _blocks(v, axis):
+    v = np.moveaxis(np.asarray(v, F64), axis, -1)
+    n = v.shape[-1]
+    if n % BLOCK:
+        raise ValueError(f"length {n} along the block axis is not a multiple of {BLOCK}")
+    return v.reshape(v.shape[:-1] + (n // BLOCK, BLOCK))
+
+
+def shared_exponent(amax):
+    """floor(log2(amax)) - 8, clamped to the E8M0 range; -127 for amax = 0."""
+    amax = np.asarray(amax, F64)
+    _, ex = np.frexp(np.where(amax > 0, amax, 1.0))
+    se = (ex - 1) - E4M3_EMAX
+    se = np.where(amax > 0, se, -SCALE_BIAS)
+    return np.clip(se, -SCALE_BIAS, SCALE_BIAS).astype(np.int64)
+
+
+def mx_quantize(v, axis):
+    """MXFP8 quantisation along `axis` (a multiple of 32 long).
+
+    Returns (codes uint8 with v's shape, scales uint8 = shared_exp + 127 with
+    the block axis shortened 32-fold)."""
+    b = _blocks(v, axis)
+    se = shared_exponent(np.max(np.abs(b), axis=-1))
+    codes = e4m3_round(np.ldexp(b, -se[..., None]))
+    codes = np.moveaxis(codes.reshape(codes.shape[:-2] + (-1,)), -1, axis)
+    scales = np.moveaxis((se + SCALE_BIAS).astype(np.uint8), -1, axis)
+    return codes, scales
+
+
+def mx_dequantize(codes, scales, axis):
+    b = _blocks(e4m3_value(codes), axis)
+    se = np.moveaxis(np.asarray(scales, np.int64), axis, -1) - SCALE_BIAS
+    out = np.ldexp(b, se[..., None])
+    return np.moveaxis(out.reshape(out.shape[:-2] + (-1,)), -1, axis)
+
+
+def mx_qdq(v, axis):
+    """Value after an MXFP8 round trip."""
+    return mx_dequantize(*mx_quantize(v, axis), axis)
+
+
+# ---------------------------------------------------------------------------
+# The routed-expert forward in MXFP8 (§3.4 "MXFP8 Support"), shared expert and
+# combine as in BF16 (§2.1 equation)
+# ---------------------------------------------------------------------------
+
+def quantize_weights(W):
+    """Pre-quantised routed weights: W_gate, W_up along d; W_down along f.
+    Returns dict of (codes, scales) keyed like W, each in W's own layout."""
+    return {
+        "W_gate": mx_quantize(W["W_gate"], axis=1),
+        "W_up": mx_quantize(W["W_up"], axis=1),
+        "W_down": mx_quantize(W["W_down"], axis=1),
+    }
+
+
+def moe_forward_mx(X, W, idx, w):
+    """Forward of the layer with MXFP8 routed experts.
+
+    Returns dict(Y [T,d], H [T*k, f] (fp64, before its quantisation),
+    Hq (dequantised H), Yexp [T*k, d] (fp64, before bf16 rounding), Ysh,
+    Xq (codes, scales), plan arrays) in plan-position order."""
+    X = np.asarray(X, F64)
+    T, d = X.shape
+    E = W["W_gate"].shape[0]
+    k = idx.shape[1]
+    counts, offsets, perm, route_pos = O.plan(idx, E)
+    tok = perm // k
+    Xq = mx_quantize(X, axis=1)
+    Xh = mx_dequantize(*Xq, axis=1)
+    Wg = mx_qdq(W["W_gate"], axis=1)
+    Wu = mx_qdq(W["W_up"], axis=1)
+    Wd = mx_qdq(W["W_down"], axis=1)
+    f = W["W_gate"].shape[2]
+    H = np.zeros((T * k, f), F64)
+    for e in range(E):
+        rows = slice(offsets[e], offsets[e + 1])
+        xe = Xh[tok[rows]]
+        H[rows] = O.silu(xe @ Wg[e]) * (xe @ Wu[e])
+    Hq = mx_qdq(H, axis=1)
+    Yexp = np.zeros((T * k, d), F64)
+    for e in range(E):
+        rows = slice(offsets[e], offsets[e + 1])
+        Yexp[rows] = Hq[rows] @ Wd[e]
+    Ysh = None
+    Y = np.zeros((T, d), F64)
+    if W.get("Wg_s") is not None:
+        Ysh = O.expert_ffn(X, W["Wg_s"], W["Wu_s"], W["Wd_s"])
+        Y += Ysh
+    for s in range(k):
+        Y += w[:, s:s + 1] * Yexp[route_pos[np.arange(T) * k + s]]
+    return dict(Y=Y, H=H, Hq=Hq, Yexp=Yexp, Ysh=Ysh, Xq=Xq, counts=counts,
+                offsets=offsets, perm=perm, route_pos=route_pos)
+
