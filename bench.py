@@ -74,12 +74,17 @@ def stage_flops(w):
     return fwd, bwd
 
 
+# sources the BF16 GEMM kernels are compiled from (device code and helpers)
+GEMM_SOURCES = ("gemm.hip", "common.h")
+
+
 def source_sha256():
-    import glob
+    """Hash of the BF16 GEMM kernel sources: a traffic record taken on other
+    sources does not describe the kernel being timed."""
     import hashlib
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2609_36070_amd", "csrc", "*"))):
-        with open(f, "rb") as fh:
+    for name in GEMM_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_36070_amd", "csrc", name), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
@@ -142,6 +147,55 @@ def schedule_timing(H, stream, reps=20):
     return res
 
 
+def mx_forward_timing(H, stream, inputs, steps, warmup):
+    """route + plan + moe_forward_mx on the forward layer of the benchmark
+    workload (routed experts in MXFP8, shared expert BF16), with per-stage
+    events; the routed weights are pre-quantised once, outside the timing."""
+    import torch
+    from paper_2609_36070_amd import binding as B
+    from paper_2609_36070_amd.layer import DeviceLayer
+    from paper_2609_36070_amd.workloads import WORKLOADS
+    w = WORKLOADS["large_shared"]
+    L = DeviceLayer(w, inputs, with_backward=False, mx=True)
+    for _ in range(warmup):
+        L.step_mx()
+    torch.cuda.synchronize()
+    nf = len(B.FWD_STAGES) + 1
+    per = []
+    a, b = H.create(), H.create()
+    H.record(a, stream)
+    for _ in range(steps):
+        ev = [H.create() for _ in range(nf)]
+        fe = B.MoeStageEvents()
+        for i, e in enumerate(ev):
+            fe.ev[i] = e
+        start = H.create()
+        H.record(start, stream)
+        L.route()
+        L.plan()
+        L.forward_mx(events=fe)
+        per.append((start, ev))
+    H.record(b, stream)
+    H.sync(b)
+    ms = H.ms(a, b) / steps
+    fwd_fl, _ = stage_flops(w)
+    stages = {}
+    for start, ev in per:
+        stages["route+plan"] = stages.get("route+plan", 0.0) + H.ms(start, ev[0])
+        for i, name in enumerate(B.FWD_STAGES):
+            stages[name] = stages.get(name, 0.0) + H.ms(ev[i], ev[i + 1])
+    out = {"workload": w.name, "ms_per_step": round(ms, 4),
+           "tflops": round(w.fwd_flops() / (ms * 1e-3) / 1e12, 2), "stages": {}}
+    for name, t in stages.items():
+        t /= steps
+        out["stages"][name] = {"ms": round(t, 4)}
+        if name in fwd_fl:
+            out["stages"][name]["tflops"] = round(fwd_fl[name][0] / (t * 1e-3) / 1e12, 1)
+    del L
+    torch.cuda.synchronize()
+    return out
+
+
 def cpu_baseline(w, inputs, sample_tokens):
     """Time the CPU oracle on the first `sample_tokens` tokens of the workload."""
     import numpy as np
@@ -181,6 +235,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-schedule", action="store_true",
                     help="skip timing the multi-rank dispatch schedule")
+    ap.add_argument("--no-mx", action="store_true", help="skip timing the MXFP8 forward")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (the reference "
                          "kernel for scaling HBM byte counters)")
@@ -304,6 +359,18 @@ def main():
     for name, v in stage_report.items():
         log(f"   {name:28s} {v['ms']:9.4f} ms  {v.get('tflops', '')}")
 
+    mxf = None
+    if not args.no_mx and w.name in ("large_shared", "large_shared_train"):
+        mxf = mx_forward_timing(H, stream, inputs, max(3, args.steps // 2), 2)
+        bf16_fwd = stages["route"] + stages["plan"] + sum(
+            v for k, v in stages.items() if k.startswith("fwd."))
+        mxf["bf16_forward_ms"] = round(bf16_fwd, 4)
+        mxf["speedup_vs_bf16_forward"] = round(bf16_fwd / mxf["ms_per_step"], 3)
+        log(f"[bench] MXFP8 forward: {mxf['ms_per_step']:.3f} ms ({mxf['tflops']} TFLOP/s), "
+            f"BF16 forward {bf16_fwd:.3f} ms")
+        for name, v in mxf["stages"].items():
+            log(f"   mx.{name:25s} {v['ms']:9.4f} ms  {v.get('tflops', '')}")
+
     sched = None
     if not args.no_schedule:
         sched = schedule_timing(H, stream)
@@ -331,6 +398,7 @@ def main():
         "cpu_baseline": cpu,
         "stages": stage_report,
         "schedule": sched,
+        "mxfp8_forward": mxf,
     }
     print(json.dumps(out), flush=True)
 

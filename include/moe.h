@@ -110,8 +110,32 @@ typedef enum {
     MOE_WS_DA = 7,      /* bf16 [T*k, f]  gradient wrt A                    */
     MOE_WS_DB = 8,      /* bf16 [T*k, f]  gradient wrt B                    */
     MOE_WS_DXPERM = 9,  /* bf16 [T*k, d]  routed dX terms, plan order       */
-    MOE_WS_COUNT = 10
+    /* MXFP8 forward only (moe_mx_workspace_region): */
+    MOE_WS_XQ = 10,     /* E4M3 [T, d]    X, one scale per 32 of d          */
+    MOE_WS_XS = 11,     /* E8M0 [T, d/32] scales of MOE_WS_XQ               */
+    MOE_WS_HQ = 12,     /* E4M3 [T*k, f]  gated activation, plan order      */
+    MOE_WS_HS = 13,     /* E8M0 [T*k, f/32] scales of MOE_WS_HQ             */
+    MOE_WS_COUNT = 14
 } moe_ws_tensor;
+
+/* MXFP8 routed-expert weights (§3.4 "MXFP8 Support"), written once by
+ * moe_mx_quantize_weights and read by moe_forward_mx.  Codes are OCP FP8
+ * E4M3; each scale byte b stands for 2^(b - 127) and covers 32 consecutive
+ * elements along the contraction axis of the GEMM that reads the weight.
+ * Both are stored K-contiguous, i.e. transposed from the bf16 layout:
+ *   Wg_q, Wu_q [E, f, d] codes: row n is column n of W_gate[e] / W_up[e]
+ *   Wg_s, Wu_s [E, f, d/32] scales
+ *   Wd_q       [E, d, f] codes: row n is column n of W_down[e]
+ *   Wd_s       [E, d, f/32] scales
+ * Quantisation of a block with largest magnitude amax: scale exponent
+ * s = floor(log2(amax)) - 8, clamped to [-127, 127] (-127 for an all-zero
+ * block); each element is x * 2^-s clamped to +-448 and rounded to the
+ * nearest E4M3 value, ties to even (a negative value that rounds to zero
+ * keeps its sign). */
+typedef struct {
+    uint8_t *Wg_q, *Wu_q, *Wd_q;
+    uint8_t *Wg_s, *Wu_s, *Wd_s;
+} moe_mx_weights;
 
 /* Optional per-stage timing.  When a moe_stage_events pointer is passed to
  * moe_forward / moe_backward, ev[i] (a hipEvent_t, or NULL to skip) is
@@ -192,6 +216,40 @@ size_t moe_schedule_workspace_bytes(int64_t R, int64_t NK, int64_t L);
 moe_status moe_schedule(int64_t R, int64_t NK, int64_t L, int64_t c, const int32_t *A,
                         int32_t *M, int32_t *S, int32_t *phi, int64_t phi_rows, void *ws,
                         size_t ws_bytes, moe_stream stream);
+
+/* MXFP8 weight pre-quantisation (§3.4 "MXFP8 Support": weights are
+ * quantised ahead of time by a dedicated kernel).  Reads W_gate, W_up,
+ * W_down of `weights` (the shared-expert pointers are ignored) and writes
+ * every array of `mx` (layouts above; caller-owned device memory).  Extra
+ * limits: T*d, T*k*f and E*f*d below 2^32 (MOE_EUNSUPPORTED). */
+moe_status moe_mx_quantize_weights(const moe_shape *shape, const moe_weights *weights,
+                                   const moe_mx_weights *mx, moe_stream stream);
+
+/* Workspace bytes of moe_forward_mx (it also serves moe_route and moe_plan);
+ * 0 for an invalid or unsupported shape.  Pure host function. */
+size_t moe_mx_workspace_bytes(const moe_shape *shape);
+
+/* Byte offset and size of a region of the MXFP8 forward workspace: only
+ * MOE_WS_ERROR, MOE_WS_YEXP, MOE_WS_YSH, MOE_WS_XQ, MOE_WS_XS, MOE_WS_HQ and
+ * MOE_WS_HS exist there (MOE_EINVAL for the others). */
+moe_status moe_mx_workspace_region(const moe_shape *shape, moe_ws_tensor which, size_t *offset,
+                                   size_t *bytes);
+
+/* Forward of the layer with MXFP8 routed experts and a BF16 shared expert
+ * (§3.4 "MXFP8 Support").  As moe_forward, except:
+ *   - X is quantised once per token (32-blocks along d) before the routed
+ *     up/gate GEMM reads it through the plan;
+ *   - the routed GEMMs run on E4M3 x E4M3 block-scaled matrix cores with
+ *     fp32 accumulation, on the weights in `mx`;
+ *   - the gated activation H is quantised along f (32-blocks) straight from
+ *     fp32 in the up/gate epilogue, and Yexp is rounded to bf16;
+ *   - `weights` supplies only the shared expert (its routed pointers are
+ *     ignored and may be NULL); nothing is kept for a backward pass.
+ * Y [T, d] bf16 out.  ws: at least moe_mx_workspace_bytes(shape) bytes. */
+moe_status moe_forward_mx(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
+                          const moe_mx_weights *mx, const int32_t *topk_idx, const float *topk_w,
+                          const moe_plan_bufs *plan, moe_bf16 *Y, void *ws, size_t ws_bytes,
+                          moe_stream stream, const moe_stage_events *events /* NULL = no timing */);
 
 /* Materialised dispatch (§3.1 "Scheduling", local part): Xperm[p] =
  * X[perm[p] / k] for p < T*k.  moe_forward does not need it (its GEMMs read

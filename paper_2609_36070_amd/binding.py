@@ -20,10 +20,12 @@ c_int = ctypes.c_int
 
 MOE_OK, MOE_EINVAL, MOE_EUNSUPPORTED, MOE_ENOSPACE, MOE_EHIP = range(5)
 WS_ERROR, WS_A, WS_B, WS_H, WS_YEXP, WS_YSH, WS_DG, WS_DA, WS_DB, WS_DXPERM = range(10)
+WS_XQ, WS_XS, WS_HQ, WS_HS = range(10, 14)
 
 EXPORTS = ("moe_workspace_bytes", "moe_workspace_region", "moe_route", "moe_plan",
            "moe_schedule_workspace_bytes", "moe_schedule", "moe_dispatch", "moe_forward",
-           "moe_backward", "moe_status_string", "moe_version")
+           "moe_backward", "moe_mx_quantize_weights", "moe_mx_workspace_bytes",
+           "moe_mx_workspace_region", "moe_forward_mx", "moe_status_string", "moe_version")
 
 
 class MoeShape(ctypes.Structure):
@@ -33,6 +35,10 @@ class MoeShape(ctypes.Structure):
 
 class MoeWeights(ctypes.Structure):
     _fields_ = [(n, c_void_p) for n in ("W_gate", "W_up", "W_down", "Wg_s", "Wu_s", "Wd_s")]
+
+
+class MoeMxWeights(ctypes.Structure):
+    _fields_ = [(n, c_void_p) for n in ("Wg_q", "Wu_q", "Wd_q", "Wg_s", "Wu_s", "Wd_s")]
 
 
 class MoePlanBufs(ctypes.Structure):
@@ -71,7 +77,8 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise FileNotFoundError(
                 f"{LIB_PATH} not found: build it with python -m paper_2609_36070_amd.build")
-        L = ctypes.CDLL(LIB_PATH)
+        # bind every symbol now: a missing kernel stub fails here, not at a launch
+        L = ctypes.CDLL(LIB_PATH, mode=os.RTLD_NOW | os.RTLD_LOCAL)
         P = ctypes.POINTER
         L.moe_workspace_bytes.argtypes = [P(MoeShape), c_int]
         L.moe_workspace_bytes.restype = c_size_t
@@ -89,8 +96,17 @@ def lib():
         L.moe_backward.argtypes = [P(MoeShape), c_void_p, c_void_p, c_void_p, P(MoeWeights),
                                    c_void_p, c_void_p, P(MoePlanBufs), c_void_p, P(MoeGrads),
                                    c_void_p, c_size_t, c_void_p, P(MoeStageEvents)]
+        L.moe_mx_quantize_weights.argtypes = [P(MoeShape), P(MoeWeights), P(MoeMxWeights),
+                                              c_void_p]
+        L.moe_mx_workspace_bytes.argtypes = [P(MoeShape)]
+        L.moe_mx_workspace_bytes.restype = c_size_t
+        L.moe_mx_workspace_region.argtypes = [P(MoeShape), c_int, P(c_size_t), P(c_size_t)]
+        L.moe_forward_mx.argtypes = [P(MoeShape), c_void_p, P(MoeWeights), P(MoeMxWeights),
+                                     c_void_p, c_void_p, P(MoePlanBufs), c_void_p, c_void_p,
+                                     c_size_t, c_void_p, P(MoeStageEvents)]
         for fn in ("moe_route", "moe_plan", "moe_schedule", "moe_dispatch", "moe_forward",
-                   "moe_backward", "moe_workspace_region"):
+                   "moe_backward", "moe_workspace_region", "moe_mx_quantize_weights",
+                   "moe_mx_workspace_region", "moe_forward_mx"):
             getattr(L, fn).restype = c_int
         L.moe_status_string.argtypes = [c_int]
         L.moe_status_string.restype = ctypes.c_char_p
@@ -189,6 +205,39 @@ def moe_schedule(R, NK, L, c, A, M, S, phi, phi_rows, ws, ws_bytes=None, stream=
     st = lib().moe_schedule(R, NK, L, c, _p(A), _p(M), _p(S), _p(phi), phi_rows, _p(ws), nbytes,
                             _stream(stream))
     return _check("moe_schedule", st, raise_on_error)
+
+
+def mx_weights_struct(Wg_q, Wu_q, Wd_q, Wg_s, Wu_s, Wd_s) -> MoeMxWeights:
+    return MoeMxWeights(_p(Wg_q), _p(Wu_q), _p(Wd_q), _p(Wg_s), _p(Wu_s), _p(Wd_s))
+
+
+def moe_mx_workspace_bytes(shape: MoeShape) -> int:
+    return int(lib().moe_mx_workspace_bytes(ctypes.byref(shape)))
+
+
+def moe_mx_workspace_region(shape: MoeShape, which: int):
+    off, nb = c_size_t(0), c_size_t(0)
+    st = lib().moe_mx_workspace_region(ctypes.byref(shape), which, ctypes.byref(off),
+                                       ctypes.byref(nb))
+    _check("moe_mx_workspace_region", st, True)
+    return off.value, nb.value
+
+
+def moe_mx_quantize_weights(shape, weights: MoeWeights, mx: MoeMxWeights, stream=None,
+                            raise_on_error=True):
+    st = lib().moe_mx_quantize_weights(ctypes.byref(shape), ctypes.byref(weights),
+                                       ctypes.byref(mx), _stream(stream))
+    return _check("moe_mx_quantize_weights", st, raise_on_error)
+
+
+def moe_forward_mx(shape, X, weights: MoeWeights, mx: MoeMxWeights, topk_idx, topk_w,
+                   plan: MoePlanBufs, Y, ws, ws_bytes=None, stream=None, raise_on_error=True,
+                   events: MoeStageEvents = None):
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    st = lib().moe_forward_mx(ctypes.byref(shape), _p(X), ctypes.byref(weights), ctypes.byref(mx),
+                              _p(topk_idx), _p(topk_w), ctypes.byref(plan), _p(Y), _p(ws), nbytes,
+                              _stream(stream), None if events is None else ctypes.byref(events))
+    return _check("moe_forward_mx", st, raise_on_error)
 
 
 def moe_dispatch(shape, X, plan: MoePlanBufs, Xperm, stream=None, raise_on_error=True):

@@ -28,7 +28,8 @@ FLAGS = [
     "-Wno-unused-command-line-argument",
     f"-I{os.path.join(ROOT, 'include')}",
 ] + os.environ.get("MOE_HIPCC_EXTRA", "").split()
-SOURCES = ["route.hip", "plan.hip", "schedule.hip", "movement.hip", "gemm.hip", "api.cpp"]
+SOURCES = ["route.hip", "plan.hip", "schedule.hip", "movement.hip", "gemm.hip", "mx.hip",
+           "gemm_mx.hip", "api.cpp"]
 
 
 def _compile(src: str) -> str:

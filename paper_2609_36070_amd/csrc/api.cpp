@@ -22,6 +22,8 @@ struct Layout {
     size_t fwd_total;
     size_t dA, dB, Hw, dgpart, dg, dZ, dXperm, dAs, dBs, dXsh, dwr_part;
     size_t bwd_total;
+    size_t xq, xs, hq, hsc;   // MXFP8 forward: quantised X and H (over the backward regions)
+    size_t mx_total;
     int dg_parts;
 };
 
@@ -63,6 +65,12 @@ Layout make_layout(const moe_shape &s) {
     L.dXsh = take(T * d * 2);
     L.dwr_part = take((size_t)dwr_nchunks((long)T) * d * E * 4);
     L.bwd_total = o;
+    o = L.fwd_total;
+    L.xq = take(T * d);
+    L.xs = take(T * d / 32);
+    L.hq = take(R * f);
+    L.hsc = take(R * f / 32);
+    L.mx_total = o;
     return L;
 }
 
@@ -139,6 +147,28 @@ SchedLayout schedule_layout(int64_t R, int64_t NK, int64_t L) {
 template <typename T>
 T *at(void *ws, size_t off) { return reinterpret_cast<T *>(static_cast<char *>(ws) + off); }
 
+// MXFP8 path: every fp8 operand is addressed with 32-bit offsets.
+moe_status check_mx_shape(const moe_shape *s) {
+    const int64_t lim = int64_t(1) << 32;
+    if (s->T * s->d >= lim || s->T * s->k * s->f >= lim || s->E * s->f * s->d >= lim)
+        return MOE_EUNSUPPORTED;
+    return MOE_OK;
+}
+
+moe_status check_mx_weights(const moe_shape *s, const moe_weights *w, const moe_mx_weights *q) {
+    if (!w || !q) return MOE_EINVAL;
+    if (!ptr_ok(q->Wg_q) || !ptr_ok(q->Wu_q) || !ptr_ok(q->Wd_q) || !ptr_ok(q->Wg_s) ||
+        !ptr_ok(q->Wu_s) || !ptr_ok(q->Wd_s))
+        return MOE_EINVAL;
+    const bool any = w->Wg_s || w->Wu_s || w->Wd_s;
+    if (s->f_shared > 0) {
+        if (!ptr_ok(w->Wg_s) || !ptr_ok(w->Wu_s) || !ptr_ok(w->Wd_s)) return MOE_EINVAL;
+    } else if (any) {
+        return MOE_EINVAL;
+    }
+    return MOE_OK;
+}
+
 // Records stage event i (if requested) on the stream.
 struct StageMarks {
     const moe_stage_events *ev;
@@ -153,6 +183,33 @@ struct StageMarks {
     do {                                                   \
         if ((expr) != hipSuccess) return MOE_EHIP;         \
     } while (0)
+
+// Shared expert (BF16 in both precisions): up/gate + SwiGLU into Hs, then
+// down into Ysh.
+hipError_t shared_up(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *X,
+                     const moe_weights *w, bool save, hipStream_t s) {
+    const int T = (int)sh.T, d = (int)sh.d, fs = (int)sh.f_shared;
+    GemmArgs g;
+    g.zeros = at<uint16_t>(ws, L.zeros);
+    g.A = X; g.lda = d; g.a_nrows = T > 0 ? T : 1; g.M = T;
+    g.B = w->Wg_s; g.B2 = w->Wu_s; g.ldb = fs;
+    g.N = fs; g.K = d;
+    g.C = at<uint16_t>(ws, L.Hs); g.ldc = fs;
+    if (save) { g.C2 = at<uint16_t>(ws, L.As); g.C3 = at<uint16_t>(ws, L.Bs); }
+    return launch_gemm_fwd_up(g, T, 1, s);
+}
+
+hipError_t shared_down(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w,
+                       hipStream_t s) {
+    const int T = (int)sh.T, d = (int)sh.d, fs = (int)sh.f_shared;
+    GemmArgs g;
+    g.zeros = at<uint16_t>(ws, L.zeros);
+    g.A = at<uint16_t>(ws, L.Hs); g.lda = fs; g.a_nrows = T > 0 ? T : 1; g.M = T;
+    g.B = w->Wd_s; g.ldb = d;
+    g.N = d; g.K = fs;
+    g.C = at<uint16_t>(ws, L.Ysh); g.ldc = d;
+    return launch_gemm_fwd_down(g, T, 1, s);
+}
 
 }  // namespace
 
@@ -288,16 +345,7 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
         MOE_TRY(launch_gemm_fwd_up(g, R, E, s));
     }
     MOE_TRY(mk.mark(2));
-    if (fs > 0) {   // shared up/gate + SwiGLU
-        GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
-        g.A = X; g.lda = d; g.a_nrows = T > 0 ? T : 1; g.M = T;
-        g.B = weights->Wg_s; g.B2 = weights->Wu_s; g.ldb = fs;
-        g.N = fs; g.K = d;
-        g.C = at<uint16_t>(ws, L.Hs); g.ldc = fs;
-        if (save_for_backward) { g.C2 = at<uint16_t>(ws, L.As); g.C3 = at<uint16_t>(ws, L.Bs); }
-        MOE_TRY(launch_gemm_fwd_up(g, T, 1, s));
-    }
+    if (fs > 0) MOE_TRY(shared_up(*shape, L, ws, X, weights, save_for_backward != 0, s));
     MOE_TRY(mk.mark(3));
     {   // routed down
         GemmArgs g;
@@ -309,15 +357,7 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
         MOE_TRY(launch_gemm_fwd_down(g, R, E, s));
     }
     MOE_TRY(mk.mark(4));
-    if (fs > 0) {   // shared down
-        GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
-        g.A = at<uint16_t>(ws, L.Hs); g.lda = fs; g.a_nrows = T > 0 ? T : 1; g.M = T;
-        g.B = weights->Wd_s; g.ldb = d;
-        g.N = d; g.K = fs;
-        g.C = at<uint16_t>(ws, L.Ysh); g.ldc = d;
-        MOE_TRY(launch_gemm_fwd_down(g, T, 1, s));
-    }
+    if (fs > 0) MOE_TRY(shared_down(*shape, L, ws, weights, s));
     MOE_TRY(mk.mark(5));
     MOE_TRY(launch_combine(at<uint16_t>(ws, L.Yexp), fs > 0 ? at<uint16_t>(ws, L.Ysh) : nullptr,
                            topk_w, plan->route_pos, T, d, k, Y, s));
@@ -467,6 +507,115 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
     MOE_TRY(launch_reverse_combine(at<uint16_t>(ws, L.dXperm), dXsh, dZ, W_r, plan->route_pos, T, d,
                                    k, E, dX, s));
     MOE_TRY(mk.mark(11));
+    return MOE_OK;
+}
+
+size_t moe_mx_workspace_bytes(const moe_shape *shape) {
+    if (check_shape(shape) != MOE_OK || check_mx_shape(shape) != MOE_OK) return 0;
+    return make_layout(*shape).mx_total;
+}
+
+moe_status moe_mx_workspace_region(const moe_shape *shape, moe_ws_tensor which, size_t *offset,
+                                   size_t *bytes) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if ((st = check_mx_shape(shape)) != MOE_OK) return st;
+    if (!offset || !bytes) return MOE_EINVAL;
+    const Layout L = make_layout(*shape);
+    const size_t R = (size_t)(shape->T * shape->k);
+    const size_t T = shape->T, d = shape->d, f = shape->f;
+    switch (which) {
+        case MOE_WS_ERROR: *offset = L.err; *bytes = 4; break;
+        case MOE_WS_YEXP: *offset = L.Yexp; *bytes = R * d * 2; break;
+        case MOE_WS_YSH: *offset = L.Ysh; *bytes = T * d * 2; break;
+        case MOE_WS_XQ: *offset = L.xq; *bytes = T * d; break;
+        case MOE_WS_XS: *offset = L.xs; *bytes = T * d / 32; break;
+        case MOE_WS_HQ: *offset = L.hq; *bytes = R * f; break;
+        case MOE_WS_HS: *offset = L.hsc; *bytes = R * f / 32; break;
+        default: return MOE_EINVAL;
+    }
+    return MOE_OK;
+}
+
+moe_status moe_mx_quantize_weights(const moe_shape *shape, const moe_weights *weights,
+                                   const moe_mx_weights *mx, moe_stream stream) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if ((st = check_mx_shape(shape)) != MOE_OK) return st;
+    if (!weights || !ptr_ok(weights->W_gate) || !ptr_ok(weights->W_up) || !ptr_ok(weights->W_down))
+        return MOE_EINVAL;
+    if (!mx || !ptr_ok(mx->Wg_q) || !ptr_ok(mx->Wu_q) || !ptr_ok(mx->Wd_q) || !ptr_ok(mx->Wg_s) ||
+        !ptr_ok(mx->Wu_s) || !ptr_ok(mx->Wd_s))
+        return MOE_EINVAL;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int E = (int)shape->E, d = (int)shape->d, f = (int)shape->f;
+    MOE_TRY(launch_mx_quant_weights(weights->W_gate, E, d, f, mx->Wg_q, mx->Wg_s, s));
+    MOE_TRY(launch_mx_quant_weights(weights->W_up, E, d, f, mx->Wu_q, mx->Wu_s, s));
+    MOE_TRY(launch_mx_quant_weights(weights->W_down, E, f, d, mx->Wd_q, mx->Wd_s, s));
+    return MOE_OK;
+}
+
+moe_status moe_forward_mx(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
+                          const moe_mx_weights *mx, const int32_t *topk_idx, const float *topk_w,
+                          const moe_plan_bufs *plan, moe_bf16 *Y, void *ws, size_t ws_bytes,
+                          moe_stream stream, const moe_stage_events *events) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if ((st = check_mx_shape(shape)) != MOE_OK) return st;
+    if (!ptr_ok(X) || !ptr_ok(topk_idx) || !ptr_ok(topk_w) || !ptr_ok(Y)) return MOE_EINVAL;
+    if ((st = check_mx_weights(shape, weights, mx)) != MOE_OK) return st;
+    if ((st = check_plan(plan)) != MOE_OK) return st;
+    if (!ptr_ok(ws)) return MOE_EINVAL;
+    const Layout L = make_layout(*shape);
+    if (ws_bytes < L.mx_total) return MOE_ENOSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int T = (int)shape->T, d = (int)shape->d, E = (int)shape->E, k = (int)shape->k;
+    const int f = (int)shape->f, fs = (int)shape->f_shared;
+    const long R = (long)T * k;
+    int *rowidx = at<int>(ws, L.rowidx);
+    uint8_t *xq = at<uint8_t>(ws, L.xq), *xs = at<uint8_t>(ws, L.xs);
+    uint8_t *hq = at<uint8_t>(ws, L.hq), *hs = at<uint8_t>(ws, L.hsc);
+    const StageMarks mk{events, s};
+
+    MOE_TRY(mk.mark(0));
+    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, rowidx, at<float>(ws, L.wperm),
+                        at<uint16_t>(ws, L.zeros), s));
+    // activation quantisation of the dispatch: each token once, before the gather
+    MOE_TRY(launch_mx_quant_rows(X, T, d, xq, xs, s));
+    MOE_TRY(mk.mark(1));
+    {   // routed up/gate + SwiGLU, H quantised in the epilogue
+        MxGemmArgs g;
+        g.A = xq; g.As = xs; g.a_rows = rowidx; g.a_nrows = T > 0 ? T : 1;
+        g.B = mx->Wg_q; g.Bs = mx->Wg_s; g.B2 = mx->Wu_q; g.Bs2 = mx->Wu_s;
+        g.K = d; g.N = f; g.offsets = plan->offsets; g.E = E;
+        g.C = hq; g.Cs = hs;
+        g.a_bytes = (uint32_t)((long)(T > 0 ? T : 1) * d);
+        g.as_bytes = (uint32_t)((long)(T > 0 ? T : 1) * d / 32);
+        g.b_bytes = (uint32_t)((long)E * f * d);
+        g.bs_bytes = (uint32_t)((long)E * f * d / 32);
+        MOE_TRY(launch_gemm_mx_up(g, R, E, s));
+    }
+    MOE_TRY(mk.mark(2));
+    if (fs > 0) MOE_TRY(shared_up(*shape, L, ws, X, weights, false, s));
+    MOE_TRY(mk.mark(3));
+    {   // routed down
+        MxGemmArgs g;
+        g.A = hq; g.As = hs; g.a_nrows = R > 0 ? (int)R : 1;
+        g.B = mx->Wd_q; g.Bs = mx->Wd_s;
+        g.K = f; g.N = d; g.offsets = plan->offsets; g.E = E;
+        g.Cb = at<uint16_t>(ws, L.Yexp);
+        g.a_bytes = (uint32_t)((R > 0 ? R : 1) * f);
+        g.as_bytes = (uint32_t)((R > 0 ? R : 1) * f / 32);
+        g.b_bytes = (uint32_t)((long)E * d * f);
+        g.bs_bytes = (uint32_t)((long)E * d * f / 32);
+        MOE_TRY(launch_gemm_mx_down(g, R, E, s));
+    }
+    MOE_TRY(mk.mark(4));
+    if (fs > 0) MOE_TRY(shared_down(*shape, L, ws, weights, s));
+    MOE_TRY(mk.mark(5));
+    MOE_TRY(launch_combine(at<uint16_t>(ws, L.Yexp), fs > 0 ? at<uint16_t>(ws, L.Ysh) : nullptr,
+                           topk_w, plan->route_pos, T, d, k, Y, s));
+    MOE_TRY(mk.mark(6));
     return MOE_OK;
 }
 

@@ -1,0 +1,403 @@
+// Grouped MXFP8 GEMMs of the routed experts (§3.4 "MXFP8 Support") on the
+// gfx950 block-scaled MFMA v_mfma_scale_f32_32x32x64_f8f6f4 (E4M3 x E4M3,
+// fp32 accumulation).  Per expert e and buffer positions p of e's region:
+//
+//   MX_UP    g = Xq[tok(p)] . Wg_q[e][n], u = Xq[tok(p)] . Wu_q[e][n];
+//            H = silu(g) * u, quantised to MXFP8 along f (the activation
+//            quantisation fused into the gated activation) -> Hq, Hs
+//   MX_DOWN  Yexp = Hq[p] . Wd_q[e][n] -> bf16
+//
+// Every operand is a matrix of K-contiguous byte rows (A: token or position
+// rows; B: one row per output column, the pre-quantised weight layout) with
+// one E8M0 scale byte per row per 32 k.  The MFMA takes each row's two
+// 32-blocks of a 64-wide k step as bytes 0-15 (block 0) and 16-31 (block 1)
+// of every lane, lane l serving row l % 32 and supplying the scale of block
+// l / 32; a lane therefore reads k [16h, 16h + 16) and [32 + 16h, 48 + 16h)
+// of its row (h = l / 32), which matches what the other operand holds.
+//
+// Pipeline as in the BF16 kernels: 256 x 256 block tile, K step 128 bytes,
+// two LDS stages filled by direct global->LDS loads (128-byte rows, chunk
+// XOR (row >> 1) & 7), 8 waves of 128 x 64, fragments double-buffered in
+// registers, tiles rastered XCD-aware.  Scale words (4 blocks of a row per K
+// step) are loaded into registers one step ahead, together with the tiles.
+#include "common.h"
+#include "kernels.h"
+#include "mx_common.h"
+
+#define LDSP __attribute__((address_space(3)))
+
+namespace {
+
+constexpr int BM = 256, BN = 256, BK = 128;
+#ifndef MOE_MX_WAVES_N
+#define MOE_MX_WAVES_N 2
+#endif
+// 2 x 2 waves of 128 x 128 (one wave per SIMD, accumulators in AGPRs) by
+// default: at 2 waves per SIMD the 128 accumulators of a 128 x 64 wave tile
+// leave too few registers for the fp8 fragments, scale words and addresses.
+constexpr int WAVES_M = 2, WAVES_N = MOE_MX_WAVES_N, NWAVES = WAVES_M * WAVES_N;
+constexpr int NTHREADS = 64 * NWAVES;
+constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N, TM = WM / 32, TN = WN / 32;
+constexpr int TILE = BM * BK;                      // bytes per operand per stage
+constexpr int LD_PER_OP = TILE / 1024 / NWAVES;    // 1 KB direct loads per operand per wave per step
+static_assert(WN == 64 || WN == 128, "gate/up column pairs need 64- or 128-column wave tiles");
+
+enum MxMode { MX_UP = 0, MX_DOWN = 1 };
+
+typedef int i32x8_t __attribute__((ext_vector_type(8)));
+
+DEV int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
+
+DEV int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Raw buffer resource over [p, p + bytes) (gfx9 word 3: 32-bit data format).
+DEV __amdgpu_buffer_rsrc_t make_rsrc(const void *p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+DEV void barrier_no_fence() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+template <int N>
+DEV void wait_vmcnt() {
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// MFMA operand for rows [r0, r0 + 32) at k step ks (64 wide) of a stage tile.
+DEV i32x8_t frag(const uint8_t *t, int r0, int ks, int lane) {
+    const int r = r0 + (lane & 31), h = lane >> 5;
+    const u32x4_t lo = ld_u32x4(t + r * BK + 16 * swz(r, 4 * ks + h));
+    const u32x4_t hi = ld_u32x4(t + r * BK + 16 * swz(r, 4 * ks + 2 + h));
+    return i32x8_t{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
+                   (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+}
+
+// XCD-aware raster (as in the BF16 kernels): each XCD gets a contiguous run of
+// a raster that walks groups of GM m-tiles with the m-tile fastest.
+DEV bool map_tile(int b, int nblocks, int tiles_m, int ntn, int &mt, int &nt) {
+    constexpr int NX = 8, GM = 4;
+    const int per = nblocks / NX;
+    const int l = (b % NX) * per + b / NX;
+    if (l >= tiles_m * ntn) return false;
+    const int group = l / (GM * ntn);
+    const int first = group * GM;
+    const int gm = min(GM, tiles_m - first);
+    const int within = l - group * GM * ntn;
+    mt = first + within % gm;
+    nt = within / gm;
+    return true;
+}
+
+template <int MODE>
+__global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, const int *__restrict__ a_rows) {
+    __shared__ __attribute__((aligned(16))) uint8_t lds_a0[TILE];
+    __shared__ __attribute__((aligned(16))) uint8_t lds_b0[TILE];
+    __shared__ __attribute__((aligned(16))) uint8_t lds_a1[TILE];
+    __shared__ __attribute__((aligned(16))) uint8_t lds_b1[TILE];
+    // scale words of the K step per stage: A tile rows; B tile columns (MX_UP:
+    // 128 gate then 128 up columns of the tile's f range)
+    __shared__ uint32_t sc_a0[BM], sc_b0[BN], sc_a1[BM], sc_b1[BN];
+    __shared__ int s_info[2];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+
+    // ---------------- tile: expert region and rows ----------------
+    const int ntn = (MODE == MX_UP) ? g.N / (BN / 2) : g.N / BN;
+    int mt = 0, ntile = 0;
+    if (!map_tile(blockIdx.x, gridDim.x, g.tiles_m, ntn, mt, ntile)) return;
+    const int n0 = ntile * ((MODE == MX_UP) ? BN / 2 : BN);
+    if (tid == 0) s_info[0] = -1;
+    __syncthreads();
+    if (tid < 64) {
+        int cum = 0;
+        for (int base = 0; base < g.E; base += 64) {
+            const int ee = base + lane;
+            const int cnt = ee < g.E ? g.offsets[ee + 1] - g.offsets[ee] : 0;
+            const int tiles = cnt > 0 ? (cnt + BM - 1) / BM : 0;
+            int x = tiles;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int y = __shfl_up(x, off, 64);
+                if (lane >= off) x += y;
+            }
+            const int excl = cum + x - tiles;
+            if (ee < g.E && mt >= excl && mt < excl + tiles) {
+                s_info[0] = ee;
+                s_info[1] = mt - excl;
+            }
+            cum += __shfl(x, 63, 64);
+        }
+    }
+    __syncthreads();
+    const int e = uniform(s_info[0]);
+    if (e < 0) return;
+    const int row0 = uniform(g.offsets[e] + uniform(s_info[1]) * BM);
+    const int row_end = uniform(g.offsets[e + 1]);
+    const long ks_row = g.K / 32;     // scale bytes per row
+
+    // physical A row of tile row r (rows past the region's end repeat its last
+    // row; their results are never stored)
+    auto a_phys = [&](int r) {
+        const int p = min(row0 + r, row_end - 1);
+        const int phys = a_rows ? a_rows[p] : p;
+        return min(max(phys, 0), g.a_nrows - 1);
+    };
+    // ---------------- direct-load set-up ----------------
+    // Every operand is read through a buffer resource (base and size in
+    // SGPRs): a load takes a 32-bit VGPR offset, the K step and any
+    // wave-uniform row offset go in the scalar offset, and the hardware
+    // returns zeros for any access past the operand's end.
+    // Tile load i of wave w is wave instruction q = LD_PER_OP w + i: 1 KB = 8
+    // rows of 128 bytes; lane -> row 8 q + lane / 8, physical chunk
+    // (lane & 7) ^ ((4 (q & 1) + lane / 16) & 7).  Rows of B (and of an
+    // ungathered A) are linear in q, so one VGPR per parity of q serves all
+    // loads; a gathered A needs one per load.
+    const __amdgpu_buffer_rsrc_t rA = make_rsrc(g.A, g.a_bytes);
+    const __amdgpu_buffer_rsrc_t rAs = make_rsrc(g.As, g.as_bytes);
+    // (B resources are built per load from the selected base: a conditional
+    // between two resource values is not accepted by the host compilation)
+    const int l8 = lane >> 3;
+    const uint32_t col_even = 16u * (uint32_t)((lane & 7) ^ ((l8 >> 1) & 7));
+    const uint32_t col_odd = 16u * (uint32_t)((lane & 7) ^ ((4 + (l8 >> 1)) & 7));
+    const uint32_t K = (uint32_t)g.K;
+    const uint32_t b_lane_even = (uint32_t)l8 * K + col_even, b_lane_odd = (uint32_t)l8 * K + col_odd;
+    constexpr bool GATHER = (MODE == MX_UP);
+    uint32_t a_off[LD_PER_OP];   // gathered A only
+#pragma unroll
+    for (int i = 0; i < LD_PER_OP; ++i) {
+        const int q = LD_PER_OP * wave + i;
+        a_off[i] = GATHER ? (uint32_t)a_phys(8 * q + l8) * K + ((q & 1) ? col_odd : col_even) : 0u;
+    }
+    // scale DMA: 8 instructions of 64 words per K step (A rows 64 c + lane for
+    // c < 4; B words 64 (c - 4) + lane), spread over the waves
+    constexpr int SC_PER_WAVE = 8 / NWAVES;
+    uint32_t sc_off[SC_PER_WAVE];
+#pragma unroll
+    for (int i = 0; i < SC_PER_WAVE; ++i) {
+        const int c = SC_PER_WAVE * wave + i;
+        if (c < 4) {
+            sc_off[i] = (uint32_t)a_phys(64 * c + lane) * (uint32_t)ks_row;
+        } else {
+            const int wd = 64 * (c - 4) + lane;               // B scale word
+            const uint32_t brow = (MODE == MX_UP) ? (uint32_t)(e * g.N + n0 + (wd & 127))
+                                                  : (uint32_t)(e * g.N + n0 + wd);
+            sc_off[i] = brow * (uint32_t)ks_row;
+        }
+    }
+
+    const int nk = g.K / BK;
+    auto issue = [&](int kt, uint8_t *la, uint8_t *lb, uint32_t *sa, uint32_t *sb) {
+        const uint32_t kb = (uint32_t)kt * BK;
+#pragma unroll
+        for (int i = 0; i < LD_PER_OP; ++i) {
+            const int q = LD_PER_OP * wave + i;
+            if constexpr (GATHER) {
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (LDSP void *)(la + q * 1024), 16, a_off[i],
+                                                         kb, 0, 0);
+            } else {
+                // rows past the region (or the operand) hold results that are never stored
+                const uint32_t arow = (uint32_t)(row0 + 8 * q);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (LDSP void *)(la + q * 1024), 16,
+                                                         (q & 1) ? b_lane_odd : b_lane_even,
+                                                         arow * K + kb, 0, 0);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < LD_PER_OP; ++i) {
+            const int q = LD_PER_OP * wave + i;
+            // B row of instruction q less the lane part l8 (uniform); MX_UP: tile
+            // rows 8 q .. 8 q + 7 lie in column group q / 4, gate or up
+            const bool up = (MODE == MX_UP) && ((q >> 2) & 1);
+            const uint32_t brow = (MODE == MX_UP)
+                ? (uint32_t)(e * g.N + n0 + (q >> 3) * 32 + 8 * (q & 3))
+                : (uint32_t)(e * g.N + n0 + 8 * q);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(up ? g.B2 : g.B, g.b_bytes),
+                                                     (LDSP void *)(lb + q * 1024), 16,
+                                                     (q & 1) ? b_lane_odd : b_lane_even,
+                                                     brow * K + kb, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < SC_PER_WAVE; ++i) {
+            const int c = SC_PER_WAVE * wave + i;
+            if (c < 4) {
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rAs, (LDSP void *)(sa + 64 * c), 4, sc_off[i],
+                                                         4 * kt, 0, 0);
+            } else {
+                const bool up = (MODE == MX_UP) && (c - 4 >= 2);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(up ? g.Bs2 : g.Bs, g.bs_bytes),
+                                                         (LDSP void *)(sb + 64 * (c - 4)), 4,
+                                                         sc_off[i], 4 * kt, 0, 0);
+            }
+        }
+    };
+
+    f32x16_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+
+    const int h = lane >> 5;
+    auto compute = [&](const uint8_t *la, const uint8_t *lb, const uint32_t *sa, const uint32_t *sb) {
+        uint32_t wa[TM], wb[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) wa[i] = sa[wm * WM + 32 * i + (lane & 31)];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            // scale word of tile column wn WN + 32 j + lane % 32 (MX_UP: gate words
+            // 0..127, up words 128..255 of the tile's f range)
+            const int wd = (MODE == MX_UP) ? (j & 1) * 128 + (wn * WN / 64 + j / 2) * 32 + (lane & 31)
+                                           : wn * WN + 32 * j + (lane & 31);
+            wb[j] = sb[wd];
+        }
+#pragma unroll
+        for (int ks = 0; ks < BK / 64; ++ks) {
+            // this lane's scales: block 2 ks + h of its row / column
+            const int sh = 8 * (2 * ks + h);
+            i32x8_t bfr[TN];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) bfr[j] = frag(lb, wn * WN + 32 * j, ks, lane);
+            // A fragments two at a time: more would not fit next to the
+            // accumulators
+#pragma unroll
+            for (int i0 = 0; i0 < TM; i0 += 2) {
+                __builtin_amdgcn_sched_barrier(0);
+                i32x8_t af[2];
+#pragma unroll
+                for (int ii = 0; ii < 2; ++ii) af[ii] = frag(la, wm * WM + 32 * (i0 + ii), ks, lane);
+#pragma unroll
+                for (int ii = 0; ii < 2; ++ii) {
+                    const int sai = (int)((wa[i0 + ii] >> sh) & 0xffu);
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) {
+                        const int sbj = (int)((wb[j] >> sh) & 0xffu);
+                        acc[i0 + ii][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                            af[ii], bfr[j], acc[i0 + ii][j], 0, 0, 0, sai, 0, sbj);
+                    }
+                }
+            }
+        }
+    };
+
+    // double-buffered K loop (stages named per half, as in the BF16 kernels)
+    if (nk > 0) issue(0, lds_a0, lds_b0, sc_a0, sc_b0);
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+        wait_vmcnt<0>();
+        barrier_no_fence();
+        issue(kt + 1, lds_a1, lds_b1, sc_a1, sc_b1);
+        asm volatile("" ::: "memory");
+        compute(lds_a0, lds_b0, sc_a0, sc_b0);
+        wait_vmcnt<0>();
+        barrier_no_fence();
+        if (kt + 2 < nk) issue(kt + 2, lds_a0, lds_b0, sc_a0, sc_b0);
+        asm volatile("" ::: "memory");
+        compute(lds_a1, lds_b1, sc_a1, sc_b1);
+    }
+    if (kt < nk) {
+        wait_vmcnt<0>();
+        barrier_no_fence();
+        compute(lds_a0, lds_b0, sc_a0, sc_b0);
+    }
+    __syncthreads();
+
+    // ---------------- epilogue ----------------
+    // accumulator layout: lane l, register q -> row 8 (q / 4) + 4 (l / 32) + q % 4,
+    // column l % 32; rows go through a per-wave LDS scratch (32 x WN fp32)
+    const int lrow = lane & 31, lhalf = lane >> 5;
+    constexpr int SP = WN + 4;
+    constexpr int WPA = NWAVES >= 4 ? NWAVES / 4 : 1;
+    uint8_t *scr_base = (wave / WPA) == 0 ? lds_a0 : (wave / WPA) == 1 ? lds_b0
+                      : (wave / WPA) == 2 ? lds_a1 : lds_b1;
+    float *scr = reinterpret_cast<float *>(scr_base) + (wave % WPA) * 32 * SP;
+    static_assert(WPA * 32 * SP * 4 <= TILE, "epilogue scratch fits a stage array");
+    auto stage = [&](int i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+                scr[(8 * (q >> 2) + 4 * lhalf + (q & 3)) * SP + 32 * j + lrow] = acc[i][j][q];
+    };
+    auto read8 = [&](int row, int c) {
+        const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(scr + row * SP + c);
+        const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(scr + row * SP + c + 4);
+        return f32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    };
+    if constexpr (MODE == MX_UP) {
+        // staged columns 64 jp + 0..31 hold the gate, 64 jp + 32..63 the up
+        // projection of the same 32 f columns: one MXFP8 block of H per row
+        // and pair, spread over 4 lanes
+        const long hs_row = g.N / 32;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            stage(i);
+#pragma unroll
+            for (int jp = 0; jp < TN / 2; ++jp) {
+                const long fcol0 = n0 + (wn * WN / 64 + jp) * 32;
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {
+                    const int row = (lane >> 2) + 16 * t, c = 8 * (lane & 3);
+                    const int p = row0 + wm * WM + 32 * i + row;
+                    const f32x8 a = read8(row, 64 * jp + c), b = read8(row, 64 * jp + 32 + c);
+                    float hv[8];
+                    float amax = 0.f;
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        hv[k] = silu_f(a[k]) * b[k];
+                        amax = fmaxf(amax, fabsf(hv[k]));
+                    }
+                    amax = fmaxf(amax, shfl_xor_f(amax, 1));
+                    amax = fmaxf(amax, shfl_xor_f(amax, 2));
+                    const int s = mx_shared_exp(amax);
+                    if (p < row_end) {
+                        *reinterpret_cast<u32x2_t *>(g.C + (long)p * g.N + fcol0 + c) =
+                            e4m3_pack8(hv, s);
+                        if ((lane & 3) == 0) g.Cs[(long)p * hs_row + fcol0 / 32] = (uint8_t)(s + 127);
+                    }
+                }
+            }
+        }
+    } else {
+        constexpr int LPR = WN / 8, RPP = 64 / LPR;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            stage(i);
+#pragma unroll
+            for (int t = 0; t < 32 / RPP; ++t) {
+                const int row = lane / LPR + RPP * t, c = 8 * (lane % LPR);
+                const int p = row0 + wm * WM + 32 * i + row;
+                const f32x8 v = read8(row, c);
+                if (p < row_end)
+                    st_u32x4(g.Cb + (long)p * g.N + n0 + wn * WN + c, pack_bf8(v));
+            }
+        }
+    }
+}
+
+template <int MODE>
+hipError_t launch_mx_mode(MxGemmArgs g, int tiles_m, int ntn, hipStream_t st) {
+    const long tiles = (long)tiles_m * ntn;
+    if (tiles <= 0) return hipSuccess;
+    g.tiles_m = tiles_m;
+    const unsigned grid = (unsigned)((tiles + 7) / 8 * 8);
+    gemm_mx_kernel<MODE><<<dim3(grid), dim3(NTHREADS), 0, st>>>(g, g.a_rows);
+    return hipGetLastError();
+}
+
+int mx_mtiles(long rows, int groups) { return (int)(rows / BM + (groups > 0 ? groups : 1)); }
+
+}  // namespace
+
+hipError_t launch_gemm_mx_up(const MxGemmArgs &g, long rows, int groups, hipStream_t st) {
+    return launch_mx_mode<MX_UP>(g, mx_mtiles(rows, groups), g.N / (BN / 2), st);
+}
+hipError_t launch_gemm_mx_down(const MxGemmArgs &g, long rows, int groups, hipStream_t st) {
+    return launch_mx_mode<MX_DOWN>(g, mx_mtiles(rows, groups), g.N / BN, st);
+}

@@ -61,6 +61,32 @@ hipError_t launch_plan(const int *topk_idx, int R, int E, int *counts, int *offs
                        hipStream_t st);
 
 constexpr int SCHED_MAX_TABLE = 8192;  // L * (R rounded up to 4): the count table staged in LDS
+// MXFP8 routed-expert GEMM problem (see gemm_mx.hip).
+struct MxGemmArgs {
+    const uint8_t *A = nullptr;        // [a_nrows][K] E4M3 rows
+    const uint8_t *As = nullptr;       // [a_nrows][K/32] E8M0 scales
+    const int *a_rows = nullptr;       // position -> A row (NULL: identity)
+    int a_nrows = 1;
+    const uint8_t *B = nullptr;        // [E][N or N/2][K] weight rows (gate for MX_UP)
+    const uint8_t *Bs = nullptr;
+    const uint8_t *B2 = nullptr;       // up weight rows (MX_UP)
+    const uint8_t *Bs2 = nullptr;
+    int K = 0, N = 0;                  // MX_UP: N = f (tile columns pair gate and up)
+    const int *offsets = nullptr;      // [E+1] expert regions
+    int E = 0;
+    uint8_t *C = nullptr;              // MX_UP: Hq [rows][N]
+    uint8_t *Cs = nullptr;             // MX_UP: Hs [rows][N/32]
+    uint16_t *Cb = nullptr;            // MX_DOWN: bf16 [rows][N]
+    uint32_t a_bytes = 0, as_bytes = 0, b_bytes = 0, bs_bytes = 0;   // operand extents (< 4 GiB)
+    int tiles_m = 0;
+};
+hipError_t launch_gemm_mx_up(const MxGemmArgs &g, long rows, int groups, hipStream_t st);
+hipError_t launch_gemm_mx_down(const MxGemmArgs &g, long rows, int groups, hipStream_t st);
+hipError_t launch_mx_quant_rows(const uint16_t *X, long rows, int K, uint8_t *q, uint8_t *sc,
+                                hipStream_t st);
+hipError_t launch_mx_quant_weights(const uint16_t *W, int E, int K, int N, uint8_t *q, uint8_t *sc,
+                                   hipStream_t st);
+
 int sched_nchunks(long NK);
 int sched_rpad(int R);
 hipError_t launch_schedule(const int *A, int R, int NK, int L, int c, int *M, int *S, int *phi,

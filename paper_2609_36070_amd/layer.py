@@ -31,8 +31,9 @@ def _dev_bf16(a, device):
 class DeviceLayer:
     """All tensors of one layer instance on the GPU, laid out as the C ABI expects."""
 
-    def __init__(self, w: Workload, inputs: dict, device="cuda", with_backward=None):
+    def __init__(self, w: Workload, inputs: dict, device="cuda", with_backward=None, mx=False):
         self.w = w
+        self.mx = mx
         self.device = torch.device(device)
         self.with_backward = w.backward if with_backward is None else with_backward
         T, d, E, k, f, fs = w.T, w.d, w.E, w.k, w.f, w.f_s
@@ -63,6 +64,11 @@ class DeviceLayer:
         nbytes = B.moe_workspace_bytes(self.shape, self.with_backward)
         if nbytes == 0:
             raise ValueError(f"unsupported shape {w}")
+        if mx:
+            mx_bytes = B.moe_mx_workspace_bytes(self.shape)
+            if mx_bytes == 0:
+                raise ValueError(f"shape unsupported in MXFP8 {w}")
+            nbytes = max(nbytes, mx_bytes)
         self.ws = torch.empty((nbytes,), dtype=torch.uint8, device=dev)
         self.weights = B.weights_struct(self.W_gate, self.W_up, self.W_down,
                                         self.Wg_s, self.Wu_s, self.Wd_s)
@@ -83,6 +89,18 @@ class DeviceLayer:
             self.grads = B.grads_struct(self.dW_gate, self.dW_up, self.dW_down, self.dW_r, self.dZ,
                                         self.dWg_s, self.dWu_s, self.dWd_s)
 
+        if mx:
+            u8 = torch.uint8
+            self.Wg_q = torch.empty((E, f, d), dtype=u8, device=dev)
+            self.Wu_q = torch.empty((E, f, d), dtype=u8, device=dev)
+            self.Wd_q = torch.empty((E, d, f), dtype=u8, device=dev)
+            self.Wg_sc = torch.empty((E, f, d // 32), dtype=u8, device=dev)
+            self.Wu_sc = torch.empty((E, f, d // 32), dtype=u8, device=dev)
+            self.Wd_sc = torch.empty((E, d, f // 32), dtype=u8, device=dev)
+            self.mx_weights = B.mx_weights_struct(self.Wg_q, self.Wu_q, self.Wd_q, self.Wg_sc,
+                                                  self.Wu_sc, self.Wd_sc)
+            self.quantize_mx()
+
     # -- the four calls of the path --------------------------------------
     def route(self, stream=None):
         B.moe_route(self.shape, self.X, self.W_r, self.bias, self.logits, self.topk_idx,
@@ -101,6 +119,21 @@ class DeviceLayer:
                        self.topk_w, self.plan_bufs, self.dX, self.grads, self.ws, stream=stream,
                        events=events)
 
+    def quantize_mx(self, stream=None):
+        """Pre-quantise the routed weights to MXFP8 (once per weight update)."""
+        B.moe_mx_quantize_weights(self.shape, self.weights, self.mx_weights, stream=stream)
+
+    def forward_mx(self, stream=None, events=None):
+        B.moe_forward_mx(self.shape, self.X, self.weights, self.mx_weights, self.topk_idx,
+                         self.topk_w, self.plan_bufs, self.Y, self.ws, stream=stream,
+                         events=events)
+
+    def step_mx(self, stream=None, fwd_events=None):
+        """Route, plan and the MXFP8 forward."""
+        self.route(stream)
+        self.plan(stream)
+        self.forward_mx(stream=stream, events=fwd_events)
+
     def step(self, stream=None, fwd_events=None, bwd_events=None):
         """One pass of the whole path: route, plan, forward (and backward)."""
         self.route(stream)
@@ -112,6 +145,10 @@ class DeviceLayer:
     # -- inspection -------------------------------------------------------
     def ws_tensor(self, which, dtype, shape):
         off, nbytes = B.moe_workspace_region(self.shape, self.with_backward, which)
+        return self.ws[off:off + nbytes].view(dtype).view(*shape)
+
+    def mx_ws_tensor(self, which, dtype, shape):
+        off, nbytes = B.moe_mx_workspace_region(self.shape, which)
         return self.ws[off:off + nbytes].view(dtype).view(*shape)
 
     def error_word(self) -> int:

@@ -35,6 +35,12 @@ def test_library_exports_every_declared_function():
     assert "gfx950" in B.version()
 
 
+def test_library_resolves_every_symbol():
+    """Every symbol the library references must be defined (a kernel whose
+    host launch stub went missing would otherwise fail only at its launch)."""
+    ctypes.CDLL(B.LIB_PATH, mode=os.RTLD_NOW | os.RTLD_LOCAL)
+
+
 def test_status_strings():
     for s in range(5):
         assert B.status_string(s)
@@ -153,6 +159,41 @@ def test_schedule_workspace_and_validation():
     assert call(nb=8) == B.MOE_ENOSPACE
     assert call(R=2000, c=0) == B.MOE_EUNSUPPORTED
     assert call(Lx=512) == B.MOE_EUNSUPPORTED
+
+
+def test_mx_workspace_and_validation():
+    L = B.lib()
+    sh = B.make_shape(64, 256, 8, 2, 256, 256)
+    mx_bytes = B.moe_mx_workspace_bytes(sh)
+    assert mx_bytes >= B.moe_workspace_bytes(sh, False) + 64 * 256 + 128 * 256
+    for which in (B.WS_ERROR, B.WS_YEXP, B.WS_YSH, B.WS_XQ, B.WS_XS, B.WS_HQ, B.WS_HS):
+        off, nb = B.moe_mx_workspace_region(sh, which)
+        assert off % 256 == 0 and off + nb <= mx_bytes
+    with pytest.raises(B.MoeError):
+        B.moe_mx_workspace_region(sh, B.WS_A)
+    assert B.moe_mx_workspace_bytes(B.make_shape(1 << 20, 4096, 8, 2, 256)) == 0   # T*d >= 2^32
+    w = B.MoeWeights(None, None, None, FAKE, FAKE, FAKE)          # routed bf16 weights unused
+    mx = B.MoeMxWeights(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+    plan = B.MoePlanBufs(FAKE, FAKE, FAKE, FAKE)
+    big = 1 << 40
+
+    def fwd(shape=sh, X=FAKE, weights=w, q=mx, Y=FAKE, nb=big):
+        return L.moe_forward_mx(ctypes.byref(shape), X, ctypes.byref(weights), ctypes.byref(q),
+                                FAKE, FAKE, ctypes.byref(plan), Y, FAKE, nb, None, None)
+
+    assert fwd(nb=mx_bytes - 1) == B.MOE_ENOSPACE
+    assert fwd(X=None) == B.MOE_EINVAL
+    assert fwd(Y=MISALIGNED) == B.MOE_EINVAL
+    assert fwd(q=B.MoeMxWeights(FAKE, None, FAKE, FAKE, FAKE, FAKE)) == B.MOE_EINVAL
+    assert fwd(weights=B.MoeWeights(None, None, None, None, None, None)) == B.MOE_EINVAL  # shared
+    sh_ns = B.make_shape(64, 256, 8, 2, 256)
+    assert fwd(shape=sh_ns) == B.MOE_EINVAL                       # shared weights without f_shared
+    assert fwd(shape=B.make_shape(1 << 20, 4096, 8, 2, 256)) == B.MOE_EUNSUPPORTED
+    wq = B.MoeWeights(FAKE, FAKE, FAKE, None, None, None)
+    assert L.moe_mx_quantize_weights(ctypes.byref(sh), ctypes.byref(B.MoeWeights()),
+                                     ctypes.byref(mx), None) == B.MOE_EINVAL
+    assert L.moe_mx_quantize_weights(ctypes.byref(sh), ctypes.byref(wq),
+                                     ctypes.byref(B.MoeMxWeights()), None) == B.MOE_EINVAL
 
 
 def test_oracle_is_not_imported_by_the_package():

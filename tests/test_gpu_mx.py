@@ -1,0 +1,172 @@
+"""GPU parity of the MXFP8 routed-expert forward (§3.4 "MXFP8 Support").
+
+Quantisation is byte work, so codes and scales must be bit-exact against the
+oracle wherever both sides quantise the same values (the bf16 weights and X).
+H is quantised from the GPU's own fp32 accumulators, so it and everything
+downstream are floats compared to the usual per-tensor bar.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe_oracle as O
+from oracle import mx_oracle as M
+from paper_2609_36070_amd import binding as B
+from paper_2609_36070_amd.layer import DeviceLayer
+from paper_2609_36070_amd.workloads import WORKLOADS, Workload, make_inputs, to_bf16
+from tests.parity import assert_close, check_route_and_plan, say, to_np, weights_dict
+
+pytestmark = pytest.mark.gpu
+
+
+def with_special_values(inp, seed):
+    """Plant exact rounding ties, negative values that round to zero, a zero
+    block and a block whose maximum saturates, in X and W_gate."""
+    rng = np.random.default_rng(seed)
+    inp = dict(inp)
+    X = inp["X"].copy()
+    if X.shape[0] >= 3:
+        X[0, :32] = 0.0                                   # all-zero block
+        X[1, :32] = to_bf16(rng.standard_normal(32).astype(np.float32) * 1e-3)
+        X[1, 0] = 1.0                                     # amax 1 -> scale 2^-8
+        X[1, 1] = -2.0 ** -20                             # rounds to -0
+        X[1, 2] = 1.0625                                  # tie between 1 and 1.125 (x 2^8)
+        X[2, 32:64] = 1.9375                              # scaled 496 -> saturates at 448
+    inp["X"] = X
+    Wg = inp["W_gate"].copy()
+    Wg[0, :32, 0] = 0.0
+    Wg[0, 0, 1] = 3.0
+    Wg[0, 1, 1] = 3.0 * 1.0625 / 2                        # another tie
+    inp["W_gate"] = Wg
+    return inp
+
+
+def mx_layer(w, seed=0, inputs=None, special=False):
+    inp = make_inputs(w, seed) if inputs is None else inputs
+    if special:
+        inp = with_special_values(inp, seed)
+    L = DeviceLayer(w, inp, mx=True)
+    L.route()
+    L.plan()
+    L.forward_mx()
+    torch.cuda.synchronize()
+    return L, inp
+
+
+def check_weight_codes(L, inp, rows=None):
+    """Every (or a sample of) pre-quantised weight row equals the oracle's."""
+    for key, q, sc in (("W_gate", L.Wg_q, L.Wg_sc), ("W_up", L.Wu_q, L.Wu_sc),
+                       ("W_down", L.Wd_q, L.Wd_sc)):
+        W = inp[key]
+        sel = range(W.shape[0]) if rows is None else rows
+        for e in sel:
+            codes, scales = M.mx_quantize(W[e], axis=0)            # [K, N] along K
+            assert np.array_equal(to_np(q[e]), codes.T), f"{key}[{e}] codes"
+            assert np.array_equal(to_np(sc[e]), scales.T), f"{key}[{e}] scales"
+
+
+def check_h_codes(hq, hs, H, eps=2.0 ** -12):
+    """The GPU quantised H from its own fp32 accumulators, the oracle from
+    fp64, so a value sitting within the accumulation error of a rounding
+    boundary may land on either neighbour.  Each GPU scale must be the
+    oracle's unless the block maximum lies within eps of a power of two; each
+    GPU code must be a nearest (or saturated) E4M3 value of some number within
+    eps * (block maximum) of the oracle's scaled H."""
+    R, f = H.shape
+    se_gpu = hs.astype(np.int64) - 127                                  # [R, f/32]
+    amax = np.abs(H).reshape(R, f // 32, 32).max(axis=2)
+    se_ref = M.shared_exponent(amax)
+    diff = se_gpu != se_ref
+    edge = np.abs(amax / np.exp2(np.maximum(se_gpu, se_ref) + 8.0) - 1.0) <= eps
+    assert np.all(~diff | edge), f"{int(np.sum(diff & ~edge))} block scales differ away from 2^k"
+    Xs = np.repeat(np.exp2(se_gpu.astype(float)), 32, axis=1)
+    v = H / Xs                                                          # oracle H, GPU scale
+    got = M.e4m3_value(hq)
+    tol = eps * np.repeat(amax / np.exp2(se_gpu.astype(float)), 32, axis=1)
+    lo, hi = M.e4m3_value(M.e4m3_round(v - tol)), M.e4m3_value(M.e4m3_round(v + tol))
+    ok = (got >= np.minimum(lo, hi)) & (got <= np.maximum(lo, hi))
+    assert np.all(ok), f"{int(np.sum(~ok))} H codes outside the rounding of oracle H +- tol"
+    return float(np.mean(hq == M.e4m3_round(v)))
+
+
+def mx_parity(w, seed=0, special=False):
+    L, inp = mx_layer(w, seed, special=special)
+    Zo, idx_g = check_route_and_plan(L, inp, w)
+    w_orc = O.gate_weights(Zo, idx_g)
+    check_weight_codes(L, inp)
+    xq, xs = M.mx_quantize(inp["X"], axis=1)
+    assert np.array_equal(to_np(L.mx_ws_tensor(B.WS_XQ, torch.uint8, (w.T, w.d))), xq)
+    assert np.array_equal(to_np(L.mx_ws_tensor(B.WS_XS, torch.uint8, (w.T, w.d // 32))), xs)
+    ref = M.moe_forward_mx(inp["X"], weights_dict(inp), idx_g, w_orc)
+    R = w.T * w.k
+    hq = to_np(L.mx_ws_tensor(B.WS_HQ, torch.uint8, (R, w.f)))
+    hs = to_np(L.mx_ws_tensor(B.WS_HS, torch.uint8, (R, w.f // 32)))
+    same = check_h_codes(hq, hs, ref["H"])
+    say(f"  H codes equal to the oracle's: {same * 100:.3f} % (the rest within fp32 error)")
+    assert_close("Yexp", to_np(L.mx_ws_tensor(B.WS_YEXP, torch.bfloat16, (R, w.d))), ref["Yexp"])
+    assert_close("Y", to_np(L.Y), ref["Y"])
+    return L, inp
+
+
+def test_mx_tiny_with_special_values():
+    mx_parity(Workload("mx_tiny", T=256, d=256, E=4, k=2, f=256, f_s=256), seed=1, special=True)
+
+
+def test_mx_ragged():
+    mx_parity(Workload("mx_ragged", T=1000, d=512, E=6, k=2, f=512, f_s=256, bias_std=0.5), seed=2)
+
+
+@pytest.mark.parametrize("w", [
+    Workload("mx_one_token", T=1, d=256, E=8, k=3, f=256, f_s=256),
+    Workload("mx_k_equals_E", T=300, d=256, E=4, k=4, f=512, bias_std=0.5),
+    Workload("mx_empty_experts", T=40, d=256, E=64, k=1, f=256, bias_std=3.0),
+    Workload("mx_many_tiles", T=700, d=768, E=3, k=2, f=768),
+], ids=lambda w: w.name)
+def test_mx_edge_shapes(w):
+    mx_parity(w, seed=3)
+
+
+def test_mx_no_tokens():
+    w = Workload("mx_none", T=0, d=256, E=4, k=2, f=256)
+    L, inp = mx_layer(w, 0)
+    assert np.all(to_np(L.offsets) == 0)
+    check_weight_codes(L, inp)
+
+
+def test_mx_determinism():
+    w = Workload("mx_det", T=1000, d=512, E=6, k=2, f=512, f_s=256, bias_std=0.5)
+    L, _ = mx_layer(w, 4)
+    first = L.Y.clone()
+    hq = L.mx_ws_tensor(B.WS_HQ, torch.uint8, (w.T * w.k, w.f)).clone()
+    for _ in range(3):
+        L.forward_mx()
+        torch.cuda.synchronize()
+        assert torch.equal(L.Y, first)
+        assert torch.equal(L.mx_ws_tensor(B.WS_HQ, torch.uint8, (w.T * w.k, w.f)), hq)
+
+
+def test_mx_full_size_sampled():
+    """large_shared in MXFP8: weight codes checked on two experts, then Y of
+    sampled tokens against a per-token fp64 evaluation on the GPU's (verified)
+    weight codes."""
+    w = WORKLOADS["large_shared"]
+    L, inp = mx_layer(w, 0)
+    check_weight_codes(L, inp, rows=[0, w.E - 1])
+    Zo, idx_g = check_route_and_plan(L, inp, w)
+    w_orc = O.gate_weights(Zo, idx_g)
+    Wg = M.mx_dequantize(to_np(L.Wg_q), to_np(L.Wg_sc), axis=2)      # [E, f, d]
+    Wu = M.mx_dequantize(to_np(L.Wu_q), to_np(L.Wu_sc), axis=2)
+    Wd = M.mx_dequantize(to_np(L.Wd_q), to_np(L.Wd_sc), axis=2)      # [E, d, f]
+    rng = np.random.default_rng(5)
+    toks = np.sort(rng.choice(w.T, 48, replace=False))
+    Y = to_np(L.Y)[toks].astype(np.float64)
+    X = inp["X"][toks].astype(np.float64)
+    xh = M.mx_qdq(X, axis=1)
+    ref = O.expert_ffn(X, inp["Wg_s"], inp["Wu_s"], inp["Wd_s"])
+    for n, t in enumerate(toks):
+        for s in range(w.k):
+            e = int(idx_g[t, s])
+            h = O.silu(Wg[e] @ xh[n]) * (Wu[e] @ xh[n])
+            hh = M.mx_qdq(h[None, :], axis=1)[0]
+            ref[n] += w_orc[t, s] * (Wd[e] @ hh)
+    assert_close("Y (sampled tokens)", Y, ref)
