@@ -196,6 +196,63 @@ def mx_forward_timing(H, stream, inputs, steps, warmup):
     return out
 
 
+def ring_timing(H, stream, w, inputs, L_full, steps, warmup):
+    """Bounded-memory execution against the one-pass path on the benchmark
+    workload: a ring holding half of the routed rows (the comparison the
+    paper makes for its macrobatch ring) versus buffers for every route.
+    Both are timed in two alternating blocks of `steps` whole steps; the
+    forward (route + plan + forward) and backward parts are timed apart."""
+    import torch
+    from paper_2609_36070_amd.layer import DeviceLayer
+    R = w.T * w.k
+    ring_rows = R // 2
+    L_ring = DeviceLayer(w, inputs, ring_rows=ring_rows)
+    for _ in range(warmup):
+        L_ring.step()
+    torch.cuda.synchronize()
+
+    def block(L):
+        marks = [(H.create(), H.create(), H.create()) for _ in range(steps)]
+        for a, m, b in marks:
+            H.record(a, stream)
+            L.route()
+            L.plan()
+            L.forward()
+            H.record(m, stream)
+            if w.backward:
+                L.backward()
+            H.record(b, stream)
+        H.sync(marks[-1][2])
+        f = sum(H.ms(a, m) for a, m, _ in marks) / steps
+        bw = sum(H.ms(m, b) for _, m, b in marks) / steps
+        for e in marks:
+            for x in e:
+                H.destroy(x)
+        return f, bw
+
+    res = {"full": [0.0, 0.0], "ring": [0.0, 0.0]}
+    for _ in range(2):
+        for name, L in (("full", L_full), ("ring", L_ring)):
+            f, bw = block(L)
+            res[name][0] += f / 2
+            res[name][1] += bw / 2
+    full_ms, ring_ms = sum(res["full"]), sum(res["ring"])
+    out = {"ring_rows": ring_rows, "routes": R, "windows": -(-R // ring_rows),
+           "workspace_gib_full": round(L_full.ws.numel() / 2 ** 30, 3),
+           "workspace_gib_ring": round(L_ring.ws.numel() / 2 ** 30, 3),
+           "full_ms": {"forward": round(res["full"][0], 4), "backward": round(res["full"][1], 4),
+                       "step": round(full_ms, 4)},
+           "ring_ms": {"forward": round(res["ring"][0], 4), "backward": round(res["ring"][1], 4),
+                       "step": round(ring_ms, 4)},
+           "overhead_pct": {"forward": round(100 * (res["ring"][0] / res["full"][0] - 1), 2),
+                            "step": round(100 * (ring_ms / full_ms - 1), 2)}}
+    if w.backward:
+        out["overhead_pct"]["backward"] = round(100 * (res["ring"][1] / res["full"][1] - 1), 2)
+    del L_ring
+    torch.cuda.synchronize()
+    return out
+
+
 def cpu_baseline(w, inputs, sample_tokens):
     """Time the CPU oracle on the first `sample_tokens` tokens of the workload."""
     import numpy as np
@@ -236,6 +293,8 @@ def main():
     ap.add_argument("--no-schedule", action="store_true",
                     help="skip timing the multi-rank dispatch schedule")
     ap.add_argument("--no-mx", action="store_true", help="skip timing the MXFP8 forward")
+    ap.add_argument("--no-ring", action="store_true",
+                    help="skip the bounded-memory (half-capacity ring) comparison")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (the reference "
                          "kernel for scaling HBM byte counters)")
@@ -371,6 +430,14 @@ def main():
         for name, v in mxf["stages"].items():
             log(f"   mx.{name:25s} {v['ms']:9.4f} ms  {v.get('tflops', '')}")
 
+    ring = None
+    if not args.no_ring:
+        ring = ring_timing(H, stream, w, inputs, L, max(3, args.steps // 2), 2)
+        log(f"[bench] ring of {ring['ring_rows']} rows ({ring['windows']} windows, "
+            f"{ring['workspace_gib_ring']} GiB vs {ring['workspace_gib_full']} GiB): "
+            f"step {ring['ring_ms']['step']:.3f} ms vs {ring['full_ms']['step']:.3f} ms, "
+            f"overhead {ring['overhead_pct']}")
+
     sched = None
     if not args.no_schedule:
         sched = schedule_timing(H, stream)
@@ -399,6 +466,7 @@ def main():
         "stages": stage_report,
         "schedule": sched,
         "mxfp8_forward": mxf,
+        "bounded_memory": ring,
     }
     print(json.dumps(out), flush=True)
 

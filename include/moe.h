@@ -282,6 +282,52 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
                         void *ws, size_t ws_bytes, moe_stream stream,
                         const moe_stage_events *events /* NULL = no timing */);
 
+/* Bounded-memory execution (§3.3 "macrobatch" ring buffer and "Ring-Aware
+ * Forward Replay").  The per-route activations (A, B, H, Yexp and their
+ * gradients) live in a ring of ring_rows rows instead of T*k rows; the plan
+ * positions are processed in windows [m C, min((m+1) C, T*k)), C = ring_rows.
+ *
+ *   moe_forward_ring  runs the windows in descending order (reverse
+ *                     macrobatch order) after the shared expert, so the
+ *                     ring ends holding window 0 in full.  Per window: the
+ *                     routed up/gate + SwiGLU and down GEMMs, then each
+ *                     token's routes that fall in the window are added, in
+ *                     ascending slot order and weighted, to an fp32
+ *                     per-token accumulator seeded with the shared-expert
+ *                     output; the last window rounds it into Y.
+ *   moe_backward_ring runs the windows in ascending order: window 0 uses the
+ *                     activations the forward left in the ring; every later
+ *                     window first recomputes its gate/up pre-activations
+ *                     (A, B only: the down projection and H are not
+ *                     replayed).  Weight gradients of a window are added to
+ *                     the previous windows' in fp32; the routed dX terms are
+ *                     summed per token across windows as in the forward.
+ *
+ * Results are deterministic.  With one window (ring_rows >= T*k) they are
+ * bitwise those of moe_forward / moe_backward; with several, Y, dX and the
+ * routed weight gradients differ only by fp32 summation order, and dZ and
+ * dW_r are bitwise those of moe_backward.
+ *   ring_rows >= 1 (MOE_EINVAL otherwise), < 2^31.
+ *   ws: at least moe_ring_workspace_bytes(shape, ring_rows, with_backward)
+ *   bytes; the region layout differs from moe_workspace_region's, so the
+ *   ring entry points and moe_forward / moe_backward must not share a ws
+ *   between a forward and its backward.  moe_route and moe_plan accept a
+ *   ring workspace.  moe_backward_ring needs the ws of a preceding
+ *   moe_forward_ring with save_for_backward = 1, the same ring_rows and the
+ *   same inputs.  Other arguments as moe_forward / moe_backward. */
+size_t moe_ring_workspace_bytes(const moe_shape *shape, int64_t ring_rows, int with_backward);
+
+moe_status moe_forward_ring(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
+                            const int32_t *topk_idx, const float *topk_w,
+                            const moe_plan_bufs *plan, moe_bf16 *Y, int64_t ring_rows,
+                            int save_for_backward, void *ws, size_t ws_bytes, moe_stream stream);
+
+moe_status moe_backward_ring(const moe_shape *shape, const moe_bf16 *dY, const moe_bf16 *X,
+                             const moe_bf16 *W_r, const moe_weights *weights,
+                             const int32_t *topk_idx, const float *topk_w,
+                             const moe_plan_bufs *plan, moe_bf16 *dX, const moe_grads *grads,
+                             int64_t ring_rows, void *ws, size_t ws_bytes, moe_stream stream);
+
 /* Static strings; never NULL. */
 const char *moe_status_string(moe_status status);
 const char *moe_version(void);

@@ -25,7 +25,8 @@ WS_XQ, WS_XS, WS_HQ, WS_HS = range(10, 14)
 EXPORTS = ("moe_workspace_bytes", "moe_workspace_region", "moe_route", "moe_plan",
            "moe_schedule_workspace_bytes", "moe_schedule", "moe_dispatch", "moe_forward",
            "moe_backward", "moe_mx_quantize_weights", "moe_mx_workspace_bytes",
-           "moe_mx_workspace_region", "moe_forward_mx", "moe_status_string", "moe_version")
+           "moe_mx_workspace_region", "moe_forward_mx", "moe_ring_workspace_bytes",
+           "moe_forward_ring", "moe_backward_ring", "moe_status_string", "moe_version")
 
 
 class MoeShape(ctypes.Structure):
@@ -104,9 +105,18 @@ def lib():
         L.moe_forward_mx.argtypes = [P(MoeShape), c_void_p, P(MoeWeights), P(MoeMxWeights),
                                      c_void_p, c_void_p, P(MoePlanBufs), c_void_p, c_void_p,
                                      c_size_t, c_void_p, P(MoeStageEvents)]
+        L.moe_ring_workspace_bytes.argtypes = [P(MoeShape), ctypes.c_int64, c_int]
+        L.moe_ring_workspace_bytes.restype = c_size_t
+        L.moe_forward_ring.argtypes = [P(MoeShape), c_void_p, P(MoeWeights), c_void_p, c_void_p,
+                                       P(MoePlanBufs), c_void_p, ctypes.c_int64, c_int, c_void_p,
+                                       c_size_t, c_void_p]
+        L.moe_backward_ring.argtypes = [P(MoeShape), c_void_p, c_void_p, c_void_p, P(MoeWeights),
+                                        c_void_p, c_void_p, P(MoePlanBufs), c_void_p, P(MoeGrads),
+                                        ctypes.c_int64, c_void_p, c_size_t, c_void_p]
         for fn in ("moe_route", "moe_plan", "moe_schedule", "moe_dispatch", "moe_forward",
                    "moe_backward", "moe_workspace_region", "moe_mx_quantize_weights",
-                   "moe_mx_workspace_region", "moe_forward_mx"):
+                   "moe_mx_workspace_region", "moe_forward_mx", "moe_forward_ring",
+                   "moe_backward_ring"):
             getattr(L, fn).restype = c_int
         L.moe_status_string.argtypes = [c_int]
         L.moe_status_string.restype = ctypes.c_char_p
@@ -266,3 +276,29 @@ def moe_backward(shape, dY, X, W_r, weights: MoeWeights, topk_idx, topk_w, plan:
                             ctypes.byref(grads), _p(ws), nbytes, _stream(stream),
                             None if events is None else ctypes.byref(events))
     return _check("moe_backward", st, raise_on_error)
+
+
+def moe_ring_workspace_bytes(shape: MoeShape, ring_rows: int, with_backward: bool) -> int:
+    return int(lib().moe_ring_workspace_bytes(ctypes.byref(shape), int(ring_rows),
+                                              int(bool(with_backward))))
+
+
+def moe_forward_ring(shape, X, weights: MoeWeights, topk_idx, topk_w, plan: MoePlanBufs, Y,
+                     ring_rows, save_for_backward, ws, ws_bytes=None, stream=None,
+                     raise_on_error=True):
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    st = lib().moe_forward_ring(ctypes.byref(shape), _p(X), ctypes.byref(weights), _p(topk_idx),
+                                _p(topk_w), ctypes.byref(plan), _p(Y), int(ring_rows),
+                                int(bool(save_for_backward)), _p(ws), nbytes, _stream(stream))
+    return _check("moe_forward_ring", st, raise_on_error)
+
+
+def moe_backward_ring(shape, dY, X, W_r, weights: MoeWeights, topk_idx, topk_w,
+                      plan: MoePlanBufs, dX, grads: MoeGrads, ring_rows, ws, ws_bytes=None,
+                      stream=None, raise_on_error=True):
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    st = lib().moe_backward_ring(ctypes.byref(shape), _p(dY), _p(X), _p(W_r),
+                                 ctypes.byref(weights), _p(topk_idx), _p(topk_w),
+                                 ctypes.byref(plan), _p(dX), ctypes.byref(grads), int(ring_rows),
+                                 _p(ws), nbytes, _stream(stream))
+    return _check("moe_backward_ring", st, raise_on_error)

@@ -15,24 +15,34 @@ constexpr size_t ALIGN = 256;
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
-// Byte offsets of every workspace region; depends only on the shape.
+// Byte offsets of every workspace region; depends only on the shape and, for
+// bounded-memory execution, on the ring size.  The prefix (error word, plan
+// scratch, W_r^T, position tables, zero page) is the same in every layout,
+// so moe_route and moe_plan work with any of them.
 struct Layout {
     size_t err, blockcounts, blockbase, blockflags, wrt, rowidx, wperm, zeros;
+    size_t prefix_total;
+    size_t acc, coff;          // ring only: fp32 per-token accumulator, window regions
     size_t A, B, H, Yexp, As, Bs, Hs, Ysh;
     size_t fwd_total;
     size_t dA, dB, Hw, dgpart, dg, dZ, dXperm, dAs, dBs, dXsh, dwr_part;
     size_t bwd_total;
     size_t xq, xs, hq, hsc;   // MXFP8 forward: quantised X and H (over the backward regions)
     size_t mx_total;
+    long act_rows;             // rows of the per-route activation buffers
     int dg_parts;
 };
 
-Layout make_layout(const moe_shape &s) {
+// ring_rows < 0: per-route activations for all T*k routes; otherwise a ring
+// of ring_rows rows (bounded-memory execution).
+Layout make_layout(const moe_shape &s, long ring_rows = -1) {
     const size_t T = s.T, d = s.d, E = s.E, f = s.f, fs = s.f_shared;
     const size_t R = T * (size_t)s.k;
     const size_t nb = (size_t)plan_nblocks((long)R);
     const size_t epad = (size_t)route_epad((int)E);
+    const size_t Ra = ring_rows < 0 ? R : (size_t)ring_rows;
     Layout L{};
+    L.act_rows = (long)Ra;
     size_t o = 0;
     auto take = [&](size_t bytes) { const size_t at = o; o += up(bytes > 0 ? bytes : 1); return at; };
     L.err = take(4);
@@ -43,23 +53,28 @@ Layout make_layout(const moe_shape &s) {
     L.rowidx = take(R * 4);
     L.wperm = take(R * 4);
     L.zeros = take(ZERO_PAGE_ELEMS * 2);
-    L.A = take(R * f * 2);
-    L.B = take(R * f * 2);
-    L.H = take(R * f * 2);
-    L.Yexp = take(R * d * 2);
+    L.prefix_total = o;
+    if (ring_rows >= 0) {
+        L.acc = take(T * d * 4);
+        L.coff = take((E + 1) * 4);
+    }
+    L.A = take(Ra * f * 2);
+    L.B = take(Ra * f * 2);
+    L.H = take(Ra * f * 2);
+    L.Yexp = take(Ra * d * 2);
     L.As = take(T * fs * 2);
     L.Bs = take(T * fs * 2);
     L.Hs = take(T * fs * 2);
     L.Ysh = take(T * d * 2);
     L.fwd_total = o;
     L.dg_parts = (int)(f / (size_t)gemm_tile_n());
-    L.dA = take(R * f * 2);
-    L.Hw = take(R * f * 2);
-    L.dB = take(R * f * 2);
+    L.dA = take(Ra * f * 2);
+    L.Hw = take(Ra * f * 2);
+    L.dB = take(Ra * f * 2);
     L.dgpart = take(R * (size_t)L.dg_parts * 4);
     L.dg = take(R * 4);
     L.dZ = take(T * E * 4);
-    L.dXperm = take(R * d * 2);
+    L.dXperm = take(Ra * d * 2);
     L.dAs = take(T * fs * 2);
     L.dBs = take(T * fs * 2);
     L.dXsh = take(T * d * 2);
@@ -115,6 +130,13 @@ moe_status check_ws(const moe_shape *s, const void *ws, size_t ws_bytes, int wit
     if (!ptr_ok(ws)) return MOE_EINVAL;
     const Layout L = make_layout(*s);
     if (ws_bytes < (with_backward ? L.bwd_total : L.fwd_total)) return MOE_ENOSPACE;
+    return MOE_OK;
+}
+
+// moe_route and moe_plan touch only the layout prefix.
+moe_status check_ws_prefix(const moe_shape *s, const void *ws, size_t ws_bytes) {
+    if (!ptr_ok(ws)) return MOE_EINVAL;
+    if (ws_bytes < make_layout(*s).prefix_total) return MOE_ENOSPACE;
     return MOE_OK;
 }
 
@@ -211,6 +233,203 @@ hipError_t shared_down(const moe_shape &sh, const Layout &L, void *ws, const moe
     return launch_gemm_fwd_down(g, T, 1, s);
 }
 
+// Positions [w0, w1) of the routed buffer, with the expert regions clipped
+// to it.  Per-route activation rows live at row p - w0 of their region, so
+// kernels keep indexing by the global position p through a shifted base.
+// The one-pass path is the single window [0, T k) with the plan's offsets.
+struct Window {
+    const int *offs;
+    int w0, w1;
+    template <class T> T *rows(void *ws, size_t region, long ld) const {
+        return at<T>(ws, region) - (long)w0 * ld;
+    }
+    int span() const { return w1 > 1 ? w1 : 1; }   // clamp bound of position-indexed rows
+    long count() const { return (long)w1 - w0; }
+};
+
+// Routed up/gate + SwiGLU over a window: H (optional) and, for the backward,
+// the pre-activations A and B.
+hipError_t routed_up(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *X,
+                     const moe_weights *w, const Window &win, bool keep_h, bool save, hipStream_t s) {
+    const int T = (int)sh.T, d = (int)sh.d, f = (int)sh.f;
+    GemmArgs g;
+    g.zeros = at<uint16_t>(ws, L.zeros);
+    g.A = X; g.lda = d; g.a_rows = at<int>(ws, L.rowidx); g.a_nrows = T > 0 ? T : 1;
+    g.B = w->W_gate; g.B2 = w->W_up; g.ldb = f; g.b_estride = (long)d * f;
+    g.N = f; g.K = d; g.offsets = win.offs; g.E = (int)sh.E;
+    if (keep_h) g.C = win.rows<uint16_t>(ws, L.H, f);
+    g.ldc = f;
+    if (save) { g.C2 = win.rows<uint16_t>(ws, L.A, f); g.C3 = win.rows<uint16_t>(ws, L.B, f); }
+    return launch_gemm_fwd_up(g, win.count(), (int)sh.E, s);
+}
+
+hipError_t routed_down(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w,
+                       const Window &win, hipStream_t s) {
+    const int d = (int)sh.d, f = (int)sh.f;
+    GemmArgs g;
+    g.zeros = at<uint16_t>(ws, L.zeros);
+    g.A = win.rows<uint16_t>(ws, L.H, f); g.lda = f; g.a_nrows = win.span();
+    g.B = w->W_down; g.ldb = d; g.b_estride = (long)f * d;
+    g.N = d; g.K = f; g.offsets = win.offs; g.E = (int)sh.E;
+    g.C = win.rows<uint16_t>(ws, L.Yexp, d); g.ldc = d;
+    return launch_gemm_fwd_down(g, win.count(), (int)sh.E, s);
+}
+
+// dh' = dY W_down^T with the SwiGLU backward and the dg partials.
+hipError_t routed_dgrad(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *dY,
+                        const moe_weights *w, const Window &win, hipStream_t s) {
+    const int T = (int)sh.T, d = (int)sh.d, f = (int)sh.f;
+    GemmArgs g;
+    g.zeros = at<uint16_t>(ws, L.zeros);
+    g.A = dY; g.lda = d; g.a_rows = at<int>(ws, L.rowidx); g.a_nrows = T > 0 ? T : 1;
+    g.B = w->W_down; g.ldb = d; g.b_estride = (long)f * d;
+    g.N = f; g.K = d; g.offsets = win.offs; g.E = (int)sh.E;
+    g.E1 = win.rows<uint16_t>(ws, L.A, f); g.E2 = win.rows<uint16_t>(ws, L.B, f); g.ldc = f;
+    g.rowscale = at<float>(ws, L.wperm);
+    g.C = win.rows<uint16_t>(ws, L.dA, f); g.C2 = win.rows<uint16_t>(ws, L.dB, f);
+    g.C3 = win.rows<uint16_t>(ws, L.Hw, f);
+    g.dgpart = at<float>(ws, L.dgpart); g.dg_ld = L.dg_parts;
+    return launch_gemm_bwd_dgrad(g, win.count(), (int)sh.E, s);
+}
+
+// dXperm = dA W_gate^T + dB W_up^T.
+hipError_t routed_dx(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w,
+                     const Window &win, hipStream_t s) {
+    const int d = (int)sh.d, f = (int)sh.f;
+    GemmArgs g;
+    g.zeros = at<uint16_t>(ws, L.zeros);
+    g.A = win.rows<uint16_t>(ws, L.dA, f); g.A2 = win.rows<uint16_t>(ws, L.dB, f);
+    g.lda = f; g.a_nrows = win.span();
+    g.B = w->W_gate; g.B2 = w->W_up; g.ldb = f; g.b_estride = (long)d * f;
+    g.N = d; g.K = f; g.offsets = win.offs; g.E = (int)sh.E;
+    g.C = win.rows<uint16_t>(ws, L.dXperm, d); g.ldc = d;
+    return launch_gemm_bwd_dx(g, win.count(), (int)sh.E, s);
+}
+
+// dW_gate[e] = Xperm_e^T dA_e, dW_up[e] = Xperm_e^T dB_e over the window's rows
+// of each expert (added to the previous windows' sums when accumulate).
+hipError_t routed_wgrad_up(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *X,
+                           const moe_grads *gr, const Window &win, bool accumulate, hipStream_t s) {
+    const int T = (int)sh.T, d = (int)sh.d, f = (int)sh.f;
+    GemmArgs g;
+    g.zeros = at<uint16_t>(ws, L.zeros);
+    g.A = X; g.lda = d; g.a_rows = at<int>(ws, L.rowidx); g.a_nrows = T > 0 ? T : 1;
+    g.B = win.rows<uint16_t>(ws, L.dA, f); g.ldb = f; g.b_nrows = win.span();
+    g.M = d; g.N = f; g.offsets = win.offs; g.E = (int)sh.E;
+    g.Cf = gr->dW_gate; g.c_estride = (long)d * f; g.ldc = f;
+    g.accumulate = accumulate ? 1 : 0;
+    hipError_t e = launch_gemm_wgrad(g, (int)sh.E, s);
+    if (e != hipSuccess) return e;
+    g.B = win.rows<uint16_t>(ws, L.dB, f); g.Cf = gr->dW_up;
+    return launch_gemm_wgrad(g, (int)sh.E, s);
+}
+
+// dW_down[e] = (w H_e)^T dYperm_e over the window.
+hipError_t routed_wgrad_down(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *dY,
+                             const moe_grads *gr, const Window &win, bool accumulate, hipStream_t s) {
+    const int T = (int)sh.T, d = (int)sh.d, f = (int)sh.f;
+    GemmArgs g;
+    g.zeros = at<uint16_t>(ws, L.zeros);
+    g.A = win.rows<uint16_t>(ws, L.Hw, f); g.lda = f; g.a_nrows = win.span();
+    g.B = dY; g.ldb = d; g.b_rows = at<int>(ws, L.rowidx); g.b_nrows = T > 0 ? T : 1;
+    g.M = f; g.N = d; g.offsets = win.offs; g.E = (int)sh.E;
+    g.Cf = gr->dW_down; g.c_estride = (long)f * d; g.ldc = d;
+    g.accumulate = accumulate ? 1 : 0;
+    return launch_gemm_wgrad(g, (int)sh.E, s);
+}
+
+// Shared-expert backward: dAs/dBs, dXsh and its three weight gradients.
+// Marks stages 7 and 8 of the stage events between its GEMMs.
+hipError_t shared_backward(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *dY,
+                           const moe_bf16 *X, const moe_weights *w, const moe_grads *gr,
+                           const StageMarks &mk, hipStream_t s) {
+    const int T = (int)sh.T, d = (int)sh.d, fs = (int)sh.f_shared;
+    const int Tn = T > 0 ? T : 1;
+    uint16_t *dAs = at<uint16_t>(ws, L.dAs), *dBs = at<uint16_t>(ws, L.dBs);
+    uint16_t *dXsh = at<uint16_t>(ws, L.dXsh);
+    hipError_t e;
+    {
+        GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
+        g.A = dY; g.lda = d; g.a_nrows = Tn; g.M = T;
+        g.B = w->Wd_s; g.ldb = d;
+        g.N = fs; g.K = d;
+        g.E1 = at<uint16_t>(ws, L.As); g.E2 = at<uint16_t>(ws, L.Bs); g.ldc = fs;
+        g.C = dAs; g.C2 = dBs;
+        if ((e = launch_gemm_bwd_dgrad(g, T, 1, s)) != hipSuccess) return e;
+    }
+    if ((e = mk.mark(7)) != hipSuccess) return e;
+    {
+        GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
+        g.A = dAs; g.A2 = dBs; g.lda = fs; g.a_nrows = Tn; g.M = T;
+        g.B = w->Wg_s; g.B2 = w->Wu_s; g.ldb = fs;
+        g.N = d; g.K = fs;
+        g.C = dXsh; g.ldc = d;
+        if ((e = launch_gemm_bwd_dx(g, T, 1, s)) != hipSuccess) return e;
+    }
+    if ((e = mk.mark(8)) != hipSuccess) return e;
+    {
+        GemmArgs g;
+        g.zeros = at<uint16_t>(ws, L.zeros);
+        g.A = X; g.lda = d; g.a_nrows = Tn;
+        g.B = dAs; g.ldb = fs; g.b_nrows = Tn;
+        g.M = d; g.N = fs; g.K = T;
+        g.Cf = gr->dWg_s; g.ldc = fs;
+        if ((e = launch_gemm_wgrad(g, 1, s)) != hipSuccess) return e;
+        g.B = dBs; g.Cf = gr->dWu_s;
+        if ((e = launch_gemm_wgrad(g, 1, s)) != hipSuccess) return e;
+    }
+    GemmArgs g;
+    g.zeros = at<uint16_t>(ws, L.zeros);
+    g.A = at<uint16_t>(ws, L.Hs); g.lda = fs; g.a_nrows = Tn;
+    g.B = dY; g.ldb = d; g.b_nrows = Tn;
+    g.M = fs; g.N = d; g.K = T;
+    g.Cf = gr->dWd_s; g.ldc = d;
+    return launch_gemm_wgrad(g, 1, s);
+}
+
+moe_status check_backward_args(const moe_shape *shape, const moe_bf16 *dY, const moe_bf16 *X,
+                               const moe_bf16 *W_r, const moe_weights *weights,
+                               const int32_t *topk_idx, const float *topk_w,
+                               const moe_plan_bufs *plan, const moe_bf16 *dX,
+                               const moe_grads *grads) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if (!ptr_ok(dY) || !ptr_ok(X) || !ptr_ok(W_r) || !ptr_ok(topk_idx) || !ptr_ok(topk_w) ||
+        !ptr_ok(dX))
+        return MOE_EINVAL;
+    if ((st = check_weights(shape, weights)) != MOE_OK) return st;
+    if ((st = check_plan(plan)) != MOE_OK) return st;
+    if (!grads || !ptr_ok(grads->dW_gate) || !ptr_ok(grads->dW_up) || !ptr_ok(grads->dW_down) ||
+        !ptr_ok(grads->dW_r) || !opt_ok(grads->dZ))
+        return MOE_EINVAL;
+    if (shape->f_shared > 0) {
+        if (!ptr_ok(grads->dWg_s) || !ptr_ok(grads->dWu_s) || !ptr_ok(grads->dWd_s)) return MOE_EINVAL;
+    } else if (grads->dWg_s || grads->dWu_s || grads->dWd_s) {
+        return MOE_EINVAL;
+    }
+    return MOE_OK;
+}
+
+// Bounded-memory execution: ring size and window count.
+moe_status check_ring(int64_t ring_rows) {
+    if (ring_rows < 1) return MOE_EINVAL;
+    if (ring_rows >= (int64_t(1) << 31)) return MOE_EUNSUPPORTED;
+    return MOE_OK;
+}
+
+long ring_act_rows(const moe_shape &sh, int64_t ring_rows) {
+    const long R = (long)sh.T * sh.k;
+    return ring_rows < R ? (long)ring_rows : R;
+}
+
+int ring_windows(const moe_shape &sh, int64_t ring_rows) {
+    const long R = (long)sh.T * sh.k;
+    const long m = (R + ring_rows - 1) / ring_rows;
+    return m > 0 ? (int)m : 1;   // an empty batch still runs one (empty) window
+}
+
 }  // namespace
 
 extern "C" {
@@ -254,7 +473,7 @@ moe_status moe_route(const moe_shape *shape, const moe_bf16 *X, const moe_bf16 *
     if (!ptr_ok(X) || !ptr_ok(W_r) || !opt_ok(bias) || !ptr_ok(logits) || !ptr_ok(topk_idx) ||
         !ptr_ok(topk_w))
         return MOE_EINVAL;
-    if ((st = check_ws(shape, ws, ws_bytes, 0)) != MOE_OK) return st;
+    if ((st = check_ws_prefix(shape, ws, ws_bytes)) != MOE_OK) return st;
     const Layout L = make_layout(*shape);
     hipStream_t s = static_cast<hipStream_t>(stream);
     MOE_TRY(launch_route(X, W_r, bias, logits, topk_idx, topk_w, at<uint16_t>(ws, L.wrt),
@@ -268,7 +487,7 @@ moe_status moe_plan(const moe_shape *shape, const int32_t *topk_idx, const moe_p
     if (st != MOE_OK) return st;
     if (!ptr_ok(topk_idx)) return MOE_EINVAL;
     if ((st = check_plan(plan)) != MOE_OK) return st;
-    if ((st = check_ws(shape, ws, ws_bytes, 0)) != MOE_OK) return st;
+    if ((st = check_ws_prefix(shape, ws, ws_bytes)) != MOE_OK) return st;
     const Layout L = make_layout(*shape);
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int R = (int)(shape->T * shape->k);
@@ -323,39 +542,19 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
     const Layout L = make_layout(*shape);
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int T = (int)shape->T, d = (int)shape->d, E = (int)shape->E, k = (int)shape->k;
-    const int f = (int)shape->f, fs = (int)shape->f_shared;
-    const long R = (long)T * k;
-    int *rowidx = at<int>(ws, L.rowidx);
-    float *wperm = at<float>(ws, L.wperm);
-    uint16_t *H = at<uint16_t>(ws, L.H);
+    const int fs = (int)shape->f_shared;
+    const Window all{plan->offsets, 0, (int)((long)T * k)};
     const StageMarks mk{events, s};
 
     MOE_TRY(mk.mark(0));
-    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, rowidx, wperm,
-                        at<uint16_t>(ws, L.zeros), s));
+    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, at<int>(ws, L.rowidx),
+                        at<float>(ws, L.wperm), at<uint16_t>(ws, L.zeros), s));
     MOE_TRY(mk.mark(1));
-    {   // routed up/gate + SwiGLU
-        GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
-        g.A = X; g.lda = d; g.a_rows = rowidx; g.a_nrows = T > 0 ? T : 1;
-        g.B = weights->W_gate; g.B2 = weights->W_up; g.ldb = f; g.b_estride = (long)d * f;
-        g.N = f; g.K = d; g.offsets = plan->offsets; g.E = E;
-        g.C = H; g.ldc = f;
-        if (save_for_backward) { g.C2 = at<uint16_t>(ws, L.A); g.C3 = at<uint16_t>(ws, L.B); }
-        MOE_TRY(launch_gemm_fwd_up(g, R, E, s));
-    }
+    MOE_TRY(routed_up(*shape, L, ws, X, weights, all, true, save_for_backward != 0, s));
     MOE_TRY(mk.mark(2));
     if (fs > 0) MOE_TRY(shared_up(*shape, L, ws, X, weights, save_for_backward != 0, s));
     MOE_TRY(mk.mark(3));
-    {   // routed down
-        GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
-        g.A = H; g.lda = f; g.a_nrows = R > 0 ? (int)R : 1;
-        g.B = weights->W_down; g.ldb = d; g.b_estride = (long)f * d;
-        g.N = d; g.K = f; g.offsets = plan->offsets; g.E = E;
-        g.C = at<uint16_t>(ws, L.Yexp); g.ldc = d;
-        MOE_TRY(launch_gemm_fwd_down(g, R, E, s));
-    }
+    MOE_TRY(routed_down(*shape, L, ws, weights, all, s));
     MOE_TRY(mk.mark(4));
     if (fs > 0) MOE_TRY(shared_down(*shape, L, ws, weights, s));
     MOE_TRY(mk.mark(5));
@@ -370,133 +569,34 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
                         const float *topk_w, const moe_plan_bufs *plan, moe_bf16 *dX,
                         const moe_grads *grads, void *ws, size_t ws_bytes, moe_stream stream,
                         const moe_stage_events *events) {
-    moe_status st = check_shape(shape);
+    moe_status st = check_backward_args(shape, dY, X, W_r, weights, topk_idx, topk_w, plan, dX, grads);
     if (st != MOE_OK) return st;
-    if (!ptr_ok(dY) || !ptr_ok(X) || !ptr_ok(W_r) || !ptr_ok(topk_idx) || !ptr_ok(topk_w) ||
-        !ptr_ok(dX))
-        return MOE_EINVAL;
-    if ((st = check_weights(shape, weights)) != MOE_OK) return st;
-    if ((st = check_plan(plan)) != MOE_OK) return st;
-    if (!grads || !ptr_ok(grads->dW_gate) || !ptr_ok(grads->dW_up) || !ptr_ok(grads->dW_down) ||
-        !ptr_ok(grads->dW_r) || !opt_ok(grads->dZ))
-        return MOE_EINVAL;
-    const bool shared = shape->f_shared > 0;
-    if (shared) {
-        if (!ptr_ok(grads->dWg_s) || !ptr_ok(grads->dWu_s) || !ptr_ok(grads->dWd_s)) return MOE_EINVAL;
-    } else if (grads->dWg_s || grads->dWu_s || grads->dWd_s) {
-        return MOE_EINVAL;
-    }
     if ((st = check_ws(shape, ws, ws_bytes, 1)) != MOE_OK) return st;
     const Layout L = make_layout(*shape);
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int T = (int)shape->T, d = (int)shape->d, E = (int)shape->E, k = (int)shape->k;
-    const int f = (int)shape->f, fs = (int)shape->f_shared;
-    const long R = (long)T * k;
-    const int Tn = T > 0 ? T : 1;
-    const int Rn = R > 0 ? (int)R : 1;
-    int *rowidx = at<int>(ws, L.rowidx);
-    float *wperm = at<float>(ws, L.wperm);
-    uint16_t *dA = at<uint16_t>(ws, L.dA), *dB = at<uint16_t>(ws, L.dB);
-    float *dgpart = at<float>(ws, L.dgpart);
+    const Window all{plan->offsets, 0, (int)((long)T * k)};
     float *dZ = grads->dZ ? grads->dZ : at<float>(ws, L.dZ);
     const StageMarks mk{events, s};
 
     MOE_TRY(mk.mark(0));
-    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, rowidx, wperm,
-                        at<uint16_t>(ws, L.zeros), s));
+    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, at<int>(ws, L.rowidx),
+                        at<float>(ws, L.wperm), at<uint16_t>(ws, L.zeros), s));
     MOE_TRY(mk.mark(1));
-    {   // dh' = dY W_down^T with SwiGLU backward and dg partials
-        GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
-        g.A = dY; g.lda = d; g.a_rows = rowidx; g.a_nrows = Tn;
-        g.B = weights->W_down; g.ldb = d; g.b_estride = (long)f * d;
-        g.N = f; g.K = d; g.offsets = plan->offsets; g.E = E;
-        g.E1 = at<uint16_t>(ws, L.A); g.E2 = at<uint16_t>(ws, L.B); g.ldc = f;
-        g.rowscale = wperm; g.C = dA; g.C2 = dB; g.C3 = at<uint16_t>(ws, L.Hw);
-        g.dgpart = dgpart; g.dg_ld = L.dg_parts;
-        MOE_TRY(launch_gemm_bwd_dgrad(g, R, E, s));
-    }
+    MOE_TRY(routed_dgrad(*shape, L, ws, dY, weights, all, s));
     MOE_TRY(mk.mark(2));
-    MOE_TRY(launch_softmax_bwd(dgpart, L.dg_parts, plan->route_pos, topk_w, topk_idx, T, k, E,
-                               at<float>(ws, L.dg), dZ, s));
+    MOE_TRY(launch_softmax_bwd(at<float>(ws, L.dgpart), L.dg_parts, plan->route_pos, topk_w, topk_idx,
+                               T, k, E, at<float>(ws, L.dg), dZ, s));
     MOE_TRY(mk.mark(3));
-    {   // dXperm = dA W_gate^T + dB W_up^T
-        GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
-        g.A = dA; g.A2 = dB; g.lda = f; g.a_nrows = Rn;
-        g.B = weights->W_gate; g.B2 = weights->W_up; g.ldb = f; g.b_estride = (long)d * f;
-        g.N = d; g.K = f; g.offsets = plan->offsets; g.E = E;
-        g.C = at<uint16_t>(ws, L.dXperm); g.ldc = d;
-        MOE_TRY(launch_gemm_bwd_dx(g, R, E, s));
-    }
+    MOE_TRY(routed_dx(*shape, L, ws, weights, all, s));
     MOE_TRY(mk.mark(4));
-    {   // dW_gate[e] = Xperm_e^T dA_e, dW_up[e] = Xperm_e^T dB_e
-        GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
-        g.A = X; g.lda = d; g.a_rows = rowidx; g.a_nrows = Tn;
-        g.B = dA; g.ldb = f; g.b_nrows = Rn;
-        g.M = d; g.N = f; g.offsets = plan->offsets; g.E = E;
-        g.Cf = grads->dW_gate; g.c_estride = (long)d * f; g.ldc = f;
-        MOE_TRY(launch_gemm_wgrad(g, E, s));
-        g.B = dB; g.Cf = grads->dW_up;
-        MOE_TRY(launch_gemm_wgrad(g, E, s));
-    }
+    MOE_TRY(routed_wgrad_up(*shape, L, ws, X, grads, all, false, s));
     MOE_TRY(mk.mark(5));
-    {   // dW_down[e] = (w H_e)^T dYperm_e
-        GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
-        g.A = at<uint16_t>(ws, L.Hw); g.lda = f; g.a_nrows = Rn;
-        g.B = dY; g.ldb = d; g.b_rows = rowidx; g.b_nrows = Tn;
-        g.M = f; g.N = d; g.offsets = plan->offsets; g.E = E;
-        g.Cf = grads->dW_down; g.c_estride = (long)f * d; g.ldc = d;
-        MOE_TRY(launch_gemm_wgrad(g, E, s));
-    }
+    MOE_TRY(routed_wgrad_down(*shape, L, ws, dY, grads, all, false, s));
     MOE_TRY(mk.mark(6));
-    uint16_t *dXsh = nullptr;
+    const bool shared = shape->f_shared > 0;
     if (shared) {
-        uint16_t *dAs = at<uint16_t>(ws, L.dAs), *dBs = at<uint16_t>(ws, L.dBs);
-        dXsh = at<uint16_t>(ws, L.dXsh);
-        {
-            GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
-            g.A = dY; g.lda = d; g.a_nrows = Tn; g.M = T;
-            g.B = weights->Wd_s; g.ldb = d;
-            g.N = fs; g.K = d;
-            g.E1 = at<uint16_t>(ws, L.As); g.E2 = at<uint16_t>(ws, L.Bs); g.ldc = fs;
-            g.C = dAs; g.C2 = dBs;
-            MOE_TRY(launch_gemm_bwd_dgrad(g, T, 1, s));
-        }
-        MOE_TRY(mk.mark(7));
-        {
-            GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
-            g.A = dAs; g.A2 = dBs; g.lda = fs; g.a_nrows = Tn; g.M = T;
-            g.B = weights->Wg_s; g.B2 = weights->Wu_s; g.ldb = fs;
-            g.N = d; g.K = fs;
-            g.C = dXsh; g.ldc = d;
-            MOE_TRY(launch_gemm_bwd_dx(g, T, 1, s));
-        }
-        MOE_TRY(mk.mark(8));
-        {
-            GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
-            g.A = X; g.lda = d; g.a_nrows = Tn;
-            g.B = dAs; g.ldb = fs; g.b_nrows = Tn;
-            g.M = d; g.N = fs; g.K = T;
-            g.Cf = grads->dWg_s; g.ldc = fs;
-            MOE_TRY(launch_gemm_wgrad(g, 1, s));
-            g.B = dBs; g.Cf = grads->dWu_s;
-            MOE_TRY(launch_gemm_wgrad(g, 1, s));
-        }
-        {
-            GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
-            g.A = at<uint16_t>(ws, L.Hs); g.lda = fs; g.a_nrows = Tn;
-            g.B = dY; g.ldb = d; g.b_nrows = Tn;
-            g.M = fs; g.N = d; g.K = T;
-            g.Cf = grads->dWd_s; g.ldc = d;
-            MOE_TRY(launch_gemm_wgrad(g, 1, s));
-        }
+        MOE_TRY(shared_backward(*shape, L, ws, dY, X, weights, grads, mk, s));
     } else {
         MOE_TRY(mk.mark(7));
         MOE_TRY(mk.mark(8));
@@ -504,9 +604,105 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
     MOE_TRY(mk.mark(9));
     MOE_TRY(launch_dwr(X, dZ, T, d, E, at<float>(ws, L.dwr_part), grads->dW_r, s));
     MOE_TRY(mk.mark(10));
-    MOE_TRY(launch_reverse_combine(at<uint16_t>(ws, L.dXperm), dXsh, dZ, W_r, plan->route_pos, T, d,
-                                   k, E, dX, s));
+    MOE_TRY(launch_reverse_combine(at<uint16_t>(ws, L.dXperm), shared ? at<uint16_t>(ws, L.dXsh) : nullptr,
+                                   dZ, W_r, plan->route_pos, T, d, k, E, nullptr, dX, s));
     MOE_TRY(mk.mark(11));
+    return MOE_OK;
+}
+
+size_t moe_ring_workspace_bytes(const moe_shape *shape, int64_t ring_rows, int with_backward) {
+    if (check_shape(shape) != MOE_OK || check_ring(ring_rows) != MOE_OK) return 0;
+    const Layout L = make_layout(*shape, ring_act_rows(*shape, ring_rows));
+    return with_backward ? L.bwd_total : L.fwd_total;
+}
+
+moe_status moe_forward_ring(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
+                            const int32_t *topk_idx, const float *topk_w, const moe_plan_bufs *plan,
+                            moe_bf16 *Y, int64_t ring_rows, int save_for_backward, void *ws,
+                            size_t ws_bytes, moe_stream stream) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if (!ptr_ok(X) || !ptr_ok(topk_idx) || !ptr_ok(topk_w) || !ptr_ok(Y)) return MOE_EINVAL;
+    if ((st = check_weights(shape, weights)) != MOE_OK) return st;
+    if ((st = check_plan(plan)) != MOE_OK) return st;
+    if ((st = check_ring(ring_rows)) != MOE_OK) return st;
+    if (!ptr_ok(ws)) return MOE_EINVAL;
+    const Layout L = make_layout(*shape, ring_act_rows(*shape, ring_rows));
+    if (ws_bytes < L.fwd_total) return MOE_ENOSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int T = (int)shape->T, d = (int)shape->d, E = (int)shape->E, k = (int)shape->k;
+    const int fs = (int)shape->f_shared;
+    const long R = (long)T * k;
+    const int nwin = ring_windows(*shape, ring_rows);
+    int *coff = at<int>(ws, L.coff);
+
+    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, at<int>(ws, L.rowidx),
+                        at<float>(ws, L.wperm), at<uint16_t>(ws, L.zeros), s));
+    if (fs > 0) {   // first: its output seeds every token's accumulator
+        MOE_TRY(shared_up(*shape, L, ws, X, weights, save_for_backward != 0, s));
+        MOE_TRY(shared_down(*shape, L, ws, weights, s));
+    }
+    // reverse window order: the ring ends up holding the first window, the
+    // one the backward consumes first
+    for (int m = nwin - 1; m >= 0; --m) {
+        const int w0 = (int)(m * ring_rows);
+        const int w1 = (int)(R < w0 + ring_rows ? R : w0 + ring_rows);
+        const Window win{coff, w0, w1};
+        MOE_TRY(launch_clip_offsets(plan->offsets, E, w0, w1, coff, s));
+        MOE_TRY(routed_up(*shape, L, ws, X, weights, win, true, save_for_backward != 0, s));
+        MOE_TRY(routed_down(*shape, L, ws, weights, win, s));
+        MOE_TRY(launch_window_accum(at<uint16_t>(ws, L.Yexp), w0, w1, topk_w,
+                                    plan->route_pos, T, d, k, at<float>(ws, L.acc), m == nwin - 1,
+                                    fs > 0 ? at<uint16_t>(ws, L.Ysh) : nullptr, m == 0 ? Y : nullptr,
+                                    s));
+    }
+    return MOE_OK;
+}
+
+moe_status moe_backward_ring(const moe_shape *shape, const moe_bf16 *dY, const moe_bf16 *X,
+                             const moe_bf16 *W_r, const moe_weights *weights, const int32_t *topk_idx,
+                             const float *topk_w, const moe_plan_bufs *plan, moe_bf16 *dX,
+                             const moe_grads *grads, int64_t ring_rows, void *ws, size_t ws_bytes,
+                             moe_stream stream) {
+    moe_status st = check_backward_args(shape, dY, X, W_r, weights, topk_idx, topk_w, plan, dX, grads);
+    if (st != MOE_OK) return st;
+    if ((st = check_ring(ring_rows)) != MOE_OK) return st;
+    if (!ptr_ok(ws)) return MOE_EINVAL;
+    const Layout L = make_layout(*shape, ring_act_rows(*shape, ring_rows));
+    if (ws_bytes < L.bwd_total) return MOE_ENOSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int T = (int)shape->T, d = (int)shape->d, E = (int)shape->E, k = (int)shape->k;
+    const long R = (long)T * k;
+    const int nwin = ring_windows(*shape, ring_rows);
+    const bool shared = shape->f_shared > 0;
+    int *coff = at<int>(ws, L.coff);
+    float *acc = at<float>(ws, L.acc);
+    float *dZ = grads->dZ ? grads->dZ : at<float>(ws, L.dZ);
+    const StageMarks none{nullptr, s};
+
+    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, at<int>(ws, L.rowidx),
+                        at<float>(ws, L.wperm), at<uint16_t>(ws, L.zeros), s));
+    if (shared) MOE_TRY(shared_backward(*shape, L, ws, dY, X, weights, grads, none, s));
+    for (int m = 0; m < nwin; ++m) {
+        const int w0 = (int)(m * ring_rows);
+        const int w1 = (int)(R < w0 + ring_rows ? R : w0 + ring_rows);
+        const Window win{coff, w0, w1};
+        MOE_TRY(launch_clip_offsets(plan->offsets, E, w0, w1, coff, s));
+        // the forward left window 0 in the ring; later windows recompute only
+        // the pre-activations the backward reads
+        if (m > 0) MOE_TRY(routed_up(*shape, L, ws, X, weights, win, false, true, s));
+        MOE_TRY(routed_dgrad(*shape, L, ws, dY, weights, win, s));
+        MOE_TRY(routed_dx(*shape, L, ws, weights, win, s));
+        MOE_TRY(launch_window_accum(at<uint16_t>(ws, L.dXperm), w0, w1, nullptr,
+                                    plan->route_pos, T, d, k, acc, m == 0,
+                                    shared ? at<uint16_t>(ws, L.dXsh) : nullptr, nullptr, s));
+        MOE_TRY(routed_wgrad_up(*shape, L, ws, X, grads, win, m > 0, s));
+        MOE_TRY(routed_wgrad_down(*shape, L, ws, dY, grads, win, m > 0, s));
+    }
+    MOE_TRY(launch_softmax_bwd(at<float>(ws, L.dgpart), L.dg_parts, plan->route_pos, topk_w, topk_idx,
+                               T, k, E, at<float>(ws, L.dg), dZ, s));
+    MOE_TRY(launch_dwr(X, dZ, T, d, E, at<float>(ws, L.dwr_part), grads->dW_r, s));
+    MOE_TRY(launch_reverse_combine(nullptr, nullptr, dZ, W_r, plan->route_pos, T, d, k, E, acc, dX, s));
     return MOE_OK;
 }
 

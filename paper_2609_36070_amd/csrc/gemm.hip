@@ -7,12 +7,14 @@
 // positions p of e's region [offsets[e], offsets[e+1]):
 //
 //   FWD_UP     A_e = X[tok(p)] W_gate[e], B_e = X[tok(p)] W_up[e],
-//              H = silu(A) * B                         (A, B kept for backward)
+//              H = silu(A) * B      (A, B kept for backward; H may be skipped
+//                                    when only A, B are recomputed)
 //   FWD_DOWN   Yexp = H W_down[e]
 //   BWD_DGRAD  dh' = dY[tok(p)] W_down[e]^T, then dg partials <dh', h>,
 //              dA = w dh' * B * silu'(A), dB = w dh' * silu(A), Hw = w * h
 //   BWD_DX     dXperm = dA W_gate[e]^T + dB W_up[e]^T  (one K loop over both)
-//   WGRAD      dW[e] = P_e^T Q_e, K = the expert's ragged route count
+//   WGRAD      dW[e] = P_e^T Q_e (or dW[e] += P_e^T Q_e), K = the expert's
+//              ragged route count
 //
 // The dispatch gather is fused into the operand loads: A rows (or WGRAD k
 // rows) are read through the plan's token index, so no expert-contiguous
@@ -152,6 +154,30 @@ DEV bool map_tile(int b, int nblocks, int tiles_m, int ntn, int &mt, int &nt) {
     return true;
 }
 
+// Weight-gradient raster.  A tile's cost is its expert's route count, so
+// XCDs that each ran whole experts would wait for the heaviest one (or idle
+// outright when a window of the bounded-memory backward holds only some of
+// the experts).  Instead every expert's ntm x ntn tiles are cut into 8 equal
+// runs, one per XCD, and each XCD walks its run of expert 0, then of expert
+// 1, and so on: all XCDs carry the same work, and the blocks an XCD runs at
+// once cover a GM x (run / GM) patch of one expert, sharing its A and B
+// panels in that XCD's L2.  Grid: 8 * groups * ceil(ntm * ntn / 8) blocks.
+DEV bool map_tile_wgrad(int b, int groups, int ntm, int ntn, int &cm, int &nt) {
+    constexpr int NX = 8, GM = 4;
+    const int per_e = ntm * ntn;
+    const int q = (per_e + NX - 1) / NX;
+    const int j = b / NX;
+    const int e = j / q, t = (b % NX) * q + j % q;
+    if (e >= groups || t >= per_e) return false;
+    const int group = t / (GM * ntn);
+    const int first = group * GM;
+    const int gm = min(GM, ntm - first);
+    const int within = t - group * GM * ntn;
+    cm = e * ntm + first + within % gm;
+    nt = within / gm;
+    return true;
+}
+
 template <int MODE, bool GROUPED>
 __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int *__restrict__ a_rows, const int *__restrict__ b_rows) {
     using Tr = Traits<MODE>;
@@ -213,8 +239,8 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
         klen = g.K;
     } else {
         const int ntn = g.N / BN, ntm = g.M / BM;
-        int cm = 0;   // (expert, m-tile) pair, m-tile fastest
-        if (!map_tile(blockIdx.x, gridDim.x, g.tiles_m, ntn, cm, ntile)) return;
+        int cm = 0;   // (expert, m-tile) pair
+        if (!map_tile_wgrad(blockIdx.x, g.tiles_m / ntm, ntm, ntn, cm, ntile)) return;
         m0 = (cm % ntm) * BM;
         e = cm / ntm;
         n0 = ntile * BN;
@@ -465,7 +491,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
 #pragma unroll
                         for (int k = 0; k < 8; ++k) h[k] = silu_f(a[k]) * b[k];
                         const long o = (long)p * g.ldc + fcol0 + c;
-                        st_u32x4(g.C + o, pack_bf8(h));
+                        if (g.C) st_u32x4(g.C + o, pack_bf8(h));
                         if (g.C2) {
                             st_u32x4(g.C2 + o, pack_bf8(a));
                             st_u32x4(g.C3 + o, pack_bf8(b));
@@ -546,18 +572,19 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
 #pragma unroll
                 for (int q = 0; q < 16; ++q) {
                     const int m = m0 + wm * WM + 32 * i + 8 * (q >> 2) + 4 * lhalf + (q & 3);
-                    out[(long)m * g.ldc + col] = acc[i][j][q];
+                    float *o = out + (long)m * g.ldc + col;
+                    *o = g.accumulate ? *o + acc[i][j][q] : acc[i][j][q];
                 }
             }
     }
 }
 
 template <int MODE>
-hipError_t launch_mode(GemmArgs g, int tiles_m, int ntn, hipStream_t st) {
+hipError_t launch_mode(GemmArgs g, int tiles_m, int ntn, hipStream_t st, long grid_blocks = 0) {
     const long tiles = (long)tiles_m * ntn;
     if (tiles <= 0) return hipSuccess;
     g.tiles_m = tiles_m;
-    const unsigned grid = (unsigned)((tiles + 7) / 8 * 8);
+    const unsigned grid = (unsigned)(grid_blocks > 0 ? grid_blocks : (tiles + 7) / 8 * 8);
     if (g.offsets)
         gemm_kernel<MODE, true><<<dim3(grid), dim3(NTHREADS), 0, st>>>(g, g.a_rows, g.b_rows);
     else
@@ -590,5 +617,6 @@ hipError_t launch_gemm_bwd_dx(const GemmArgs &g, long rows, int groups, hipStrea
     return launch_mode<BWD_DX>(g, mtiles(g, rows, groups), g.N / BN, st);
 }
 hipError_t launch_gemm_wgrad(const GemmArgs &g, int groups, hipStream_t st) {
-    return launch_mode<WGRAD>(g, groups * (g.M / BM), g.N / BN, st);
+    const long per_e = (long)(g.M / BM) * (g.N / BN);
+    return launch_mode<WGRAD>(g, groups * (g.M / BM), g.N / BN, st, 8L * groups * ((per_e + 7) / 8));
 }

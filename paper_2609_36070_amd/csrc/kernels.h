@@ -39,6 +39,7 @@ struct GemmArgs {
     const float *rowscale = nullptr;              // BWD_DGRAD: router weight per row
     float *dgpart = nullptr;
     int dg_ld = 0;
+    int accumulate = 0;                // WGRAD: add to Cf instead of overwriting it
     int tiles_m = 0;                   // set by the launcher: m-tile slots of the raster
 };
 
@@ -105,6 +106,10 @@ hipError_t launch_softmax_bwd(const float *dgpart, int nparts, const int *route_
                               float *dg_out, float *dZ, hipStream_t st);
 hipError_t launch_reverse_combine(const uint16_t *dXperm, const uint16_t *dXsh, const float *dZ,
                                   const uint16_t *W_r, const int *route_pos, int T, int d, int k,
-                                  int E, uint16_t *dX, hipStream_t st);
+                                  int E, const float *dXacc, uint16_t *dX, hipStream_t st);
+hipError_t launch_window_accum(const uint16_t *ring, int w0, int w1, const float *topk_w,
+                               const int *route_pos, int T, int d, int k, float *acc, int init,
+                               const uint16_t *add, uint16_t *out, hipStream_t st);
+hipError_t launch_clip_offsets(const int *offsets, int E, int w0, int w1, int *out, hipStream_t st);
 hipError_t launch_dwr(const uint16_t *X, const float *dZ, int T, int d, int E, float *part,
                       float *dWr, hipStream_t st);

@@ -160,6 +160,7 @@ __global__ __launch_bounds__(256) void reverse_combine_kernel(const uint16_t *__
                                                               const uint16_t *__restrict__ Wr,
                                                               const int *__restrict__ route_pos,
                                                               int T, int d, int k, int E, int R,
+                                                              const float *__restrict__ dXacc,
                                                               uint16_t *__restrict__ dX) {
     __shared__ float dz[256];
     const int nc = d / 8;
@@ -178,7 +179,17 @@ __global__ __launch_bounds__(256) void reverse_combine_kernel(const uint16_t *__
         }
         for (int c = threadIdx.x; c < nc; c += 256) {
             float acc[8];
-            if (dXsh) {
+            if (dXacc) {
+                // shared-expert and routed terms already summed per token
+                // (bounded-memory backward)
+                const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(dXacc + (long)t * d + 8 * c);
+                const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(dXacc + (long)t * d + 8 * c + 4);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    acc[q] = lo[q];
+                    acc[4 + q] = hi[q];
+                }
+            } else if (dXsh) {
                 const u32x4_t v = ld_u32x4(dXsh + (long)t * d + 8 * c);
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
@@ -189,14 +200,16 @@ __global__ __launch_bounds__(256) void reverse_combine_kernel(const uint16_t *__
 #pragma unroll
                 for (int q = 0; q < 8; ++q) acc[q] = 0.f;
             }
+            if (!dXacc) {
 #pragma unroll
-            for (int s = 0; s < 16; ++s) {
-                if (s < k && pos[s] >= 0) {
-                    const u32x4_t v = ld_u32x4(dXperm + (long)pos[s] * d + 8 * c);
+                for (int s = 0; s < 16; ++s) {
+                    if (s < k && pos[s] >= 0) {
+                        const u32x4_t v = ld_u32x4(dXperm + (long)pos[s] * d + 8 * c);
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        acc[2 * q] = acc[2 * q] + bf_lo(v[q]);
-                        acc[2 * q + 1] = acc[2 * q + 1] + bf_hi(v[q]);
+                        for (int q = 0; q < 4; ++q) {
+                            acc[2 * q] = acc[2 * q] + bf_lo(v[q]);
+                            acc[2 * q + 1] = acc[2 * q + 1] + bf_hi(v[q]);
+                        }
                     }
                 }
             }
@@ -230,6 +243,90 @@ __global__ __launch_bounds__(256) void reverse_combine_kernel(const uint16_t *__
             st_u32x4(dX + (long)t * d + 8 * c, o);
         }
     }
+}
+
+// Bounded-memory execution: per-route rows of the positions [w0, w1) live in
+// a ring (row p at ring row p - w0).  For every token, the routes that fall
+// in the window are added to an fp32 per-token accumulator in ascending slot
+// order (optionally weighted by the gate weight); windows are visited in a
+// fixed order, so the sums are deterministic.  `init` starts the accumulator
+// at `add` (a bf16 row per token, the shared-expert term) or at zero; with
+// `out` the result is rounded once into out instead of being stored in acc.
+// A single window covering every route therefore adds in exactly the order
+// of the one-pass combine.
+__global__ __launch_bounds__(256) void window_accum_kernel(const uint16_t *__restrict__ ring, int w0,
+                                                           int w1, const float *__restrict__ topk_w,
+                                                           const int *__restrict__ route_pos, int T,
+                                                           int d, int k, float *__restrict__ acc,
+                                                           int init, const uint16_t *__restrict__ add,
+                                                           uint16_t *__restrict__ out) {
+    const int nc = d / 8;
+    for (int t = blockIdx.x; t < T; t += gridDim.x) {
+        int pos[16];
+        float wt[16];
+        bool any = false;
+#pragma unroll
+        for (int s = 0; s < 16; ++s) {
+            pos[s] = -1;
+            wt[s] = 1.f;
+            if (s < k) {
+                const int p = route_pos[(long)t * k + s];
+                pos[s] = (p >= w0 && p < w1) ? p - w0 : -1;
+                if (topk_w) wt[s] = topk_w[(long)t * k + s];
+                any = any || pos[s] >= 0;
+            }
+        }
+        if (!any && !init && !out) continue;   // nothing of this token in the window
+        for (int c = threadIdx.x; c < nc; c += 256) {
+            float a[8];
+            float *ap = acc + (long)t * d + 8 * c;
+            if (init && add) {
+                const u32x4_t v = ld_u32x4(add + (long)t * d + 8 * c);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    a[2 * q] = bf_lo(v[q]);
+                    a[2 * q + 1] = bf_hi(v[q]);
+                }
+            } else if (init) {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) a[q] = 0.f;
+            } else {
+                const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(ap);
+                const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(ap + 4);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    a[q] = lo[q];
+                    a[4 + q] = hi[q];
+                }
+            }
+#pragma unroll
+            for (int s = 0; s < 16; ++s) {
+                if (s < k && pos[s] >= 0) {
+                    const u32x4_t v = ld_u32x4(ring + (long)pos[s] * d + 8 * c);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        a[2 * q] = a[2 * q] + wt[s] * bf_lo(v[q]);
+                        a[2 * q + 1] = a[2 * q + 1] + wt[s] * bf_hi(v[q]);
+                    }
+                }
+            }
+            if (out) {
+                u32x4_t o;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) o[q] = pack_bf2(a[2 * q], a[2 * q + 1]);
+                st_u32x4(out + (long)t * d + 8 * c, o);
+            } else {
+                *reinterpret_cast<f32x4_t *>(ap) = f32x4_t{a[0], a[1], a[2], a[3]};
+                *reinterpret_cast<f32x4_t *>(ap + 4) = f32x4_t{a[4], a[5], a[6], a[7]};
+            }
+        }
+    }
+}
+
+// Expert regions restricted to the window [w0, w1).
+__global__ __launch_bounds__(256) void clip_offsets_kernel(const int *__restrict__ offsets, int E,
+                                                           int w0, int w1, int *__restrict__ out) {
+    for (int e = threadIdx.x; e <= E; e += 256) out[e] = min(max(offsets[e], w0), w1);
 }
 
 // dW_r = X^T dZ in two fixed-order stages.  Stage 1: block (column block,
@@ -328,10 +425,24 @@ hipError_t launch_softmax_bwd(const float *dgpart, int nparts, const int *route_
 
 hipError_t launch_reverse_combine(const uint16_t *dXperm, const uint16_t *dXsh, const float *dZ,
                                   const uint16_t *W_r, const int *route_pos, int T, int d, int k,
-                                  int E, uint16_t *dX, hipStream_t st) {
+                                  int E, const float *dXacc, uint16_t *dX, hipStream_t st) {
     if (T == 0) return hipSuccess;
     reverse_combine_kernel<<<dim3(rows_grid(T)), dim3(256), 0, st>>>(dXperm, dXsh, dZ, W_r, route_pos,
-                                                                      T, d, k, E, T * k, dX);
+                                                                      T, d, k, E, T * k, dXacc, dX);
+    return hipGetLastError();
+}
+
+hipError_t launch_window_accum(const uint16_t *ring, int w0, int w1, const float *topk_w,
+                               const int *route_pos, int T, int d, int k, float *acc, int init,
+                               const uint16_t *add, uint16_t *out, hipStream_t st) {
+    if (T == 0) return hipSuccess;
+    window_accum_kernel<<<dim3(rows_grid(T)), dim3(256), 0, st>>>(ring, w0, w1, topk_w, route_pos, T, d,
+                                                                   k, acc, init, add, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_clip_offsets(const int *offsets, int E, int w0, int w1, int *out, hipStream_t st) {
+    clip_offsets_kernel<<<dim3(1), dim3(256), 0, st>>>(offsets, E, w0, w1, out);
     return hipGetLastError();
 }
 

@@ -31,9 +31,13 @@ def _dev_bf16(a, device):
 class DeviceLayer:
     """All tensors of one layer instance on the GPU, laid out as the C ABI expects."""
 
-    def __init__(self, w: Workload, inputs: dict, device="cuda", with_backward=None, mx=False):
+    def __init__(self, w: Workload, inputs: dict, device="cuda", with_backward=None, mx=False,
+                 ring_rows=None):
+        """ring_rows: run forward/backward in bounded memory, with the per-route
+        activations in a ring of that many rows (None: room for all T*k routes)."""
         self.w = w
         self.mx = mx
+        self.ring_rows = ring_rows
         self.device = torch.device(device)
         self.with_backward = w.backward if with_backward is None else with_backward
         T, d, E, k, f, fs = w.T, w.d, w.E, w.k, w.f, w.f_s
@@ -61,7 +65,12 @@ class DeviceLayer:
         self.perm = _empty((R,), i32, dev)
         self.route_pos = _empty((R,), i32, dev)
         self.Y = _empty((T, d), bf, dev)
-        nbytes = B.moe_workspace_bytes(self.shape, self.with_backward)
+        if ring_rows is None:
+            nbytes = B.moe_workspace_bytes(self.shape, self.with_backward)
+        else:
+            if mx:
+                raise ValueError("the MXFP8 forward has no bounded-memory variant")
+            nbytes = B.moe_ring_workspace_bytes(self.shape, ring_rows, self.with_backward)
         if nbytes == 0:
             raise ValueError(f"unsupported shape {w}")
         if mx:
@@ -111,10 +120,24 @@ class DeviceLayer:
 
     def forward(self, save_for_backward=None, stream=None, events=None):
         save = self.with_backward if save_for_backward is None else save_for_backward
+        if self.ring_rows is not None:
+            if events is not None:
+                raise ValueError("stage events are not recorded in bounded-memory execution")
+            B.moe_forward_ring(self.shape, self.X, self.weights, self.topk_idx, self.topk_w,
+                               self.plan_bufs, self.Y, self.ring_rows, save, self.ws,
+                               stream=stream)
+            return
         B.moe_forward(self.shape, self.X, self.weights, self.topk_idx, self.topk_w,
                       self.plan_bufs, self.Y, save, self.ws, stream=stream, events=events)
 
     def backward(self, stream=None, events=None):
+        if self.ring_rows is not None:
+            if events is not None:
+                raise ValueError("stage events are not recorded in bounded-memory execution")
+            B.moe_backward_ring(self.shape, self.dY, self.X, self.W_r, self.weights,
+                                self.topk_idx, self.topk_w, self.plan_bufs, self.dX, self.grads,
+                                self.ring_rows, self.ws, stream=stream)
+            return
         B.moe_backward(self.shape, self.dY, self.X, self.W_r, self.weights, self.topk_idx,
                        self.topk_w, self.plan_bufs, self.dX, self.grads, self.ws, stream=stream,
                        events=events)
@@ -144,6 +167,8 @@ class DeviceLayer:
 
     # -- inspection -------------------------------------------------------
     def ws_tensor(self, which, dtype, shape):
+        if self.ring_rows is not None and which != B.WS_ERROR:
+            raise ValueError("named regions describe the one-pass layout only")
         off, nbytes = B.moe_workspace_region(self.shape, self.with_backward, which)
         return self.ws[off:off + nbytes].view(dtype).view(*shape)
 

@@ -129,6 +129,57 @@ def test_plan_forward_backward_validation():
                           None, None) == B.MOE_EINVAL
 
 
+@pytest.mark.parametrize("name", sorted(WORKLOADS))
+def test_ring_workspace_sizes(name):
+    """The ring workspace shrinks with the ring and never exceeds the one-pass
+    one; a ring holding every route needs exactly the one-pass activations."""
+    w = WORKLOADS[name]
+    sh = B.make_shape(w.T, w.d, w.E, w.k, w.f, w.f_s)
+    R = w.T * w.k
+    for bwd in (False, True):
+        full = B.moe_workspace_bytes(sh, bwd)
+        sizes = [B.moe_ring_workspace_bytes(sh, c, bwd) for c in (256, max(R // 2, 1), R, 4 * R)]
+        assert all(0 < b for b in sizes)
+        assert sizes[0] <= sizes[1] <= sizes[2] == sizes[3]
+        # the ring adds an fp32 per-token accumulator and the clipped offsets
+        extra = w.T * w.d * 4 + 4 * (w.E + 1) + 2 * 256
+        assert sizes[2] <= full + extra
+        per_row = (3 * w.f + w.d + (3 * w.f + w.d if bwd else 0)) * 2
+        assert sizes[2] - sizes[1] >= (R - R // 2) * per_row - 16 * 256
+
+
+def test_ring_validation():
+    L = B.lib()
+    sh = B.make_shape(64, 256, 8, 2, 256)
+    plan = B.MoePlanBufs(FAKE, FAKE, FAKE, FAKE)
+    w = B.MoeWeights(FAKE, FAKE, FAKE, None, None, None)
+    g = B.MoeGrads(FAKE, FAKE, FAKE, FAKE, None, None, None, None)
+    big = 1 << 40
+    assert B.moe_ring_workspace_bytes(sh, 0, True) == 0
+    assert B.moe_ring_workspace_bytes(sh, 1 << 31, True) == 0
+    assert B.moe_ring_workspace_bytes(B.make_shape(16, 100, 8, 2, 256), 256, False) == 0
+
+    def fwd(ring, ws_bytes=big, weights=w, Y=FAKE):
+        return L.moe_forward_ring(ctypes.byref(sh), FAKE, ctypes.byref(weights), FAKE, FAKE,
+                                  ctypes.byref(plan), Y, ring, 1, FAKE, ws_bytes, None)
+
+    def bwd(ring, ws_bytes=big, grads=g):
+        return L.moe_backward_ring(ctypes.byref(sh), FAKE, FAKE, FAKE, ctypes.byref(w), FAKE,
+                                   FAKE, ctypes.byref(plan), FAKE, ctypes.byref(grads), ring, FAKE,
+                                   ws_bytes, None)
+
+    assert fwd(0) == B.MOE_EINVAL and bwd(-5) == B.MOE_EINVAL
+    assert fwd(1 << 31) == B.MOE_EUNSUPPORTED
+    assert fwd(64, Y=MISALIGNED) == B.MOE_EINVAL
+    assert fwd(64, weights=B.MoeWeights(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)) == B.MOE_EINVAL
+    need_f = B.moe_ring_workspace_bytes(sh, 64, False)
+    need_b = B.moe_ring_workspace_bytes(sh, 64, True)
+    assert fwd(64, ws_bytes=need_f - 1) == B.MOE_ENOSPACE
+    assert bwd(64, ws_bytes=need_f) == B.MOE_ENOSPACE       # backward needs the larger one
+    assert bwd(64, ws_bytes=need_b - 1) == B.MOE_ENOSPACE
+    assert bwd(64, grads=B.MoeGrads(FAKE, FAKE, None, FAKE, None, None, None, None)) == B.MOE_EINVAL
+
+
 def test_schedule_workspace_and_validation():
     L = B.lib()
     # error word + per-(rank, chunk) flags + per-(rank, chunk, expert) counts

@@ -1,0 +1,159 @@
+"""GPU parity of bounded-memory execution (§3.3: the macrobatch ring buffer,
+reverse macrobatch order and the ring-aware forward replay in the backward).
+
+Every case is checked twice: against the oracle to the usual per-tensor bar,
+and against the one-pass path on the same inputs.  What the windows cannot
+change must not change at all: routing, the plan, dZ and dW_r are compared
+bitwise, and with a single window every output is.  With several windows Y,
+dX and the routed weight gradients differ from the one-pass results only by
+fp32 summation order.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe_oracle as O
+from paper_2609_36070_amd.layer import DeviceLayer
+from paper_2609_36070_amd.workloads import WORKLOADS, Workload, make_inputs
+from tests.parity import assert_close, check_route_and_plan, say, to_np, weights_dict
+
+pytestmark = pytest.mark.gpu
+
+RAGGED_TRAIN = Workload("ragged_train", T=1000, d=512, E=6, k=2, f=512, f_s=256, bias_std=0.5,
+                        backward=True)
+
+EXACT = ("logits", "topk_idx", "topk_w", "counts", "offsets", "perm", "route_pos", "dZ", "dW_r")
+SUMMED = ("Y", "dX", "dW_gate", "dW_up", "dW_down")
+SHARED = ("dWg_s", "dWu_s", "dWd_s")
+
+
+def run_pair(w, ring_rows, seed):
+    """The one-pass layer and the ring layer on the same inputs."""
+    inp = make_inputs(w, seed)
+    say(f"[gpu] {w.name} T={w.T} d={w.d} E={w.E} k={w.k} f={w.f} f_s={w.f_s} "
+        f"ring_rows={ring_rows} seed={seed}")
+    full = DeviceLayer(w, inp)
+    full.step()
+    ring = DeviceLayer(w, inp, ring_rows=ring_rows)
+    assert ring.ws.numel() <= full.ws.numel() + w.T * w.d * 4 + 4096
+    ring.step()
+    torch.cuda.synchronize()
+    return full, ring, inp
+
+
+def compare_to_one_pass(full, ring, w, ring_rows):
+    one_window = ring_rows >= w.T * w.k
+    names = EXACT + SUMMED + (SHARED if w.f_s else ())
+    for n in names:
+        a, b = getattr(full, n), getattr(ring, n)
+        if n in EXACT or n in SHARED or one_window:
+            assert torch.equal(a, b), f"{n} differs from the one-pass result"
+        else:
+            assert_close(f"{n} (ring vs one-pass)", to_np(b), to_np(a), rel=4e-3)
+    say("  exact: " + ", ".join(n for n in names if torch.equal(getattr(full, n), getattr(ring, n))))
+
+
+def oracle_parity(ring, inp, w):
+    Zo, idx_g = check_route_and_plan(ring, inp, w)
+    w_orc = O.gate_weights(Zo, idx_g)
+    fw = O.moe_forward(inp["X"], weights_dict(inp), idx_g, w_orc)
+    assert_close("Y", to_np(ring.Y), fw["Y"])
+    g = O.moe_backward(inp["X"], inp["W_r"], weights_dict(inp), idx_g, w_orc, inp["dY"])
+    for n in ("dX", "dW_gate", "dW_up", "dW_down", "dZ", "dW_r") + (SHARED if w.f_s else ()):
+        assert_close(n, to_np(getattr(ring, n)), g[n])
+
+
+@pytest.mark.parametrize("ring_rows", [2000, 8000, 256, 700, 97],
+                         ids=["one_window", "larger_than_batch", "256", "700_ragged", "97_many"])
+def test_ring_parity(ring_rows):
+    w = RAGGED_TRAIN                       # T * k = 2000 routes
+    full, ring, inp = run_pair(w, ring_rows, seed=11)
+    oracle_parity(ring, inp, w)
+    compare_to_one_pass(full, ring, w, ring_rows)
+
+
+@pytest.mark.parametrize("w,ring_rows", [
+    (Workload("one_token", T=1, d=256, E=8, k=3, f=256, f_s=256, backward=True), 2),
+    (Workload("k_equals_E", T=300, d=256, E=4, k=4, f=512, bias_std=0.5, backward=True), 256),
+    (Workload("empty_experts", T=40, d=256, E=64, k=1, f=256, bias_std=3.0, backward=True), 16),
+    (Workload("many_tiles", T=700, d=768, E=3, k=2, f=768, backward=True), 600),
+], ids=lambda v: v.name if isinstance(v, Workload) else str(v))
+def test_ring_edge_shapes(w, ring_rows):
+    full, ring, inp = run_pair(w, ring_rows, seed=12)
+    oracle_parity(ring, inp, w)
+    compare_to_one_pass(full, ring, w, ring_rows)
+
+
+def test_ring_no_tokens():
+    """An empty batch: one empty window; every weight gradient is zero."""
+    w = Workload("no_tokens", T=0, d=256, E=8, k=2, f=256, f_s=256, backward=True)
+    ring = DeviceLayer(w, make_inputs(w, 0), ring_rows=256)
+    for n in ("dW_gate", "dW_up", "dW_down", "dW_r") + SHARED:
+        getattr(ring, n).fill_(5.0)
+    ring.step()
+    torch.cuda.synchronize()
+    for n in ("dW_gate", "dW_up", "dW_down", "dW_r") + SHARED:
+        assert torch.count_nonzero(getattr(ring, n)) == 0, n
+
+
+def test_ring_determinism_and_graph_replay():
+    w = RAGGED_TRAIN
+    ring = DeviceLayer(w, make_inputs(w, 13), ring_rows=700)
+    ring.step()
+    torch.cuda.synchronize()
+    names = EXACT + SUMMED + SHARED
+    first = {n: getattr(ring, n).clone() for n in names}
+    for rep in range(3):
+        ring.step()
+        torch.cuda.synchronize()
+        for n in names:
+            assert torch.equal(getattr(ring, n), first[n]), (rep, n)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        ring.step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        ring.step()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for n in names:
+            getattr(ring, n).fill_(-7 if getattr(ring, n).dtype == torch.int32 else 3.0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for n in names:
+            assert torch.equal(getattr(ring, n), first[n]), (rep, n)
+    say("  repeats and graph replays bitwise equal")
+
+
+def test_ring_full_size_half_capacity():
+    """The training workload with a ring holding half of the routes (the
+    comparison the paper makes): sampled rows and columns against the
+    oracle, everything against the one-pass path."""
+    w = WORKLOADS["large_shared_train"]
+    R = w.T * w.k
+    full, ring, inp = run_pair(w, R // 2, seed=0)
+    Zo, idx_g = check_route_and_plan(ring, inp, w)
+    w_orc = O.gate_weights(Zo, idx_g)
+    W64 = weights_dict(inp, as_f64=True)
+    rng = np.random.default_rng(3)
+    toks = np.unique(np.concatenate([[0, w.T - 1], rng.choice(w.T, 10, replace=False)]))
+    assert_close("Y[sampled tokens]", to_np(ring.Y)[toks],
+                 O.moe_forward_dense(inp["X"], W64, idx_g, w_orc, toks))
+    dX_ref, dZ_ref, _ = O.token_backward(inp["X"], inp["W_r"], W64, idx_g, w_orc, inp["dY"], toks)
+    assert_close("dX[sampled tokens]", to_np(ring.dX)[toks], dX_ref)
+    assert_close("dZ[sampled tokens]", to_np(ring.dZ)[toks], dZ_ref)
+    cols = np.array([0, 777, w.f - 1])
+    # expert 0 sits in the first window, the last expert in the second: one
+    # is served from the ring the forward left, the other by the replay
+    for e in (0, w.E - 1):
+        a, b, c = O.expert_weight_grad_columns(inp["X"], W64, idx_g, w_orc, inp["dY"], e, cols)
+        assert_close(f"dW_gate[{e}][:, cols]", to_np(ring.dW_gate[e])[:, cols], a)
+        assert_close(f"dW_up[{e}][:, cols]", to_np(ring.dW_up[e])[:, cols], b)
+        assert_close(f"dW_down[{e}][cols, :]", to_np(ring.dW_down[e])[cols, :], c)
+    compare_to_one_pass(full, ring, w, R // 2)
+    say(f"  workspace: one-pass {full.ws.numel() / 2**30:.2f} GiB, "
+        f"ring {ring.ws.numel() / 2**30:.2f} GiB")
