@@ -295,6 +295,9 @@ def main():
     ap.add_argument("--no-mx", action="store_true", help="skip timing the MXFP8 forward")
     ap.add_argument("--no-ring", action="store_true",
                     help="skip the bounded-memory (half-capacity ring) comparison")
+    ap.add_argument("--ring-only", type=int, default=0, metavar="ROWS",
+                    help="time only steps in bounded-memory execution with a ring of ROWS rows "
+                         "(for kernel traces of that mode); prints its own JSON line")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (the reference "
                          "kernel for scaling HBM byte counters)")
@@ -315,9 +318,28 @@ def main():
     t_in = time.perf_counter()
     inputs = make_inputs(w, seed=0)
     log(f"[bench] inputs drawn in {time.perf_counter() - t_in:.1f} s")
-    L = DeviceLayer(w, inputs)
     stream = torch.cuda.current_stream().cuda_stream
     H = HipEvents()
+    if args.ring_only:
+        L = DeviceLayer(w, inputs, ring_rows=args.ring_only)
+        for _ in range(args.warmup):
+            L.step()
+        torch.cuda.synchronize()
+        a, b = H.create(), H.create()
+        H.record(a, stream)
+        for _ in range(args.steps):
+            L.step()
+        H.record(b, stream)
+        H.sync(b)
+        ms = H.ms(a, b) / args.steps
+        step_flops = w.fwd_flops() + (w.bwd_flops() if w.backward else 0.0)
+        print(json.dumps({"mode": "bounded_memory", "workload": w.name,
+                          "ring_rows": args.ring_only, "steps": args.steps,
+                          "ms_per_step": round(ms, 4),
+                          "tflops": round(step_flops / (ms * 1e-3) / 1e12, 2),
+                          "workspace_gib": round(L.ws.numel() / 2 ** 30, 3)}), flush=True)
+        return
+    L = DeviceLayer(w, inputs)
 
     if args.calibrate_copy_mib:
         n = args.calibrate_copy_mib * (1 << 20) // 4

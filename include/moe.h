@@ -296,12 +296,14 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
  *                     per-token accumulator seeded with the shared-expert
  *                     output; the last window rounds it into Y.
  *   moe_backward_ring runs the windows in ascending order: window 0 uses the
- *                     activations the forward left in the ring; every later
- *                     window first recomputes its gate/up pre-activations
+ *                     activations the forward left in the ring; the gate/up
+ *                     pre-activations of every later window are recomputed
  *                     (A, B only: the down projection and H are not
- *                     replayed).  Weight gradients of a window are added to
- *                     the previous windows' in fp32; the routed dX terms are
- *                     summed per token across windows as in the forward.
+ *                     replayed), in the same launch as the previous window's
+ *                     weight gradients.  Weight gradients of a window are
+ *                     added to the previous windows' in fp32; the routed dX
+ *                     terms are summed per token across windows as in the
+ *                     forward.
  *
  * Results are deterministic.  With one window (ring_rows >= T*k) they are
  * bitwise those of moe_forward / moe_backward; with several, Y, dX and the

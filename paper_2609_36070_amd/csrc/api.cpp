@@ -56,7 +56,7 @@ Layout make_layout(const moe_shape &s, long ring_rows = -1) {
     L.prefix_total = o;
     if (ring_rows >= 0) {
         L.acc = take(T * d * 4);
-        L.coff = take((E + 1) * 4);
+        L.coff = take(2 * (E + 1) * 4);
     }
     L.A = take(Ra * f * 2);
     L.B = take(Ra * f * 2);
@@ -249,8 +249,8 @@ struct Window {
 
 // Routed up/gate + SwiGLU over a window: H (optional) and, for the backward,
 // the pre-activations A and B.
-hipError_t routed_up(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *X,
-                     const moe_weights *w, const Window &win, bool keep_h, bool save, hipStream_t s) {
+GemmArgs up_args(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *X,
+                 const moe_weights *w, const Window &win, bool keep_h, bool save) {
     const int T = (int)sh.T, d = (int)sh.d, f = (int)sh.f;
     GemmArgs g;
     g.zeros = at<uint16_t>(ws, L.zeros);
@@ -260,7 +260,12 @@ hipError_t routed_up(const moe_shape &sh, const Layout &L, void *ws, const moe_b
     if (keep_h) g.C = win.rows<uint16_t>(ws, L.H, f);
     g.ldc = f;
     if (save) { g.C2 = win.rows<uint16_t>(ws, L.A, f); g.C3 = win.rows<uint16_t>(ws, L.B, f); }
-    return launch_gemm_fwd_up(g, win.count(), (int)sh.E, s);
+    return g;
+}
+
+hipError_t routed_up(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *X,
+                     const moe_weights *w, const Window &win, bool keep_h, bool save, hipStream_t s) {
+    return launch_gemm_fwd_up(up_args(sh, L, ws, X, w, win, keep_h, save), win.count(), (int)sh.E, s);
 }
 
 hipError_t routed_down(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w,
@@ -306,36 +311,30 @@ hipError_t routed_dx(const moe_shape &sh, const Layout &L, void *ws, const moe_w
     return launch_gemm_bwd_dx(g, win.count(), (int)sh.E, s);
 }
 
-// dW_gate[e] = Xperm_e^T dA_e, dW_up[e] = Xperm_e^T dB_e over the window's rows
-// of each expert (added to the previous windows' sums when accumulate).
-hipError_t routed_wgrad_up(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *X,
-                           const moe_grads *gr, const Window &win, bool accumulate, hipStream_t s) {
+// Weight gradients over the window's rows of each expert (added to the
+// previous windows' sums when accumulate):
+//   which 0: dW_gate[e] = Xperm_e^T dA_e   1: dW_up[e] = Xperm_e^T dB_e
+//   which 2: dW_down[e] = (w H_e)^T dYperm_e
+GemmArgs wgrad_args(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *X,
+                    const moe_bf16 *dY, const moe_grads *gr, const Window &win, bool accumulate,
+                    int which) {
     const int T = (int)sh.T, d = (int)sh.d, f = (int)sh.f;
     GemmArgs g;
     g.zeros = at<uint16_t>(ws, L.zeros);
-    g.A = X; g.lda = d; g.a_rows = at<int>(ws, L.rowidx); g.a_nrows = T > 0 ? T : 1;
-    g.B = win.rows<uint16_t>(ws, L.dA, f); g.ldb = f; g.b_nrows = win.span();
-    g.M = d; g.N = f; g.offsets = win.offs; g.E = (int)sh.E;
-    g.Cf = gr->dW_gate; g.c_estride = (long)d * f; g.ldc = f;
+    g.offsets = win.offs; g.E = (int)sh.E;
     g.accumulate = accumulate ? 1 : 0;
-    hipError_t e = launch_gemm_wgrad(g, (int)sh.E, s);
-    if (e != hipSuccess) return e;
-    g.B = win.rows<uint16_t>(ws, L.dB, f); g.Cf = gr->dW_up;
-    return launch_gemm_wgrad(g, (int)sh.E, s);
-}
-
-// dW_down[e] = (w H_e)^T dYperm_e over the window.
-hipError_t routed_wgrad_down(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *dY,
-                             const moe_grads *gr, const Window &win, bool accumulate, hipStream_t s) {
-    const int T = (int)sh.T, d = (int)sh.d, f = (int)sh.f;
-    GemmArgs g;
-    g.zeros = at<uint16_t>(ws, L.zeros);
-    g.A = win.rows<uint16_t>(ws, L.Hw, f); g.lda = f; g.a_nrows = win.span();
-    g.B = dY; g.ldb = d; g.b_rows = at<int>(ws, L.rowidx); g.b_nrows = T > 0 ? T : 1;
-    g.M = f; g.N = d; g.offsets = win.offs; g.E = (int)sh.E;
-    g.Cf = gr->dW_down; g.c_estride = (long)f * d; g.ldc = d;
-    g.accumulate = accumulate ? 1 : 0;
-    return launch_gemm_wgrad(g, (int)sh.E, s);
+    if (which < 2) {
+        g.A = X; g.lda = d; g.a_rows = at<int>(ws, L.rowidx); g.a_nrows = T > 0 ? T : 1;
+        g.B = win.rows<uint16_t>(ws, which == 0 ? L.dA : L.dB, f); g.ldb = f; g.b_nrows = win.span();
+        g.M = d; g.N = f;
+        g.Cf = which == 0 ? gr->dW_gate : gr->dW_up; g.c_estride = (long)d * f; g.ldc = f;
+    } else {
+        g.A = win.rows<uint16_t>(ws, L.Hw, f); g.lda = f; g.a_nrows = win.span();
+        g.B = dY; g.ldb = d; g.b_rows = at<int>(ws, L.rowidx); g.b_nrows = T > 0 ? T : 1;
+        g.M = f; g.N = d;
+        g.Cf = gr->dW_down; g.c_estride = (long)f * d; g.ldc = d;
+    }
+    return g;
 }
 
 // Shared-expert backward: dAs/dBs, dXsh and its three weight gradients.
@@ -590,9 +589,10 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
     MOE_TRY(mk.mark(3));
     MOE_TRY(routed_dx(*shape, L, ws, weights, all, s));
     MOE_TRY(mk.mark(4));
-    MOE_TRY(routed_wgrad_up(*shape, L, ws, X, grads, all, false, s));
+    MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, 0), E, s));
+    MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, 1), E, s));
     MOE_TRY(mk.mark(5));
-    MOE_TRY(routed_wgrad_down(*shape, L, ws, dY, grads, all, false, s));
+    MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, 2), E, s));
     MOE_TRY(mk.mark(6));
     const bool shared = shape->f_shared > 0;
     if (shared) {
@@ -683,21 +683,40 @@ moe_status moe_backward_ring(const moe_shape *shape, const moe_bf16 *dY, const m
     MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, at<int>(ws, L.rowidx),
                         at<float>(ws, L.wperm), at<uint16_t>(ws, L.zeros), s));
     if (shared) MOE_TRY(shared_backward(*shape, L, ws, dY, X, weights, grads, none, s));
-    for (int m = 0; m < nwin; ++m) {
+    // windows alternate between two clipped-offset arrays, so the replay of
+    // window m + 1 can share a launch with the weight gradients of window m
+    auto window = [&](int m) {
         const int w0 = (int)(m * ring_rows);
         const int w1 = (int)(R < w0 + ring_rows ? R : w0 + ring_rows);
-        const Window win{coff, w0, w1};
-        MOE_TRY(launch_clip_offsets(plan->offsets, E, w0, w1, coff, s));
-        // the forward left window 0 in the ring; later windows recompute only
-        // the pre-activations the backward reads
-        if (m > 0) MOE_TRY(routed_up(*shape, L, ws, X, weights, win, false, true, s));
+        return Window{coff + (m & 1) * (E + 1), w0, w1};
+    };
+    auto clip = [&](int m) {
+        const Window w = window(m);
+        return launch_clip_offsets(plan->offsets, E, w.w0, w.w1, coff + (m & 1) * (E + 1), s);
+    };
+    MOE_TRY(clip(0));
+    for (int m = 0; m < nwin; ++m) {
+        const Window win = window(m);
+        // window 0 uses the activations the forward left in the ring; the
+        // pre-activations of every later window were recomputed in the
+        // previous window's weight-gradient launch
         MOE_TRY(routed_dgrad(*shape, L, ws, dY, weights, win, s));
         MOE_TRY(routed_dx(*shape, L, ws, weights, win, s));
-        MOE_TRY(launch_window_accum(at<uint16_t>(ws, L.dXperm), w0, w1, nullptr,
+        MOE_TRY(launch_window_accum(at<uint16_t>(ws, L.dXperm), win.w0, win.w1, nullptr,
                                     plan->route_pos, T, d, k, acc, m == 0,
                                     shared ? at<uint16_t>(ws, L.dXsh) : nullptr, nullptr, s));
-        MOE_TRY(routed_wgrad_up(*shape, L, ws, X, grads, win, m > 0, s));
-        MOE_TRY(routed_wgrad_down(*shape, L, ws, dY, grads, win, m > 0, s));
+        GemmArgs wg[3];
+        for (int i = 0; i < 3; ++i) wg[i] = wgrad_args(*shape, L, ws, X, dY, grads, win, m > 0, i);
+        if (m + 1 < nwin) {
+            // recompute only A and B of the next window (no H, no down
+            // projection): its dgrad reads nothing else
+            const Window nxt = window(m + 1);
+            MOE_TRY(clip(m + 1));
+            const GemmArgs up = up_args(*shape, L, ws, X, weights, nxt, false, true);
+            MOE_TRY(launch_gemm_wgrad_batch(wg, 3, E, &up, nxt.count(), s));
+        } else {
+            MOE_TRY(launch_gemm_wgrad_batch(wg, 3, E, nullptr, 0, s));
+        }
     }
     MOE_TRY(launch_softmax_bwd(at<float>(ws, L.dgpart), L.dg_parts, plan->route_pos, topk_w, topk_idx,
                                T, k, E, at<float>(ws, L.dg), dZ, s));

@@ -157,38 +157,49 @@ DEV bool map_tile(int b, int nblocks, int tiles_m, int ntn, int &mt, int &nt) {
 // Weight-gradient raster.  A tile's cost is its expert's route count, so
 // XCDs that each ran whole experts would wait for the heaviest one (or idle
 // outright when a window of the bounded-memory backward holds only some of
-// the experts).  Instead every expert's ntm x ntn tiles are cut into 8 equal
-// runs, one per XCD, and each XCD walks its run of expert 0, then of expert
-// 1, and so on: all XCDs carry the same work, and the blocks an XCD runs at
-// once cover a GM x (run / GM) patch of one expert, sharing its A and B
-// panels in that XCD's L2.  Grid: 8 * groups * ceil(ntm * ntn / 8) blocks.
+// the experts).  Instead each expert's ntm x ntn tiles are cut into blocks of
+// 4 x 4 tiles, the blocks of all experts are numbered expert by expert, and
+// block h goes to XCD h % 8: every XCD gets an equal share of each expert
+// (up to one block), and the 32 tiles an XCD runs at once are two such
+// blocks, each sharing 4 A and 4 B panels in that XCD's L2.
+// Grid: 8 * 16 * ceil(groups * blocks_per_expert / 8) workgroups.
+constexpr int WG_BM = 4, WG_BN = 4;
+__host__ __device__ __forceinline__ int wgrad_blocks_per_expert(int ntm, int ntn) {
+    return ((ntm + WG_BM - 1) / WG_BM) * ((ntn + WG_BN - 1) / WG_BN);
+}
 DEV bool map_tile_wgrad(int b, int groups, int ntm, int ntn, int &cm, int &nt) {
-    constexpr int NX = 8, GM = 4;
-    const int per_e = ntm * ntn;
-    const int q = (per_e + NX - 1) / NX;
-    const int j = b / NX;
-    const int e = j / q, t = (b % NX) * q + j % q;
-    if (e >= groups || t >= per_e) return false;
-    const int group = t / (GM * ntn);
-    const int first = group * GM;
-    const int gm = min(GM, ntm - first);
-    const int within = t - group * GM * ntn;
-    cm = e * ntm + first + within % gm;
-    nt = within / gm;
+    constexpr int NX = 8, PER = WG_BM * WG_BN;
+    const int nbm = (ntm + WG_BM - 1) / WG_BM;
+    const int nb = wgrad_blocks_per_expert(ntm, ntn);
+    const int j = b / NX;                        // position in this XCD's sequence
+    const int h = (j / PER) * NX + b % NX;       // block
+    const int t = j % PER;                       // tile within the block, m fastest
+    const int e = h / nb, lb = h % nb;
+    if (e >= groups) return false;
+    const int mt = (lb % nbm) * WG_BM + t % WG_BM;
+    nt = (lb / nbm) * WG_BN + t / WG_BM;
+    if (mt >= ntm || nt >= ntn) return false;
+    cm = e * ntm + mt;
     return true;
 }
 
+// Two LDS stages, each operand its own object: the compiler then knows the
+// tile being read never aliases the tile being filled and does not stall the
+// reads on the in-flight direct loads.  They live at file scope so that one
+// kernel can run tiles of several products (each product's tile code uses
+// the same arrays).
+__shared__ __attribute__((aligned(16))) uint16_t lds_a0[TILE_ELEMS];
+__shared__ __attribute__((aligned(16))) uint16_t lds_b0[TILE_ELEMS];
+__shared__ __attribute__((aligned(16))) uint16_t lds_a1[TILE_ELEMS];
+__shared__ __attribute__((aligned(16))) uint16_t lds_b1[TILE_ELEMS];
+__shared__ int s_info[2];
+
+// One output tile of product MODE: workgroup vb of a grid of nvb (a multiple
+// of 8, so vb % 8 is the XCD the tile runs on).
 template <int MODE, bool GROUPED>
-__global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int *__restrict__ a_rows, const int *__restrict__ b_rows) {
+DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int *__restrict__ b_rows,
+                   int vb, int nvb) {
     using Tr = Traits<MODE>;
-    // Two LDS stages, each operand its own object: the compiler then knows the
-    // tile being read never aliases the tile being filled and does not stall
-    // the reads on the in-flight direct loads.
-    __shared__ __attribute__((aligned(16))) uint16_t lds_a0[TILE_ELEMS];
-    __shared__ __attribute__((aligned(16))) uint16_t lds_b0[TILE_ELEMS];
-    __shared__ __attribute__((aligned(16))) uint16_t lds_a1[TILE_ELEMS];
-    __shared__ __attribute__((aligned(16))) uint16_t lds_b1[TILE_ELEMS];
-    __shared__ int s_info[2];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -201,7 +212,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
     if constexpr (Tr::GROUPED_ROWS) {
         const int ntn = (MODE == FWD_UP) ? g.N / (BN / 2) : g.N / BN;
         int mt = 0;
-        if (!map_tile(blockIdx.x, gridDim.x, g.tiles_m, ntn, mt, ntile)) return;
+        if (!map_tile(vb, nvb, g.tiles_m, ntn, mt, ntile)) return;
         n0 = ntile * ((MODE == FWD_UP) ? BN / 2 : BN);
         if constexpr (GROUPED) {
             if (tid == 0) s_info[0] = -1;
@@ -240,7 +251,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
     } else {
         const int ntn = g.N / BN, ntm = g.M / BM;
         int cm = 0;   // (expert, m-tile) pair
-        if (!map_tile_wgrad(blockIdx.x, g.tiles_m / ntm, ntm, ntn, cm, ntile)) return;
+        if (!map_tile_wgrad(vb, g.tiles_m / ntm, ntm, ntn, cm, ntile)) return;
         m0 = (cm % ntm) * BM;
         e = cm / ntm;
         n0 = ntile * BN;
@@ -251,6 +262,8 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
             kbeg = 0;
             klen = g.K;
         }
+        // an expert with no rows adds nothing to a running sum
+        if (klen == 0 && g.accumulate) return;
     }
 
     // ---------------- direct-load set-up ----------------
@@ -563,20 +576,69 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int
             }
         }
     } else {  // WGRAD
-        float *out = g.Cf + (long)e * g.c_estride;
+        // accumulator q of MFMA tile (i, j) is row 8 (q >> 2) + 4 lhalf + (q & 3)
+        // of the 32-row block, column lrow
+        float *out = g.Cf + (long)e * g.c_estride + (long)(m0 + wm * WM + 4 * lhalf) * g.ldc
+                   + n0 + wn * WN + lrow;
+        const long ld = g.ldc;
+        if (g.accumulate) {
+            // read all 16 old values of an MFMA tile before adding, so the
+            // loads overlap instead of each waiting for its own round trip
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+            for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int col = n0 + wn * WN + 32 * j + lrow;
+                for (int j = 0; j < TN; ++j) {
+                    float *o = out + (long)(32 * i) * ld + 32 * j;
+                    float old[16];
 #pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    const int m = m0 + wm * WM + 32 * i + 8 * (q >> 2) + 4 * lhalf + (q & 3);
-                    float *o = out + (long)m * g.ldc + col;
-                    *o = g.accumulate ? *o + acc[i][j][q] : acc[i][j][q];
+                    for (int q = 0; q < 16; ++q) old[q] = o[(8 * (q >> 2) + (q & 3)) * ld];
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) o[(8 * (q >> 2) + (q & 3)) * ld] = old[q] + acc[i][j][q];
                 }
-            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    float *o = out + (long)(32 * i) * ld + 32 * j;
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) o[(8 * (q >> 2) + (q & 3)) * ld] = acc[i][j][q];
+                }
+        }
     }
+}
+
+template <int MODE, bool GROUPED>
+__global__ __launch_bounds__(NTHREADS, 1) void gemm_kernel(GemmArgs g, const int *__restrict__ a_rows,
+                                                          const int *__restrict__ b_rows) {
+    gemm_tile<MODE, GROUPED>(g, a_rows, b_rows, blockIdx.x, gridDim.x);
+}
+
+// Several grouped weight-gradient products, optionally followed by one
+// grouped up/gate product, in one launch.  Product i owns workgroups
+// [start[i], start[i+1]) (each start a multiple of 8, so its XCD raster is
+// the one a launch of its own would have).  Workgroups are dispatched in
+// order: the long weight-gradient tiles go first and the short up/gate tiles
+// fill the tail.
+constexpr int MAX_BATCH = 4;
+struct GemmBatch {
+    GemmArgs g[MAX_BATCH];
+    int start[MAX_BATCH + 1];
+    int n;          // products
+    int up_last;    // the last product is FWD_UP
+};
+
+__global__ __launch_bounds__(NTHREADS, 1) void gemm_batch_kernel(GemmBatch bt) {
+    const int b = blockIdx.x;
+    int i = 0;
+#pragma unroll
+    for (int j = 1; j < MAX_BATCH; ++j)
+        if (j < bt.n && b >= bt.start[j]) i = j;
+    const int vb = b - bt.start[i], nvb = bt.start[i + 1] - bt.start[i];
+    if (bt.up_last && i == bt.n - 1)
+        gemm_tile<FWD_UP, true>(bt.g[i], bt.g[i].a_rows, bt.g[i].b_rows, vb, nvb);
+    else
+        gemm_tile<WGRAD, true>(bt.g[i], bt.g[i].a_rows, bt.g[i].b_rows, vb, nvb);
 }
 
 template <int MODE>
@@ -617,6 +679,46 @@ hipError_t launch_gemm_bwd_dx(const GemmArgs &g, long rows, int groups, hipStrea
     return launch_mode<BWD_DX>(g, mtiles(g, rows, groups), g.N / BN, st);
 }
 hipError_t launch_gemm_wgrad(const GemmArgs &g, int groups, hipStream_t st) {
-    const long per_e = (long)(g.M / BM) * (g.N / BN);
-    return launch_mode<WGRAD>(g, groups * (g.M / BM), g.N / BN, st, 8L * groups * ((per_e + 7) / 8));
+    const long nblk = (long)groups * wgrad_blocks_per_expert(g.M / BM, g.N / BN);
+    return launch_mode<WGRAD>(g, groups * (g.M / BM), g.N / BN, st,
+                              8L * WG_BM * WG_BN * ((nblk + 7) / 8));
+}
+
+hipError_t launch_gemm_wgrad_batch(const GemmArgs *wg, int nw, int groups, const GemmArgs *up,
+                                   long up_rows, hipStream_t st) {
+    GemmBatch bt{};
+    if (nw < 0 || nw + (up ? 1 : 0) > MAX_BATCH) return hipErrorInvalidValue;
+    long at = 0;
+    bt.n = 0;
+    for (int i = 0; i < nw; ++i) {
+        GemmArgs g = wg[i];
+        if (!g.offsets) return hipErrorInvalidValue;
+        const int ntm = g.M / BM, ntn = g.N / BN;
+        g.tiles_m = groups * ntm;
+        const long nblk = (long)groups * wgrad_blocks_per_expert(ntm, ntn);
+        const long blocks = 8L * WG_BM * WG_BN * ((nblk + 7) / 8);
+        if ((long)g.tiles_m * ntn <= 0) continue;
+        bt.g[bt.n] = g;
+        bt.start[bt.n] = (int)at;
+        at += blocks;
+        ++bt.n;
+    }
+    if (up) {
+        GemmArgs g = *up;
+        if (!g.offsets) return hipErrorInvalidValue;
+        const int ntn = g.N / (BN / 2);
+        g.tiles_m = mtiles(g, up_rows, groups);
+        const long tiles = (long)g.tiles_m * ntn;
+        if (tiles > 0) {
+            bt.g[bt.n] = g;
+            bt.start[bt.n] = (int)at;
+            at += (tiles + 7) / 8 * 8;
+            ++bt.n;
+            bt.up_last = 1;
+        }
+    }
+    if (bt.n == 0) return hipSuccess;
+    bt.start[bt.n] = (int)at;
+    gemm_batch_kernel<<<dim3((unsigned)at), dim3(NTHREADS), 0, st>>>(bt);
+    return hipGetLastError();
 }

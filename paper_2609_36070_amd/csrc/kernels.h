@@ -50,6 +50,10 @@ hipError_t launch_gemm_fwd_down(const GemmArgs &g, long rows, int groups, hipStr
 hipError_t launch_gemm_bwd_dgrad(const GemmArgs &g, long rows, int groups, hipStream_t st);
 hipError_t launch_gemm_bwd_dx(const GemmArgs &g, long rows, int groups, hipStream_t st);
 hipError_t launch_gemm_wgrad(const GemmArgs &g, int groups, hipStream_t st);
+// Up to 4 grouped weight-gradient products (same groups), optionally with one
+// grouped up/gate product over `up_rows` plan rows, in one launch.
+hipError_t launch_gemm_wgrad_batch(const GemmArgs *wg, int nw, int groups, const GemmArgs *up,
+                                   long up_rows, hipStream_t st);
 
 int route_epad(int E);
 hipError_t launch_route(const uint16_t *X, const uint16_t *W_r, const float *bias, float *logits,

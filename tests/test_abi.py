@@ -141,8 +141,8 @@ def test_ring_workspace_sizes(name):
         sizes = [B.moe_ring_workspace_bytes(sh, c, bwd) for c in (256, max(R // 2, 1), R, 4 * R)]
         assert all(0 < b for b in sizes)
         assert sizes[0] <= sizes[1] <= sizes[2] == sizes[3]
-        # the ring adds an fp32 per-token accumulator and the clipped offsets
-        extra = w.T * w.d * 4 + 4 * (w.E + 1) + 2 * 256
+        # the ring adds an fp32 per-token accumulator and two clipped-offset arrays
+        extra = w.T * w.d * 4 + 8 * (w.E + 1) + 2 * 256
         assert sizes[2] <= full + extra
         per_row = (3 * w.f + w.d + (3 * w.f + w.d if bwd else 0)) * 2
         assert sizes[2] - sizes[1] >= (R - R // 2) * per_row - 16 * 256
