@@ -196,6 +196,40 @@ def mx_forward_timing(H, stream, inputs, steps, warmup):
     return out
 
 
+def fused_forward_timing(H, stream, L, steps):
+    """route + plan + forward with the separate launches against the same with
+    the fused persistent forward, on the benchmark layer (A and B saved when
+    it trains), in two alternating blocks of `steps` steps."""
+    import torch
+
+    def block(fused):
+        a, b = H.create(), H.create()
+        H.record(a, stream)
+        for _ in range(steps):
+            L.route()
+            L.plan()
+            if fused:
+                L.forward_fused()
+            else:
+                L.forward()
+        H.record(b, stream)
+        H.sync(b)
+        ms = H.ms(a, b) / steps
+        H.destroy(a)
+        H.destroy(b)
+        return ms
+
+    block(True)                      # warm-up of the fused launch
+    torch.cuda.synchronize()
+    res = {"separate": 0.0, "fused": 0.0}
+    for _ in range(2):
+        res["separate"] += block(False) / 2
+        res["fused"] += block(True) / 2
+    err = L.error_word()
+    return {"separate_ms": round(res["separate"], 4), "fused_ms": round(res["fused"], 4),
+            "speedup": round(res["separate"] / res["fused"], 4), "error_word": err}
+
+
 def ring_timing(H, stream, w, inputs, L_full, steps, warmup):
     """Bounded-memory execution against the one-pass path on the benchmark
     workload: a ring holding half of the routed rows (the comparison the
@@ -295,6 +329,8 @@ def main():
     ap.add_argument("--no-mx", action="store_true", help="skip timing the MXFP8 forward")
     ap.add_argument("--no-ring", action="store_true",
                     help="skip the bounded-memory (half-capacity ring) comparison")
+    ap.add_argument("--no-fused", action="store_true",
+                    help="skip timing the fused persistent forward")
     ap.add_argument("--ring-only", type=int, default=0, metavar="ROWS",
                     help="time only steps in bounded-memory execution with a ring of ROWS rows "
                          "(for kernel traces of that mode); prints its own JSON line")
@@ -452,6 +488,12 @@ def main():
         for name, v in mxf["stages"].items():
             log(f"   mx.{name:25s} {v['ms']:9.4f} ms  {v.get('tflops', '')}")
 
+    fused = None
+    if not args.no_fused:
+        fused = fused_forward_timing(H, stream, L, max(5, args.steps))
+        log(f"[bench] forward (route+plan+forward): separate launches {fused['separate_ms']:.3f} ms, "
+            f"fused persistent {fused['fused_ms']:.3f} ms ({fused['speedup']}x)")
+
     ring = None
     if not args.no_ring:
         ring = ring_timing(H, stream, w, inputs, L, max(3, args.steps // 2), 2)
@@ -488,6 +530,7 @@ def main():
         "stages": stage_report,
         "schedule": sched,
         "mxfp8_forward": mxf,
+        "fused_forward": fused,
         "bounded_memory": ring,
     }
     print(json.dumps(out), flush=True)

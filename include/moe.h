@@ -99,8 +99,10 @@ typedef struct {
 
 /* Named regions of the workspace, for inspection after a synchronisation. */
 typedef enum {
-    MOE_WS_ERROR = 0,   /* int32[1]: nonzero after moe_plan saw an expert id
-                           outside [0, E) (such routes are left unplaced)   */
+    MOE_WS_ERROR = 0,   /* int32[1], reset by moe_plan.  Bit 0: moe_plan
+                           saw an expert id outside [0, E) (such routes are
+                           left unplaced).  Bit 1: a dependency wait of
+                           moe_forward_fused gave up (results invalid). */
     MOE_WS_A = 1,       /* bf16 [T*k, f]  x W_gate[e] in plan order         */
     MOE_WS_B = 2,       /* bf16 [T*k, f]  x W_up[e]                         */
     MOE_WS_H = 3,       /* bf16 [T*k, f]  silu(A) * B                       */
@@ -268,6 +270,25 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
                        const moe_plan_bufs *plan, moe_bf16 *Y, int save_for_backward,
                        void *ws, size_t ws_bytes, moe_stream stream,
                        const moe_stage_events *events /* NULL = no timing */);
+
+/* Forward of the layer as one persistent launch (§3.2: all of the layer's
+ * computation fused into one kernel; §3.4 "Shared Expert": the shared
+ * expert's tiles are scheduled first).  One workgroup per compute unit takes
+ * work items from per-XCD queues in a fixed order: shared up/gate tiles,
+ * routed up/gate tiles, shared down tiles, routed down tiles, then the
+ * combine of blocks of 16 tokens.  A down tile starts when every up/gate tile
+ * of its rows is done; a token block's combine starts when the down tiles
+ * holding all of its routes are done, so the combine overlaps the last down
+ * tiles instead of following them.
+ * Same arguments, workspace and results as moe_forward, bitwise (each tile
+ * runs the same code, the combine adds in the same order); A and B are kept
+ * when save_for_backward = 1, so moe_backward can follow.  Every wait is
+ * bounded: if one gives up, bit 1 of the MOE_WS_ERROR word is set and the
+ * launch still ends (the outputs are then invalid). */
+moe_status moe_forward_fused(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
+                             const int32_t *topk_idx, const float *topk_w,
+                             const moe_plan_bufs *plan, moe_bf16 *Y, int save_for_backward,
+                             void *ws, size_t ws_bytes, moe_stream stream);
 
 /* Backward of the layer for upstream gradient dY [T, d] bf16, with the
  * selection held fixed.  Needs the same ws as a preceding moe_forward with

@@ -26,7 +26,8 @@ EXPORTS = ("moe_workspace_bytes", "moe_workspace_region", "moe_route", "moe_plan
            "moe_schedule_workspace_bytes", "moe_schedule", "moe_dispatch", "moe_forward",
            "moe_backward", "moe_mx_quantize_weights", "moe_mx_workspace_bytes",
            "moe_mx_workspace_region", "moe_forward_mx", "moe_ring_workspace_bytes",
-           "moe_forward_ring", "moe_backward_ring", "moe_status_string", "moe_version")
+           "moe_forward_ring", "moe_backward_ring", "moe_forward_fused", "moe_status_string",
+           "moe_version")
 
 
 class MoeShape(ctypes.Structure):
@@ -105,6 +106,9 @@ def lib():
         L.moe_forward_mx.argtypes = [P(MoeShape), c_void_p, P(MoeWeights), P(MoeMxWeights),
                                      c_void_p, c_void_p, P(MoePlanBufs), c_void_p, c_void_p,
                                      c_size_t, c_void_p, P(MoeStageEvents)]
+        L.moe_forward_fused.argtypes = [P(MoeShape), c_void_p, P(MoeWeights), c_void_p, c_void_p,
+                                        P(MoePlanBufs), c_void_p, c_int, c_void_p, c_size_t,
+                                        c_void_p]
         L.moe_ring_workspace_bytes.argtypes = [P(MoeShape), ctypes.c_int64, c_int]
         L.moe_ring_workspace_bytes.restype = c_size_t
         L.moe_forward_ring.argtypes = [P(MoeShape), c_void_p, P(MoeWeights), c_void_p, c_void_p,
@@ -116,7 +120,7 @@ def lib():
         for fn in ("moe_route", "moe_plan", "moe_schedule", "moe_dispatch", "moe_forward",
                    "moe_backward", "moe_workspace_region", "moe_mx_quantize_weights",
                    "moe_mx_workspace_region", "moe_forward_mx", "moe_forward_ring",
-                   "moe_backward_ring"):
+                   "moe_backward_ring", "moe_forward_fused"):
             getattr(L, fn).restype = c_int
         L.moe_status_string.argtypes = [c_int]
         L.moe_status_string.restype = ctypes.c_char_p
@@ -302,3 +306,12 @@ def moe_backward_ring(shape, dY, X, W_r, weights: MoeWeights, topk_idx, topk_w,
                                  ctypes.byref(plan), _p(dX), ctypes.byref(grads), int(ring_rows),
                                  _p(ws), nbytes, _stream(stream))
     return _check("moe_backward_ring", st, raise_on_error)
+
+
+def moe_forward_fused(shape, X, weights: MoeWeights, topk_idx, topk_w, plan: MoePlanBufs, Y,
+                      save_for_backward, ws, ws_bytes=None, stream=None, raise_on_error=True):
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    st = lib().moe_forward_fused(ctypes.byref(shape), _p(X), ctypes.byref(weights), _p(topk_idx),
+                                 _p(topk_w), ctypes.byref(plan), _p(Y),
+                                 int(bool(save_for_backward)), _p(ws), nbytes, _stream(stream))
+    return _check("moe_forward_fused", st, raise_on_error)

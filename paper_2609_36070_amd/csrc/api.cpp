@@ -20,7 +20,7 @@ size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 // scratch, W_r^T, position tables, zero page) is the same in every layout,
 // so moe_route and moe_plan work with any of them.
 struct Layout {
-    size_t err, blockcounts, blockbase, blockflags, wrt, rowidx, wperm, zeros;
+    size_t err, blockcounts, blockbase, blockflags, wrt, rowidx, wperm, zeros, fused;
     size_t prefix_total;
     size_t acc, coff;          // ring only: fp32 per-token accumulator, window regions
     size_t A, B, H, Yexp, As, Bs, Hs, Ysh;
@@ -53,6 +53,7 @@ Layout make_layout(const moe_shape &s, long ring_rows = -1) {
     L.rowidx = take(R * 4);
     L.wperm = take(R * 4);
     L.zeros = take(ZERO_PAGE_ELEMS * 2);
+    L.fused = take((size_t)fused_counter_ints((long)T, (long)R, (int)E) * 4);
     L.prefix_total = o;
     if (ring_rows >= 0) {
         L.acc = take(T * d * 4);
@@ -208,8 +209,8 @@ struct StageMarks {
 
 // Shared expert (BF16 in both precisions): up/gate + SwiGLU into Hs, then
 // down into Ysh.
-hipError_t shared_up(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *X,
-                     const moe_weights *w, bool save, hipStream_t s) {
+GemmArgs shared_up_args(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *X,
+                        const moe_weights *w, bool save) {
     const int T = (int)sh.T, d = (int)sh.d, fs = (int)sh.f_shared;
     GemmArgs g;
     g.zeros = at<uint16_t>(ws, L.zeros);
@@ -218,11 +219,15 @@ hipError_t shared_up(const moe_shape &sh, const Layout &L, void *ws, const moe_b
     g.N = fs; g.K = d;
     g.C = at<uint16_t>(ws, L.Hs); g.ldc = fs;
     if (save) { g.C2 = at<uint16_t>(ws, L.As); g.C3 = at<uint16_t>(ws, L.Bs); }
-    return launch_gemm_fwd_up(g, T, 1, s);
+    return g;
 }
 
-hipError_t shared_down(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w,
-                       hipStream_t s) {
+hipError_t shared_up(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *X,
+                     const moe_weights *w, bool save, hipStream_t s) {
+    return launch_gemm_fwd_up(shared_up_args(sh, L, ws, X, w, save), sh.T, 1, s);
+}
+
+GemmArgs shared_down_args(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w) {
     const int T = (int)sh.T, d = (int)sh.d, fs = (int)sh.f_shared;
     GemmArgs g;
     g.zeros = at<uint16_t>(ws, L.zeros);
@@ -230,7 +235,12 @@ hipError_t shared_down(const moe_shape &sh, const Layout &L, void *ws, const moe
     g.B = w->Wd_s; g.ldb = d;
     g.N = d; g.K = fs;
     g.C = at<uint16_t>(ws, L.Ysh); g.ldc = d;
-    return launch_gemm_fwd_down(g, T, 1, s);
+    return g;
+}
+
+hipError_t shared_down(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w,
+                       hipStream_t s) {
+    return launch_gemm_fwd_down(shared_down_args(sh, L, ws, w), sh.T, 1, s);
 }
 
 // Positions [w0, w1) of the routed buffer, with the expert regions clipped
@@ -268,8 +278,8 @@ hipError_t routed_up(const moe_shape &sh, const Layout &L, void *ws, const moe_b
     return launch_gemm_fwd_up(up_args(sh, L, ws, X, w, win, keep_h, save), win.count(), (int)sh.E, s);
 }
 
-hipError_t routed_down(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w,
-                       const Window &win, hipStream_t s) {
+GemmArgs down_args(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w,
+                   const Window &win) {
     const int d = (int)sh.d, f = (int)sh.f;
     GemmArgs g;
     g.zeros = at<uint16_t>(ws, L.zeros);
@@ -277,7 +287,12 @@ hipError_t routed_down(const moe_shape &sh, const Layout &L, void *ws, const moe
     g.B = w->W_down; g.ldb = d; g.b_estride = (long)f * d;
     g.N = d; g.K = f; g.offsets = win.offs; g.E = (int)sh.E;
     g.C = win.rows<uint16_t>(ws, L.Yexp, d); g.ldc = d;
-    return launch_gemm_fwd_down(g, win.count(), (int)sh.E, s);
+    return g;
+}
+
+hipError_t routed_down(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w,
+                       const Window &win, hipStream_t s) {
+    return launch_gemm_fwd_down(down_args(sh, L, ws, w, win), win.count(), (int)sh.E, s);
 }
 
 // dh' = dY W_down^T with the SwiGLU backward and the dg partials.
@@ -560,6 +575,37 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
     MOE_TRY(launch_combine(at<uint16_t>(ws, L.Yexp), fs > 0 ? at<uint16_t>(ws, L.Ysh) : nullptr,
                            topk_w, plan->route_pos, T, d, k, Y, s));
     MOE_TRY(mk.mark(6));
+    return MOE_OK;
+}
+
+moe_status moe_forward_fused(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
+                             const int32_t *topk_idx, const float *topk_w, const moe_plan_bufs *plan,
+                             moe_bf16 *Y, int save_for_backward, void *ws, size_t ws_bytes,
+                             moe_stream stream) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if (!ptr_ok(X) || !ptr_ok(topk_idx) || !ptr_ok(topk_w) || !ptr_ok(Y)) return MOE_EINVAL;
+    if ((st = check_weights(shape, weights)) != MOE_OK) return st;
+    if ((st = check_plan(plan)) != MOE_OK) return st;
+    if ((st = check_ws(shape, ws, ws_bytes, 0)) != MOE_OK) return st;
+    const Layout L = make_layout(*shape);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int T = (int)shape->T, d = (int)shape->d, E = (int)shape->E, k = (int)shape->k;
+    const bool shared = shape->f_shared > 0;
+    const long R = (long)T * k;
+    const Window all{plan->offsets, 0, (int)R};
+    const bool save = save_for_backward != 0;
+
+    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, at<int>(ws, L.rowidx),
+                        at<float>(ws, L.wperm), at<uint16_t>(ws, L.zeros), s));
+    const GemmArgs none;
+    MOE_TRY(launch_fused_forward(shared ? shared_up_args(*shape, L, ws, X, weights, save) : none,
+                                 up_args(*shape, L, ws, X, weights, all, true, save),
+                                 shared ? shared_down_args(*shape, L, ws, weights) : none,
+                                 down_args(*shape, L, ws, weights, all), shared, T, R, E,
+                                 at<uint16_t>(ws, L.Yexp), at<uint16_t>(ws, L.Ysh), topk_w,
+                                 plan->route_pos, topk_idx, plan->offsets, d, k, Y,
+                                 at<int>(ws, L.fused), at<int>(ws, L.err), s));
     return MOE_OK;
 }
 

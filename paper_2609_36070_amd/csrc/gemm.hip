@@ -196,12 +196,56 @@ __shared__ int s_info[2];
 
 // One output tile of product MODE: workgroup vb of a grid of nvb (a multiple
 // of 8, so vb % 8 is the XCD the tile runs on).
-template <int MODE, bool GROUPED>
+// Fused forward: the longest a workgroup waits for a counter, in ticks of
+// the 100 MHz real-time clock (0.2 s; a legitimate wait lasts a few tile
+// times, well under 10 ms).  A wait that runs out sets bit 1 of the error
+// word; once that bit is set every later wait returns at once, so a launch
+// always ends soon after.
+#ifndef MOE_FUSED_WAIT_TICKS
+#define MOE_FUSED_WAIT_TICKS 20000000ull
+#endif
+
+// Poll *ctr until it reaches need (one thread).  Counters are written by
+// other workgroups of the same launch with agent-scope release adds after
+// their data; the data a waiter then reads was never read before in this
+// launch by any workgroup, so no cache level can hold a stale copy of it.
+DEV void poll_count(const int *ctr, int need, int *err) {
+    const unsigned long long t0 = wall_clock64();
+    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < need) {
+        if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 2) return;
+        if (wall_clock64() - t0 > MOE_FUSED_WAIT_TICKS) {
+            __hip_atomic_fetch_or(err, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return;
+        }
+        __builtin_amdgcn_s_sleep(2);
+    }
+}
+
+DEV void wait_count(const int *ctr, int need, int *err) {
+    if (threadIdx.x == 0) poll_count(ctr, need, err);
+    __syncthreads();
+}
+
+// Publish a finished tile: every wave waits for its own stores, then one
+// release add (which writes this XCD's L2 back) makes them visible to all XCDs.
+DEV void signal_done(int *ctr) {
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int MODE, bool GROUPED, bool PERSISTENT = false>
 DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int *__restrict__ b_rows,
                    int vb, int nvb) {
     using Tr = Traits<MODE>;
+    int slot = 0;   // m-tile slot of a row product (fused forward dependencies)
 
-    const int tid = threadIdx.x;
+    // In a persistent loop the thread index passes through an empty asm, so
+    // the compiler cannot hoist this tile's per-thread addressing out of the
+    // loop (holding it in registers across tiles spills).
+    int tid_v = threadIdx.x;
+    if constexpr (PERSISTENT) asm volatile("" : "+v"(tid_v));
+    const int tid = tid_v;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
@@ -248,6 +292,8 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
             if (row0 >= row_end) return;
         }
         klen = g.K;
+        slot = mt;
+        if (g.dep) wait_count(g.dep + mt, g.dep_need, g.err);
     } else {
         const int ntn = g.N / BN, ntm = g.M / BM;
         int cm = 0;   // (expert, m-tile) pair
@@ -322,6 +368,26 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
     const int nk = (MODE == BWD_DX) ? 2 * (g.K / BK) : (klen + BK - 1) / BK;
     const int nk_half = g.K / BK;
 
+    // Forward col tiles: this lane's source for each of its loads at K step
+    // 0, so the K loop only adds kt * BK rows (and never re-reads the weight
+    // pointers, which a persistent kernel would otherwise reload every step).
+    const long ldb = g.ldb;
+    const uint16_t *bcol[LD_PER_OP];
+    if constexpr (MODE == FWD_UP || MODE == FWD_DOWN) {
+#pragma unroll
+        for (int i = 0; i < LD_PER_OP; ++i) {
+            const int kr = 2 * (LD_PER_OP * wave + i) + (lane >> 5);
+            const int col = col_of(kr);
+            if constexpr (MODE == FWD_UP) {
+                // tile columns: 32-column groups alternate gate / up over the same f range
+                const int fcol = (int)b_col_off + (col >> 6) * 32 + (col & 31);
+                bcol[i] = (((col >> 5) & 1) ? g.B2 : g.B) + (long)e * g.b_estride + (long)kr * ldb + fcol;
+            } else {
+                bcol[i] = b_col_base + (long)kr * ldb + b_col_off + col;
+            }
+        }
+    }
+
     auto issue = [&](int kt, uint16_t *la, uint16_t *lb) {
         // WGRAD k rows come through the plan's token index: fetch every index
         // this K step needs first (scalar loads, one wait), then issue the
@@ -377,15 +443,10 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
                 const int col = col_of(kr);
                 const uint16_t *src;
                 if constexpr (MODE == WGRAD) {
-                    src = kk < klen ? b_col_base + (long)pb[i] * g.ldb + b_col_off + col
+                    src = kk < klen ? b_col_base + (long)pb[i] * ldb + b_col_off + col
                                     : g.zeros + col;
-                } else if constexpr (MODE == FWD_UP) {
-                    // tile columns: 32-column groups alternate gate / up over the same f range
-                    const int which = (col >> 5) & 1;
-                    const int fcol = (int)b_col_off + (col >> 6) * 32 + (col & 31);
-                    src = (which ? g.B2 : g.B) + (long)e * g.b_estride + (long)kk * g.ldb + fcol;
                 } else {
-                    src = b_col_base + (long)kk * g.ldb + b_col_off + col;
+                    src = bcol[i] + (long)(kt * BK) * ldb;
                 }
                 load_lds16(src, lb + lds_off[i]);
             }
@@ -606,6 +667,9 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
                 }
         }
     }
+    if constexpr (Tr::GROUPED_ROWS) {
+        if (g.sig) signal_done(g.sig + slot);
+    }
 }
 
 template <int MODE, bool GROUPED>
@@ -720,5 +784,256 @@ hipError_t launch_gemm_wgrad_batch(const GemmArgs *wg, int nw, int groups, const
     if (bt.n == 0) return hipSuccess;
     bt.start[bt.n] = (int)at;
     gemm_batch_kernel<<<dim3((unsigned)at), dim3(NTHREADS), 0, st>>>(bt);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Fused persistent forward.
+//
+// One workgroup per CU loops over a work queue until it is empty.  Work
+// items, in queue order: the shared expert's up/gate tiles (first: they
+// need nothing), the routed up/gate tiles, the shared down tiles, the
+// routed down tiles, and the combine of blocks of FUSED_TB tokens.  There is
+// one queue per XCD (workgroup index mod 8); queue x holds, for each GEMM,
+// exactly the tiles the XCD-aware raster gives XCD x in a launch of its own,
+// in the same order, so every tile keeps its L2 neighbours.  A down tile
+// waits until all up/gate tiles of its m-tile slot have been published; a
+// combine block waits for the down tiles holding its tokens' routes.  Items
+// are taken in queue order and wait only on items earlier in some queue,
+// which running workgroups hold and finish without waiting on later ones:
+// the launch cannot deadlock (and every wait is bounded besides).
+//
+// Each tile is computed by the same code as in the separate launches and
+// the combine adds in the same order, so results are bitwise those of the
+// unfused forward.
+namespace {
+
+constexpr int FUSED_TB = 16;   // tokens per combine item (k <= 16: <= 256 route checks)
+
+struct FusedFwd {
+    GemmArgs g[4];       // shared up, routed up, shared down, routed down
+    int grid[4];         // workgroups of each product's own launch (multiple of 8)
+    int base[6];         // queue item index where each phase starts (5 phases)
+    int *queue;          // [8] tickets
+    int *err;
+    const uint16_t *Yexp, *Ysh;
+    const float *topk_w;
+    const int *route_pos, *topk_idx, *offsets;
+    const int *down_done_r, *down_done_s;
+    int need_r, need_s;  // n-tiles per m-tile of the routed / shared down products
+    int T, d, k, E, R;
+    uint16_t *Y;
+};
+
+__shared__ int s_ticket;
+__shared__ int s_tilebase[257];
+
+DEV void fused_combine(const FusedFwd &fa, int blk) {
+    const int t0 = blk * FUSED_TB;
+    if (t0 >= fa.T) return;
+    const int t1 = min(fa.T, t0 + FUSED_TB);
+    const int tid = threadIdx.x;
+    // dependencies: the routed down m-tile of every route of these tokens,
+    // and the shared down m-tiles of the tokens (one thread each)
+    const int npairs = (t1 - t0) * fa.k;
+    if (tid < npairs) {
+        const long j = (long)t0 * fa.k + tid;
+        const int p = fa.route_pos[j], e = fa.topk_idx[j];
+        if (p >= 0 && p < fa.R && e >= 0 && e < fa.E)
+            poll_count(fa.down_done_r + s_tilebase[e] + (p - fa.offsets[e]) / BM, fa.need_r, fa.err);
+    } else if (fa.Ysh && tid < npairs + 2) {
+        poll_count(fa.down_done_s + (tid == npairs ? t0 : t1 - 1) / BM, fa.need_s, fa.err);
+    }
+    __syncthreads();
+    // the combine of the unfused path: fp32 from Ysh, + w * Yexp in slot
+    // order.  Work unit u = (token, 8-column chunk); each thread takes two
+    // units per pass with all of their loads in flight together (one
+    // workgroup per CU leaves few waves to hide memory latency).
+    const int nc = fa.d / 8;
+    const int units = (t1 - t0) * nc;
+    for (int u0 = tid; u0 < units; u0 += 2 * NTHREADS) {
+        int tt[2], cc[2], pos[2][16];
+        float wt[2][16];
+        u32x4_t rows[2][16], sh[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int u = min(u0 + h * NTHREADS, units - 1);
+            tt[h] = t0 + u / nc;
+            cc[h] = u % nc;
+#pragma unroll
+            for (int s = 0; s < 16; ++s) {
+                pos[h][s] = -1;
+                wt[h][s] = 0.f;
+                if (s < fa.k) {
+                    const int p = fa.route_pos[(long)tt[h] * fa.k + s];
+                    pos[h][s] = (p >= 0 && p < fa.R) ? p : -1;
+                    wt[h][s] = fa.topk_w[(long)tt[h] * fa.k + s];
+                }
+            }
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+#pragma unroll
+            for (int s = 0; s < 16; ++s)
+                if (s < fa.k) rows[h][s] = ld_u32x4(fa.Yexp + (long)max(pos[h][s], 0) * fa.d + 8 * cc[h]);
+            if (fa.Ysh) sh[h] = ld_u32x4(fa.Ysh + (long)tt[h] * fa.d + 8 * cc[h]);
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            if (h == 1 && u0 + NTHREADS >= units) break;
+            float acc[8];
+            if (fa.Ysh) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    acc[2 * q] = bf_lo(sh[h][q]);
+                    acc[2 * q + 1] = bf_hi(sh[h][q]);
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+            }
+#pragma unroll
+            for (int s = 0; s < 16; ++s) {
+                if (s < fa.k && pos[h][s] >= 0) {
+                    const u32x4_t v = rows[h][s];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        acc[2 * q] = acc[2 * q] + wt[h][s] * bf_lo(v[q]);
+                        acc[2 * q + 1] = acc[2 * q + 1] + wt[h][s] * bf_hi(v[q]);
+                    }
+                }
+            }
+            u32x4_t o;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) o[q] = pack_bf2(acc[2 * q], acc[2 * q + 1]);
+            st_u32x4(fa.Y + (long)tt[h] * fa.d + 8 * cc[h], o);
+        }
+    }
+}
+
+__global__ __launch_bounds__(NTHREADS, 1) void fused_forward_kernel(FusedFwd fa) {
+    const int tid = threadIdx.x;
+    const int q = blockIdx.x & 7;
+    // first m-tile slot of every expert (the grouped raster's prefix)
+    if (tid < 64) {
+        const int lane = tid;
+        int cum = 0;
+        for (int base = 0; base < fa.E; base += 64) {
+            const int ee = base + lane;
+            const int cnt = ee < fa.E ? fa.offsets[ee + 1] - fa.offsets[ee] : 0;
+            const int tiles = cnt > 0 ? (cnt + BM - 1) / BM : 0;
+            int x = tiles;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int y = __shfl_up(x, off, 64);
+                if (lane >= off) x += y;
+            }
+            if (ee < fa.E) s_tilebase[ee] = cum + x - tiles;
+            cum += __shfl(x, 63, 64);
+        }
+    }
+    __syncthreads();
+    // the next ticket is requested when an item starts, so its round trip
+    // overlaps the item instead of stalling the workgroup between items
+    if (tid == 0) s_ticket = __hip_atomic_fetch_add(fa.queue + q, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    int t = s_ticket;
+    for (;;) {
+        if (t >= fa.base[5]) break;
+        int next = 0;
+        if (tid == 0) next = __hip_atomic_fetch_add(fa.queue + q, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        int P = 0;
+#pragma unroll
+        for (int i = 1; i < 5; ++i)
+            if (t >= fa.base[i]) P = i;
+        const int j = t - fa.base[P];
+        const int vb = 8 * j + q;
+        if (P == 0) gemm_tile<FWD_UP, false, true>(fa.g[0], fa.g[0].a_rows, fa.g[0].b_rows, vb, fa.grid[0]);
+        else if (P == 1) gemm_tile<FWD_UP, true, true>(fa.g[1], fa.g[1].a_rows, fa.g[1].b_rows, vb, fa.grid[1]);
+        else if (P == 2) gemm_tile<FWD_DOWN, false, true>(fa.g[2], fa.g[2].a_rows, fa.g[2].b_rows, vb, fa.grid[2]);
+        else if (P == 3) gemm_tile<FWD_DOWN, true, true>(fa.g[3], fa.g[3].a_rows, fa.g[3].b_rows, vb, fa.grid[3]);
+        else fused_combine(fa, vb);
+        __syncthreads();   // LDS of this item is free for the next
+        if (tid == 0) s_ticket = next;
+        __syncthreads();
+        t = s_ticket;
+    }
+}
+
+__global__ void fill_zero_kernel(int *p, int n) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
+}
+
+int cu_count() {
+    static int n = 0;
+    if (n == 0) {
+        int dev = 0, v = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+            n = v;
+        else
+            n = 256;
+    }
+    return n;
+}
+
+}  // namespace
+
+// counters: queue[8], up_done_s[tm_s], up_done_r[tm_r], down_done_s[tm_s], down_done_r[tm_r]
+int fused_counter_ints(long T, long R, int E) {
+    const long tm_s = (T + BM - 1) / BM, tm_r = R / BM + (E > 0 ? E : 1);
+    return (int)(8 + 2 * tm_s + 2 * tm_r);
+}
+
+hipError_t launch_fused_forward(const GemmArgs &up_s, const GemmArgs &up_r, const GemmArgs &down_s,
+                                const GemmArgs &down_r, bool shared, long T, long R, int E,
+                                const uint16_t *Yexp, const uint16_t *Ysh, const float *topk_w,
+                                const int *route_pos, const int *topk_idx, const int *offsets, int d,
+                                int k, uint16_t *Y, int *counters, int *err, hipStream_t st) {
+    if (T <= 0) return hipSuccess;
+    if (k > 16 || E > 256) return hipErrorInvalidValue;
+    const long tm_s = (T + BM - 1) / BM, tm_r = R / BM + (E > 0 ? E : 1);
+    const int n = fused_counter_ints(T, R, E);
+    int *queue = counters;
+    int *up_done_s = counters + 8, *up_done_r = up_done_s + tm_s;
+    int *down_done_s = up_done_r + tm_r, *down_done_r = down_done_s + tm_s;
+    fill_zero_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st>>>(counters, n);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+
+    FusedFwd fa{};
+    fa.g[0] = up_s; fa.g[1] = up_r; fa.g[2] = down_s; fa.g[3] = down_r;
+    const int ntn_up_s = shared ? up_s.N / (BN / 2) : 0, ntn_up_r = up_r.N / (BN / 2);
+    const int ntn_dn_s = shared ? down_s.N / BN : 0, ntn_dn_r = down_r.N / BN;
+    fa.g[0].tiles_m = shared ? (int)tm_s : 0;
+    fa.g[1].tiles_m = (int)tm_r;
+    fa.g[2].tiles_m = shared ? (int)tm_s : 0;
+    fa.g[3].tiles_m = (int)tm_r;
+    const long tiles[4] = {(long)fa.g[0].tiles_m * ntn_up_s, (long)tm_r * ntn_up_r,
+                           (long)fa.g[2].tiles_m * ntn_dn_s, (long)tm_r * ntn_dn_r};
+    fa.g[0].sig = up_done_s; fa.g[1].sig = up_done_r;
+    fa.g[2].dep = up_done_s; fa.g[2].dep_need = ntn_up_s; fa.g[2].sig = down_done_s;
+    fa.g[3].dep = up_done_r; fa.g[3].dep_need = ntn_up_r; fa.g[3].sig = down_done_r;
+    for (int i = 0; i < 4; ++i) fa.g[i].err = err;
+    long at = 0;
+    for (int i = 0; i < 4; ++i) {
+        fa.grid[i] = (int)((tiles[i] + 7) / 8 * 8);
+        fa.base[i] = (int)at;
+        at += fa.grid[i] / 8;
+    }
+    const long nblk = (T + FUSED_TB - 1) / FUSED_TB;
+    fa.base[4] = (int)at;
+    at += (nblk + 7) / 8;
+    fa.base[5] = (int)at;
+    fa.queue = queue;
+    fa.err = err;
+    fa.Yexp = Yexp; fa.Ysh = shared ? Ysh : nullptr;
+    fa.topk_w = topk_w; fa.route_pos = route_pos; fa.topk_idx = topk_idx; fa.offsets = offsets;
+    fa.down_done_r = down_done_r; fa.down_done_s = down_done_s;
+    fa.need_r = ntn_dn_r; fa.need_s = ntn_dn_s;
+    fa.T = (int)T; fa.d = d; fa.k = k; fa.E = E; fa.R = (int)R;
+    fa.Y = Y;
+    const int grid = cu_count() / 8 * 8 > 0 ? cu_count() / 8 * 8 : 8;
+    fused_forward_kernel<<<dim3(grid), dim3(NTHREADS), 0, st>>>(fa);
     return hipGetLastError();
 }

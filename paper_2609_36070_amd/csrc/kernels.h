@@ -41,6 +41,12 @@ struct GemmArgs {
     int dg_ld = 0;
     int accumulate = 0;                // WGRAD: add to Cf instead of overwriting it
     int tiles_m = 0;                   // set by the launcher: m-tile slots of the raster
+    // fused forward (row products only): before loading, wait until
+    // dep[m-tile slot] >= dep_need; after storing, add 1 to sig[m-tile slot]
+    const int *dep = nullptr;
+    int dep_need = 0;
+    int *sig = nullptr;
+    int *err = nullptr;                // bit 1 set when a wait gave up
 };
 
 int gemm_tile_m();
@@ -52,6 +58,16 @@ hipError_t launch_gemm_bwd_dx(const GemmArgs &g, long rows, int groups, hipStrea
 hipError_t launch_gemm_wgrad(const GemmArgs &g, int groups, hipStream_t st);
 // Up to 4 grouped weight-gradient products (same groups), optionally with one
 // grouped up/gate product over `up_rows` plan rows, in one launch.
+// Fused persistent forward: shared up/gate, routed up/gate, shared down,
+// routed down and the combine in one launch (see gemm.hip).  `counters`
+// holds fused_counter_ints(...) ints; the launcher clears them first.  A
+// wait that gives up sets bit 1 of *err.
+int fused_counter_ints(long T, long R, int E);
+hipError_t launch_fused_forward(const GemmArgs &up_s, const GemmArgs &up_r, const GemmArgs &down_s,
+                                const GemmArgs &down_r, bool shared, long T, long R, int E,
+                                const uint16_t *Yexp, const uint16_t *Ysh, const float *topk_w,
+                                const int *route_pos, const int *topk_idx, const int *offsets, int d,
+                                int k, uint16_t *Y, int *counters, int *err, hipStream_t st);
 hipError_t launch_gemm_wgrad_batch(const GemmArgs *wg, int nw, int groups, const GemmArgs *up,
                                    long up_rows, hipStream_t st);
 

@@ -81,6 +81,12 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint16_t *__restrict
             }
         }
         for (int c = threadIdx.x; c < nc; c += 256) {
+            // every load first (slots past k or without a position read row 0
+            // and are not added), so they are in flight together
+            u32x4_t rows[16];
+#pragma unroll
+            for (int s = 0; s < 16; ++s)
+                if (s < k) rows[s] = ld_u32x4(Yexp + (long)max(pos[s], 0) * d + 8 * c);
             float acc[8];
             if (Ysh) {
                 const u32x4_t v = ld_u32x4(Ysh + (long)t * d + 8 * c);
@@ -96,7 +102,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint16_t *__restrict
 #pragma unroll
             for (int s = 0; s < 16; ++s) {
                 if (s < k && pos[s] >= 0) {
-                    const u32x4_t v = ld_u32x4(Yexp + (long)pos[s] * d + 8 * c);
+                    const u32x4_t v = rows[s];
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
                         acc[2 * q] = acc[2 * q] + wt[s] * bf_lo(v[q]);
@@ -201,10 +207,14 @@ __global__ __launch_bounds__(256) void reverse_combine_kernel(const uint16_t *__
                 for (int q = 0; q < 8; ++q) acc[q] = 0.f;
             }
             if (!dXacc) {
+                u32x4_t rows[16];   // all loads first, as in the combine
+#pragma unroll
+                for (int s = 0; s < 16; ++s)
+                    if (s < k) rows[s] = ld_u32x4(dXperm + (long)max(pos[s], 0) * d + 8 * c);
 #pragma unroll
                 for (int s = 0; s < 16; ++s) {
                     if (s < k && pos[s] >= 0) {
-                        const u32x4_t v = ld_u32x4(dXperm + (long)pos[s] * d + 8 * c);
+                        const u32x4_t v = rows[s];
 #pragma unroll
                         for (int q = 0; q < 4; ++q) {
                             acc[2 * q] = acc[2 * q] + bf_lo(v[q]);
@@ -299,10 +309,14 @@ __global__ __launch_bounds__(256) void window_accum_kernel(const uint16_t *__res
                     a[4 + q] = hi[q];
                 }
             }
+            u32x4_t rows[16];   // all loads first, as in the combine
+#pragma unroll
+            for (int s = 0; s < 16; ++s)
+                if (s < k) rows[s] = ld_u32x4(ring + (long)max(pos[s], 0) * d + 8 * c);
 #pragma unroll
             for (int s = 0; s < 16; ++s) {
                 if (s < k && pos[s] >= 0) {
-                    const u32x4_t v = ld_u32x4(ring + (long)pos[s] * d + 8 * c);
+                    const u32x4_t v = rows[s];
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
                         a[2 * q] = a[2 * q] + wt[s] * bf_lo(v[q]);

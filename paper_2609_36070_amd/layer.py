@@ -130,6 +130,14 @@ class DeviceLayer:
         B.moe_forward(self.shape, self.X, self.weights, self.topk_idx, self.topk_w,
                       self.plan_bufs, self.Y, save, self.ws, stream=stream, events=events)
 
+    def forward_fused(self, save_for_backward=None, stream=None):
+        """The forward as one persistent launch (same results as forward())."""
+        if self.ring_rows is not None:
+            raise ValueError("the fused forward has no bounded-memory variant")
+        save = self.with_backward if save_for_backward is None else save_for_backward
+        B.moe_forward_fused(self.shape, self.X, self.weights, self.topk_idx, self.topk_w,
+                            self.plan_bufs, self.Y, save, self.ws, stream=stream)
+
     def backward(self, stream=None, events=None):
         if self.ring_rows is not None:
             if events is not None:

@@ -180,6 +180,24 @@ def test_ring_validation():
     assert bwd(64, grads=B.MoeGrads(FAKE, FAKE, None, FAKE, None, None, None, None)) == B.MOE_EINVAL
 
 
+def test_fused_forward_validation():
+    L = B.lib()
+    sh = B.make_shape(64, 256, 8, 2, 256)
+    plan = B.MoePlanBufs(FAKE, FAKE, FAKE, FAKE)
+    w = B.MoeWeights(FAKE, FAKE, FAKE, None, None, None)
+    big = 1 << 40
+
+    def fwd(shape=sh, weights=w, Y=FAKE, ws_bytes=big, X=FAKE):
+        return L.moe_forward_fused(ctypes.byref(shape), X, ctypes.byref(weights), FAKE, FAKE,
+                                   ctypes.byref(plan), Y, 1, FAKE, ws_bytes, None)
+
+    assert fwd(X=None) == B.MOE_EINVAL
+    assert fwd(Y=MISALIGNED) == B.MOE_EINVAL
+    assert fwd(weights=B.MoeWeights(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)) == B.MOE_EINVAL
+    assert fwd(ws_bytes=B.moe_workspace_bytes(sh, False) - 1) == B.MOE_ENOSPACE
+    assert fwd(shape=B.make_shape(64, 192, 8, 2, 256)) == B.MOE_EUNSUPPORTED
+
+
 def test_schedule_workspace_and_validation():
     L = B.lib()
     # error word + per-(rank, chunk) flags + per-(rank, chunk, expert) counts
