@@ -135,24 +135,6 @@ DEV bf16x8_t frag_col(const uint16_t *t, int n0, int ks, int lane) {
     return bf16x8_t{v[0][0], v[0][1], v[0][2], v[0][3], v[1][0], v[1][1], v[1][2], v[1][3]};
 }
 
-// XCD-aware raster.  Workgroups are dealt to the 8 XCDs round-robin; each XCD
-// instead gets a contiguous run of the logical tile order, which walks groups
-// of GM m-tiles with the m-tile fastest.  The ~32 blocks an XCD runs at once
-// then share GM A panels and ~8 B panels in that XCD's L2.  The grid is a
-// multiple of 8; blocks past the tile count return at once.
-DEV bool map_tile(int b, int nblocks, int tiles_m, int ntn, int &mt, int &nt) {
-    constexpr int NX = 8, GM = 4;
-    const int per = nblocks / NX;
-    const int l = (b % NX) * per + b / NX;
-    if (l >= tiles_m * ntn) return false;
-    const int group = l / (GM * ntn);
-    const int first = group * GM;
-    const int gm = min(GM, tiles_m - first);
-    const int within = l - group * GM * ntn;
-    mt = first + within % gm;
-    nt = within / gm;
-    return true;
-}
 
 // Weight-gradient raster.  A tile's cost is its expert's route count, so
 // XCDs that each ran whole experts would wait for the heaviest one (or idle
@@ -256,7 +238,7 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
     if constexpr (Tr::GROUPED_ROWS) {
         const int ntn = (MODE == FWD_UP) ? g.N / (BN / 2) : g.N / BN;
         int mt = 0;
-        if (!map_tile(vb, nvb, g.tiles_m, ntn, mt, ntile)) return;
+        if (!map_tile(vb, g.tiles_m, ntn, mt, ntile)) return;
         n0 = ntile * ((MODE == FWD_UP) ? BN / 2 : BN);
         if constexpr (GROUPED) {
             if (tid == 0) s_info[0] = -1;
@@ -710,7 +692,7 @@ hipError_t launch_mode(GemmArgs g, int tiles_m, int ntn, hipStream_t st, long gr
     const long tiles = (long)tiles_m * ntn;
     if (tiles <= 0) return hipSuccess;
     g.tiles_m = tiles_m;
-    const unsigned grid = (unsigned)(grid_blocks > 0 ? grid_blocks : (tiles + 7) / 8 * 8);
+    const unsigned grid = (unsigned)(grid_blocks > 0 ? grid_blocks : raster_grid(tiles_m, ntn));
     if (g.offsets)
         gemm_kernel<MODE, true><<<dim3(grid), dim3(NTHREADS), 0, st>>>(g, g.a_rows, g.b_rows);
     else
@@ -776,7 +758,7 @@ hipError_t launch_gemm_wgrad_batch(const GemmArgs *wg, int nw, int groups, const
         if (tiles > 0) {
             bt.g[bt.n] = g;
             bt.start[bt.n] = (int)at;
-            at += (tiles + 7) / 8 * 8;
+            at += raster_grid(g.tiles_m, ntn);
             ++bt.n;
             bt.up_last = 1;
         }
@@ -1016,8 +998,9 @@ hipError_t launch_fused_forward(const GemmArgs &up_s, const GemmArgs &up_r, cons
     fa.g[3].dep = up_done_r; fa.g[3].dep_need = ntn_up_r; fa.g[3].sig = down_done_r;
     for (int i = 0; i < 4; ++i) fa.g[i].err = err;
     long at = 0;
+    const int ntns[4] = {ntn_up_s, ntn_up_r, ntn_dn_s, ntn_dn_r};
     for (int i = 0; i < 4; ++i) {
-        fa.grid[i] = (int)((tiles[i] + 7) / 8 * 8);
+        fa.grid[i] = tiles[i] > 0 ? (int)raster_grid(fa.g[i].tiles_m, ntns[i]) : 0;
         fa.base[i] = (int)at;
         at += fa.grid[i] / 8;
     }

@@ -75,22 +75,6 @@ DEV i32x8_t frag(const uint8_t *t, int r0, int ks, int lane) {
                    (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
 }
 
-// XCD-aware raster (as in the BF16 kernels): each XCD gets a contiguous run of
-// a raster that walks groups of GM m-tiles with the m-tile fastest.
-DEV bool map_tile(int b, int nblocks, int tiles_m, int ntn, int &mt, int &nt) {
-    constexpr int NX = 8, GM = 4;
-    const int per = nblocks / NX;
-    const int l = (b % NX) * per + b / NX;
-    if (l >= tiles_m * ntn) return false;
-    const int group = l / (GM * ntn);
-    const int first = group * GM;
-    const int gm = min(GM, tiles_m - first);
-    const int within = l - group * GM * ntn;
-    mt = first + within % gm;
-    nt = within / gm;
-    return true;
-}
-
 template <int MODE>
 __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, const int *__restrict__ a_rows) {
     __shared__ __attribute__((aligned(16))) uint8_t lds_a0[TILE];
@@ -109,7 +93,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
     // ---------------- tile: expert region and rows ----------------
     const int ntn = (MODE == MX_UP) ? g.N / (BN / 2) : g.N / BN;
     int mt = 0, ntile = 0;
-    if (!map_tile(blockIdx.x, gridDim.x, g.tiles_m, ntn, mt, ntile)) return;
+    if (!map_tile(blockIdx.x, g.tiles_m, ntn, mt, ntile)) return;
     const int n0 = ntile * ((MODE == MX_UP) ? BN / 2 : BN);
     if (tid == 0) s_info[0] = -1;
     __syncthreads();
@@ -386,7 +370,7 @@ hipError_t launch_mx_mode(MxGemmArgs g, int tiles_m, int ntn, hipStream_t st) {
     const long tiles = (long)tiles_m * ntn;
     if (tiles <= 0) return hipSuccess;
     g.tiles_m = tiles_m;
-    const unsigned grid = (unsigned)((tiles + 7) / 8 * 8);
+    const unsigned grid = (unsigned)raster_grid(tiles_m, ntn);
     gemm_mx_kernel<MODE><<<dim3(grid), dim3(NTHREADS), 0, st>>>(g, g.a_rows);
     return hipGetLastError();
 }
