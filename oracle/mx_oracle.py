@@ -179,3 +179,82 @@ def moe_forward_mx(X, W, idx, w):
     return dict(Y=Y, H=H, Hq=Hq, Yexp=Yexp, Ysh=Ysh, Xq=Xq, counts=counts,
                 offsets=offsets, perm=perm, route_pos=route_pos)
 
+
+
+def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True):
+    """Backward of the layer with MXFP8 routed experts (teacher-forced on idx, w).
+
+    Readings (§3.4 "MXFP8 Support" names MXFP8 training and fused activation
+    quantisation; it does not say which backward products run in MXFP8):
+
+    * the pre-activations a, b and the activation h come from the MXFP8
+      forward (X quantised along d, W_gate / W_up along d);
+    * the two products that contract over a model dimension run in MXFP8:
+      dh' = Q_d(dY) Q_d(W_down[e])^T (dY per token and W_down per row, blocks
+      along d), and dX_e = Q_f(dA) Q_f(W_gate[e])^T + Q_f(dB) Q_f(W_up[e])^T
+      (dA, dB quantised along f from their fp32 values, W_gate / W_up per row
+      of [d, f], blocks along f);
+    * the weight-gradient products contract over each expert's ragged token
+      set and stay BF16: dW_gate = X_e^T dA, dW_up = X_e^T dB,
+      dW_down = (w h)^T dY_e, with the unquantised X, dY and the fp32 dA, dB
+      (the gradient passes straight through the quantiser);
+    * the router-weight gradient, the softmax backward, dW_r, the shared expert
+      (BF16) and dX's router term are those of the BF16 backward.
+
+    quant=False replaces every quantise-dequantise by the identity, which must
+    reproduce moe_oracle.moe_backward.
+    """
+    qdq = mx_qdq if quant else (lambda v, axis: np.asarray(v, F64))
+    X = np.asarray(X, F64)
+    dY = np.asarray(dY, F64)
+    T, d = X.shape
+    E, _, f = W["W_gate"].shape
+    k = idx.shape[1]
+    Xh = qdq(X, 1)
+    dYh = qdq(dY, 1)
+    dX = np.zeros((T, d), F64)
+    dWg = np.zeros((E, d, f), F64)
+    dWu = np.zeros((E, d, f), F64)
+    dWd = np.zeros((E, f, d), F64)
+    dg = np.zeros((T, k), F64)
+    for e in range(E):
+        ts, ss = np.nonzero(np.asarray(idx) == e)
+        if ts.size == 0:
+            continue
+        Wg = np.asarray(W["W_gate"][e], F64)
+        Wu = np.asarray(W["W_up"][e], F64)
+        Wd = np.asarray(W["W_down"][e], F64)
+        a = Xh[ts] @ qdq(Wg, 0)                # forward: blocks of W_gate[e] [d, f] along d
+        b = Xh[ts] @ qdq(Wu, 0)
+        h = O.silu(a) * b
+        we = np.asarray(w, F64)[ts, ss][:, None]
+        dhp = dYh[ts] @ qdq(Wd, 1).T           # W_down[e] [f, d], blocks along d
+        dg[ts, ss] = (dhp * h).sum(axis=1)
+        dh = we * dhp
+        dA = dh * b * O._dsilu(a)
+        dB = dh * O.silu(a)
+        dWg[e] = X[ts].T @ dA
+        dWu[e] = X[ts].T @ dB
+        dWd[e] = (we * h).T @ dY[ts]
+        np.add.at(dX, ts, qdq(dA, 1) @ qdq(Wg, 1).T + qdq(dB, 1) @ qdq(Wu, 1).T)
+    dz_sel = O.softmax_restricted_backward(np.asarray(w, F64), dg)
+    dZ = np.zeros((T, W_r.shape[1]), F64)
+    np.put_along_axis(dZ, np.asarray(idx, np.int64), dz_sel, axis=1)
+    dW_r = X.T @ dZ
+    dX += dZ @ np.asarray(W_r, F64).T
+    out = dict(dX=dX, dW_gate=dWg, dW_up=dWu, dW_down=dWd, dW_r=dW_r, dZ=dZ, dg=dg,
+               dWg_s=None, dWu_s=None, dWd_s=None)
+    if W.get("Wg_s") is not None:             # the shared expert stays BF16
+        Wg = np.asarray(W["Wg_s"], F64)
+        Wu = np.asarray(W["Wu_s"], F64)
+        Wd = np.asarray(W["Wd_s"], F64)
+        a = X @ Wg
+        b = X @ Wu
+        dhs = dY @ Wd.T
+        dA = dhs * b * O._dsilu(a)
+        dB = dhs * O.silu(a)
+        out["dWg_s"] = X.T @ dA
+        out["dWu_s"] = X.T @ dB
+        out["dWd_s"] = (O.silu(a) * b).T @ dY
+        out["dX"] = out["dX"] + dA @ Wg.T + dB @ Wu.T
+    return out
