@@ -181,6 +181,14 @@ def moe_forward_mx(X, W, idx, w):
 
 
 
+def bf16_round(v):
+    """Round to the nearest bfloat16 (8 significand bits), ties to even, via
+    float32 (the GPU rounds its fp32 results the same way)."""
+    b = np.asarray(v, np.float32).view(np.uint32).astype(np.uint64)
+    b = (b + 0x7FFF + ((b >> 16) & 1)) & 0xFFFF0000
+    return b.astype(np.uint32).view(np.float32).astype(F64)
+
+
 def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True):
     """Backward of the layer with MXFP8 routed experts (teacher-forced on idx, w).
 
@@ -188,7 +196,9 @@ def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True):
     quantisation; it does not say which backward products run in MXFP8):
 
     * the pre-activations a, b and the activation h come from the MXFP8
-      forward (X quantised along d, W_gate / W_up along d);
+      forward (X quantised along d, W_gate / W_up along d); a and b are kept
+      in bf16 between the passes, as the BF16 path keeps them, and the
+      backward works from those values (quant=True only);
     * the two products that contract over a model dimension run in MXFP8:
       dh' = Q_d(dY) Q_d(W_down[e])^T (dY per token and W_down per row, blocks
       along d), and dX_e = Q_f(dA) Q_f(W_gate[e])^T + Q_f(dB) Q_f(W_up[e])^T
@@ -226,6 +236,8 @@ def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True):
         Wd = np.asarray(W["W_down"][e], F64)
         a = Xh[ts] @ qdq(Wg, 0)                # forward: blocks of W_gate[e] [d, f] along d
         b = Xh[ts] @ qdq(Wu, 0)
+        if quant:                              # kept in bf16 for the backward
+            a, b = bf16_round(a), bf16_round(b)
         h = O.silu(a) * b
         we = np.asarray(w, F64)[ts, ss][:, None]
         dhp = dYh[ts] @ qdq(Wd, 1).T           # W_down[e] [f, d], blocks along d
@@ -258,3 +270,78 @@ def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True):
         out["dWd_s"] = (O.silu(a) * b).T @ dY
         out["dX"] = out["dX"] + dA @ Wg.T + dB @ Wu.T
     return out
+
+
+# ---------------------------------------------------------------------------
+# Sampled evaluation of the MXFP8 backward for full-size workloads: each
+# sampled output follows the same definition as moe_backward_mx, restricted
+# to what it depends on.
+# ---------------------------------------------------------------------------
+
+def _mx_expert_weights(W, e):
+    """The routed weights of expert e as the MXFP8 passes see them."""
+    Wg = np.asarray(W["W_gate"][e], F64)
+    Wu = np.asarray(W["W_up"][e], F64)
+    Wd = np.asarray(W["W_down"][e], F64)
+    return dict(g_fwd=mx_qdq(Wg, 0), u_fwd=mx_qdq(Wu, 0), d_bwd=mx_qdq(Wd, 1),
+                g_bwd=mx_qdq(Wg, 1), u_bwd=mx_qdq(Wu, 1))
+
+
+def mx_token_backward(X, W_r, W, idx, w, dY, tokens):
+    """dX, dZ and dg of moe_backward_mx for the given tokens only."""
+    X = np.asarray(X, F64)
+    dY = np.asarray(dY, F64)
+    E = W["W_gate"].shape[0]
+    tokens = np.asarray(tokens)
+    k = idx.shape[1]
+    cache = {}
+    dX = np.zeros((len(tokens), X.shape[1]))
+    dg = np.zeros((len(tokens), k))
+    for n, t in enumerate(tokens):
+        xq = mx_qdq(X[t:t + 1], 1)[0]
+        dyq = mx_qdq(dY[t:t + 1], 1)[0]
+        for s in range(k):
+            e = int(idx[t, s])
+            if e not in cache:
+                cache[e] = _mx_expert_weights(W, e)
+            q = cache[e]
+            a = bf16_round(xq @ q["g_fwd"])
+            b = bf16_round(xq @ q["u_fwd"])
+            dhp = q["d_bwd"] @ dyq
+            dg[n, s] = dhp @ (O.silu(a) * b)
+            dh = w[t, s] * dhp
+            dA = dh * b * O._dsilu(a)
+            dB = dh * O.silu(a)
+            dX[n] += q["g_bwd"] @ mx_qdq(dA[None, :], 1)[0] + q["u_bwd"] @ mx_qdq(dB[None, :], 1)[0]
+    dz_sel = O.softmax_restricted_backward(np.asarray(w, F64)[tokens], dg)
+    dZ = np.zeros((len(tokens), W_r.shape[1]))
+    np.put_along_axis(dZ, np.asarray(idx, np.int64)[tokens], dz_sel, axis=1)
+    dX += dZ @ np.asarray(W_r, F64).T
+    if W.get("Wg_s") is not None:
+        Wg, Wu, Wd = (np.asarray(W[key], F64) for key in ("Wg_s", "Wu_s", "Wd_s"))
+        x = X[tokens]
+        a, b = x @ Wg, x @ Wu
+        dhs = dY[tokens] @ Wd.T
+        dX += (dhs * b * O._dsilu(a)) @ Wg.T + (dhs * O.silu(a)) @ Wu.T
+    return dX, dZ, dg
+
+
+def mx_expert_weight_grad_columns(X, W, idx, w, dY, e, cols):
+    """dW_gate[e][:, cols], dW_up[e][:, cols] and dW_down[e][cols, :] of
+    moe_backward_mx."""
+    X = np.asarray(X, F64)
+    dY = np.asarray(dY, F64)
+    ts, ss = np.nonzero(np.asarray(idx) == e)
+    Wg = np.asarray(W["W_gate"][e], F64)
+    Wu = np.asarray(W["W_up"][e], F64)
+    Wd = np.asarray(W["W_down"][e], F64)
+    xq = mx_qdq(X[ts], 1)
+    a = bf16_round(xq @ mx_qdq(Wg, 0)[:, cols])
+    b = bf16_round(xq @ mx_qdq(Wu, 0)[:, cols])
+    dhp = mx_qdq(dY[ts], 1) @ mx_qdq(Wd, 1)[cols, :].T
+    we = np.asarray(w, F64)[ts, ss][:, None]
+    dh = we * dhp
+    dA = dh * b * O._dsilu(a)
+    dB = dh * O.silu(a)
+    h = O.silu(a) * b
+    return X[ts].T @ dA, X[ts].T @ dB, (we * h).T @ dY[ts]

@@ -34,6 +34,18 @@ def layer(T=64, d=128, E=4, k=2, f=96, fs=0, seed=0):
     return inp["X"].astype(np.float64), inp["W_r"], W, idx, wts, inp["dY"].astype(np.float64)
 
 
+def test_bf16_round_closed_forms():
+    one = 1.0
+    assert M.bf16_round(one + 2.0 ** -8) == one                    # tie -> even (down)
+    assert M.bf16_round(one + 3 * 2.0 ** -8) == one + 2.0 ** -6    # tie -> even (up)
+    assert M.bf16_round(one + 2.0 ** -8 + 2.0 ** -20) == one + 2.0 ** -7
+    assert M.bf16_round(-(one + 2.0 ** -7)) == -(one + 2.0 ** -7)  # representable, kept
+    v = np.random.default_rng(0).standard_normal(1000)
+    r = M.bf16_round(v)
+    assert np.all(np.abs(r - v) <= np.abs(v) * 2.0 ** -8)          # half an ulp at 8 bits
+    assert np.all((r.astype(np.float32).view(np.uint32) & 0xFFFF) == 0)
+
+
 def test_without_quantisation_it_is_the_bf16_backward():
     X, W_r, W, idx, wts, dY = layer(fs=64, seed=1)
     a = M.moe_backward_mx(X, W_r, W, idx, wts, dY, quant=False)
@@ -157,3 +169,21 @@ def test_close_to_the_bf16_backward():
         assert 1e-4 < rel < 0.15, (key, rel)            # quantised, but close
     for key in ("dWg_s", "dWu_s", "dWd_s"):
         assert np.array_equal(mx[key], ref[key]), key   # the shared expert stays BF16
+
+
+def test_sampled_evaluation_matches_the_full_backward():
+    """The per-token and per-column evaluations used at full size give the
+    full MXFP8 backward's rows and columns."""
+    X, W_r, W, idx, wts, dY = layer(fs=64, seed=12)
+    full = M.moe_backward_mx(X, W_r, W, idx, wts, dY)
+    toks = np.array([0, 5, 17, 63])
+    dX, dZ, dg = M.mx_token_backward(X, W_r, W, idx, wts, dY, toks)
+    for name, got, ref in (("dX", dX, full["dX"][toks]), ("dZ", dZ, full["dZ"][toks]),
+                           ("dg", dg, full["dg"][toks])):
+        assert np.allclose(got, ref, rtol=0, atol=1e-12 * np.abs(ref).max()), name
+    cols = np.array([0, 33, 95])
+    for e in range(W["W_gate"].shape[0]):
+        a, b, c = M.mx_expert_weight_grad_columns(X, W, idx, wts, dY, e, cols)
+        for got, ref in ((a, full["dW_gate"][e][:, cols]), (b, full["dW_up"][e][:, cols]),
+                         (c, full["dW_down"][e][cols, :])):
+            assert np.allclose(got, ref, rtol=0, atol=1e-12 * max(np.abs(ref).max(), 1e-30))
