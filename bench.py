@@ -196,6 +196,44 @@ def mx_forward_timing(H, stream, inputs, steps, warmup):
     return out
 
 
+def mx_training_timing(H, stream, inputs, steps, warmup):
+    """route + plan + moe_forward_mx (pre-activations kept) + moe_backward_mx
+    on the training workload; the routed weights are pre-quantised once (both
+    layouts), outside the timing."""
+    import torch
+    from paper_2609_36070_amd.layer import DeviceLayer
+    from paper_2609_36070_amd.workloads import WORKLOADS
+    w = WORKLOADS["large_shared_train"]
+    L = DeviceLayer(w, inputs, mx=True)
+    for _ in range(warmup):
+        L.step_mx()
+    torch.cuda.synchronize()
+    a, m, b = H.create(), H.create(), H.create()
+    fwd = bwd = 0.0
+    for _ in range(steps):
+        H.record(a, stream)
+        L.route()
+        L.plan()
+        L.forward_mx()
+        H.record(m, stream)
+        L.backward_mx()
+        H.record(b, stream)
+        H.sync(b)
+        fwd += H.ms(a, m)
+        bwd += H.ms(m, b)
+    for e in (a, m, b):
+        H.destroy(e)
+    fwd /= steps
+    bwd /= steps
+    flops = w.fwd_flops() + w.bwd_flops()
+    out = {"workload": w.name, "forward_ms": round(fwd, 4), "backward_ms": round(bwd, 4),
+           "ms_per_step": round(fwd + bwd, 4),
+           "tflops": round(flops / ((fwd + bwd) * 1e-3) / 1e12, 2), "error_word": L.error_word()}
+    del L
+    torch.cuda.synchronize()
+    return out
+
+
 def fused_forward_timing(H, stream, L, steps):
     """route + plan + forward with the separate launches against the same with
     the fused persistent forward, on the benchmark layer (A and B saved when
@@ -488,6 +526,13 @@ def main():
         for name, v in mxf["stages"].items():
             log(f"   mx.{name:25s} {v['ms']:9.4f} ms  {v.get('tflops', '')}")
 
+    mxt = None
+    if not args.no_mx and w.name == "large_shared_train":
+        mxt = mx_training_timing(H, stream, inputs, max(3, args.steps // 2), 2)
+        mxt["speedup_vs_bf16_step"] = round(ms_step / mxt["ms_per_step"], 3)
+        log(f"[bench] MXFP8 training step: {mxt['ms_per_step']:.3f} ms (forward {mxt['forward_ms']:.3f}, "
+            f"backward {mxt['backward_ms']:.3f}; {mxt['tflops']} TFLOP/s), BF16 step {ms_step:.3f} ms")
+
     fused = None
     if not args.no_fused:
         fused = fused_forward_timing(H, stream, L, max(5, args.steps))
@@ -530,6 +575,7 @@ def main():
         "stages": stage_report,
         "schedule": sched,
         "mxfp8_forward": mxf,
+        "mxfp8_training_step": mxt,
         "fused_forward": fused,
         "bounded_memory": ring,
     }

@@ -117,7 +117,14 @@ typedef enum {
     MOE_WS_XS = 11,     /* E8M0 [T, d/32] scales of MOE_WS_XQ               */
     MOE_WS_HQ = 12,     /* E4M3 [T*k, f]  gated activation, plan order      */
     MOE_WS_HS = 13,     /* E8M0 [T*k, f/32] scales of MOE_WS_HQ             */
-    MOE_WS_COUNT = 14
+    /* MXFP8 backward only (moe_mx_workspace_region): */
+    MOE_WS_DYQ = 14,    /* E4M3 [T, d]    dY, one scale per 32 of d         */
+    MOE_WS_DYS = 15,    /* E8M0 [T, d/32] scales of MOE_WS_DYQ              */
+    MOE_WS_DAQ = 16,    /* E4M3 [T*k, f]  gradient wrt A, plan order        */
+    MOE_WS_DAS = 17,    /* E8M0 [T*k, f/32]                                 */
+    MOE_WS_DBQ = 18,    /* E4M3 [T*k, f]  gradient wrt B                    */
+    MOE_WS_DBS = 19,    /* E8M0 [T*k, f/32]                                 */
+    MOE_WS_COUNT = 20
 } moe_ws_tensor;
 
 /* MXFP8 routed-expert weights (§3.4 "MXFP8 Support"), written once by
@@ -227,15 +234,35 @@ moe_status moe_schedule(int64_t R, int64_t NK, int64_t L, int64_t c, const int32
 moe_status moe_mx_quantize_weights(const moe_shape *shape, const moe_weights *weights,
                                    const moe_mx_weights *mx, moe_stream stream);
 
-/* Workspace bytes of moe_forward_mx (it also serves moe_route and moe_plan);
- * 0 for an invalid or unsupported shape.  Pure host function. */
-size_t moe_mx_workspace_bytes(const moe_shape *shape);
+/* Workspace bytes of moe_forward_mx (with_backward = 0; it also serves
+ * moe_route and moe_plan) or of moe_forward_mx with save_for_backward = 1
+ * followed by moe_backward_mx (with_backward = 1); 0 for an invalid or
+ * unsupported shape.  Pure host function. */
+size_t moe_mx_workspace_bytes(const moe_shape *shape, int with_backward);
 
-/* Byte offset and size of a region of the MXFP8 forward workspace: only
- * MOE_WS_ERROR, MOE_WS_YEXP, MOE_WS_YSH, MOE_WS_XQ, MOE_WS_XS, MOE_WS_HQ and
- * MOE_WS_HS exist there (MOE_EINVAL for the others). */
+/* Byte offset and size of a region of the MXFP8 workspace: the MXFP8 regions
+ * MOE_WS_XQ .. MOE_WS_DBS, or any region of moe_workspace_region's
+ * backward layout (the MXFP8 paths use it for the rest). */
 moe_status moe_mx_workspace_region(const moe_shape *shape, moe_ws_tensor which, size_t *offset,
                                    size_t *bytes);
+
+/* MXFP8 weights for the backward (§3.4 "MXFP8 Support"), written by
+ * moe_mx_quantize_weights_bwd.  Each weight row is quantised along the axis
+ * its backward product contracts, which is its contiguous axis, so the
+ * layouts are those of the bf16 weights:
+ *   Wg_q, Wu_q [E, d, f] codes, blocks along f; Wg_s, Wu_s [E, d, f/32]
+ *   Wd_q       [E, f, d] codes, blocks along d; Wd_s       [E, f, d/32]
+ * (same quantisation rule as moe_mx_weights). */
+typedef struct {
+    uint8_t *Wg_q, *Wu_q, *Wd_q;
+    uint8_t *Wg_s, *Wu_s, *Wd_s;
+} moe_mx_bwd_weights;
+
+/* Pre-quantises the routed weights for moe_backward_mx (once per weight
+ * update).  Reads W_gate, W_up, W_down of `weights`; writes every array of
+ * `mx`.  Limits as moe_mx_quantize_weights. */
+moe_status moe_mx_quantize_weights_bwd(const moe_shape *shape, const moe_weights *weights,
+                                       const moe_mx_bwd_weights *mx, moe_stream stream);
 
 /* Forward of the layer with MXFP8 routed experts and a BF16 shared expert
  * (§3.4 "MXFP8 Support").  As moe_forward, except:
@@ -246,12 +273,36 @@ moe_status moe_mx_workspace_region(const moe_shape *shape, moe_ws_tensor which, 
  *   - the gated activation H is quantised along f (32-blocks) straight from
  *     fp32 in the up/gate epilogue, and Yexp is rounded to bf16;
  *   - `weights` supplies only the shared expert (its routed pointers are
- *     ignored and may be NULL); nothing is kept for a backward pass.
- * Y [T, d] bf16 out.  ws: at least moe_mx_workspace_bytes(shape) bytes. */
+ *     ignored and may be NULL);
+ *   - save_for_backward = 1 keeps the routed pre-activations A, B (bf16,
+ *     from the MXFP8 products) and the shared expert's for moe_backward_mx.
+ * Y [T, d] bf16 out.  ws: at least moe_mx_workspace_bytes(shape,
+ * save_for_backward) bytes. */
 moe_status moe_forward_mx(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
                           const moe_mx_weights *mx, const int32_t *topk_idx, const float *topk_w,
-                          const moe_plan_bufs *plan, moe_bf16 *Y, void *ws, size_t ws_bytes,
-                          moe_stream stream, const moe_stage_events *events /* NULL = no timing */);
+                          const moe_plan_bufs *plan, moe_bf16 *Y, int save_for_backward, void *ws,
+                          size_t ws_bytes, moe_stream stream,
+                          const moe_stage_events *events /* NULL = no timing */);
+
+/* Backward of the layer with MXFP8 routed experts (§3.4 "MXFP8 Support":
+ * activation quantisation fused into the dispatch, the grouped GEMMs and the
+ * gated activation).  As moe_backward, except:
+ *   - dY is quantised once per token along d, and dh' = Q(dY) Q(W_down)^T
+ *     runs on the block-scaled matrix cores with the weights in `mx`;
+ *   - the gated-activation backward in that GEMM's epilogue writes dA, dB
+ *     in bf16 and also quantised along f, and dXperm = Q(dA) Q(W_gate)^T +
+ *     Q(dB) Q(W_up)^T runs in MXFP8;
+ *   - the weight gradients contract over each expert's ragged token set
+ *     and stay BF16 on X, dY and the bf16 dA, dB, w h; the shared expert,
+ *     the router gradient and dX's router term are those of moe_backward.
+ * Needs the ws of a preceding moe_forward_mx with save_for_backward = 1 (at
+ * least moe_mx_workspace_bytes(shape, 1) bytes) and the same inputs.
+ * `weights` as for moe_backward. */
+moe_status moe_backward_mx(const moe_shape *shape, const moe_bf16 *dY, const moe_bf16 *X,
+                           const moe_bf16 *W_r, const moe_weights *weights,
+                           const moe_mx_bwd_weights *mx, const int32_t *topk_idx,
+                           const float *topk_w, const moe_plan_bufs *plan, moe_bf16 *dX,
+                           const moe_grads *grads, void *ws, size_t ws_bytes, moe_stream stream);
 
 /* Materialised dispatch (§3.1 "Scheduling", local part): Xperm[p] =
  * X[perm[p] / k] for p < T*k.  moe_forward does not need it (its GEMMs read

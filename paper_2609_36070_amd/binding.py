@@ -21,13 +21,14 @@ c_int = ctypes.c_int
 MOE_OK, MOE_EINVAL, MOE_EUNSUPPORTED, MOE_ENOSPACE, MOE_EHIP = range(5)
 WS_ERROR, WS_A, WS_B, WS_H, WS_YEXP, WS_YSH, WS_DG, WS_DA, WS_DB, WS_DXPERM = range(10)
 WS_XQ, WS_XS, WS_HQ, WS_HS = range(10, 14)
+WS_DYQ, WS_DYS, WS_DAQ, WS_DAS, WS_DBQ, WS_DBS = range(14, 20)
 
 EXPORTS = ("moe_workspace_bytes", "moe_workspace_region", "moe_route", "moe_plan",
            "moe_schedule_workspace_bytes", "moe_schedule", "moe_dispatch", "moe_forward",
            "moe_backward", "moe_mx_quantize_weights", "moe_mx_workspace_bytes",
            "moe_mx_workspace_region", "moe_forward_mx", "moe_ring_workspace_bytes",
-           "moe_forward_ring", "moe_backward_ring", "moe_forward_fused", "moe_status_string",
-           "moe_version")
+           "moe_forward_ring", "moe_backward_ring", "moe_forward_fused",
+           "moe_mx_quantize_weights_bwd", "moe_backward_mx", "moe_status_string", "moe_version")
 
 
 class MoeShape(ctypes.Structure):
@@ -40,6 +41,10 @@ class MoeWeights(ctypes.Structure):
 
 
 class MoeMxWeights(ctypes.Structure):
+    _fields_ = [(n, c_void_p) for n in ("Wg_q", "Wu_q", "Wd_q", "Wg_s", "Wu_s", "Wd_s")]
+
+
+class MoeMxBwdWeights(ctypes.Structure):
     _fields_ = [(n, c_void_p) for n in ("Wg_q", "Wu_q", "Wd_q", "Wg_s", "Wu_s", "Wd_s")]
 
 
@@ -100,12 +105,17 @@ def lib():
                                    c_void_p, c_size_t, c_void_p, P(MoeStageEvents)]
         L.moe_mx_quantize_weights.argtypes = [P(MoeShape), P(MoeWeights), P(MoeMxWeights),
                                               c_void_p]
-        L.moe_mx_workspace_bytes.argtypes = [P(MoeShape)]
+        L.moe_mx_workspace_bytes.argtypes = [P(MoeShape), c_int]
         L.moe_mx_workspace_bytes.restype = c_size_t
         L.moe_mx_workspace_region.argtypes = [P(MoeShape), c_int, P(c_size_t), P(c_size_t)]
         L.moe_forward_mx.argtypes = [P(MoeShape), c_void_p, P(MoeWeights), P(MoeMxWeights),
-                                     c_void_p, c_void_p, P(MoePlanBufs), c_void_p, c_void_p,
-                                     c_size_t, c_void_p, P(MoeStageEvents)]
+                                     c_void_p, c_void_p, P(MoePlanBufs), c_void_p, c_int,
+                                     c_void_p, c_size_t, c_void_p, P(MoeStageEvents)]
+        L.moe_mx_quantize_weights_bwd.argtypes = [P(MoeShape), P(MoeWeights), P(MoeMxBwdWeights),
+                                                  c_void_p]
+        L.moe_backward_mx.argtypes = [P(MoeShape), c_void_p, c_void_p, c_void_p, P(MoeWeights),
+                                      P(MoeMxBwdWeights), c_void_p, c_void_p, P(MoePlanBufs),
+                                      c_void_p, P(MoeGrads), c_void_p, c_size_t, c_void_p]
         L.moe_forward_fused.argtypes = [P(MoeShape), c_void_p, P(MoeWeights), c_void_p, c_void_p,
                                         P(MoePlanBufs), c_void_p, c_int, c_void_p, c_size_t,
                                         c_void_p]
@@ -120,7 +130,8 @@ def lib():
         for fn in ("moe_route", "moe_plan", "moe_schedule", "moe_dispatch", "moe_forward",
                    "moe_backward", "moe_workspace_region", "moe_mx_quantize_weights",
                    "moe_mx_workspace_region", "moe_forward_mx", "moe_forward_ring",
-                   "moe_backward_ring", "moe_forward_fused"):
+                   "moe_backward_ring", "moe_forward_fused", "moe_mx_quantize_weights_bwd",
+                   "moe_backward_mx"):
             getattr(L, fn).restype = c_int
         L.moe_status_string.argtypes = [c_int]
         L.moe_status_string.restype = ctypes.c_char_p
@@ -225,8 +236,29 @@ def mx_weights_struct(Wg_q, Wu_q, Wd_q, Wg_s, Wu_s, Wd_s) -> MoeMxWeights:
     return MoeMxWeights(_p(Wg_q), _p(Wu_q), _p(Wd_q), _p(Wg_s), _p(Wu_s), _p(Wd_s))
 
 
-def moe_mx_workspace_bytes(shape: MoeShape) -> int:
-    return int(lib().moe_mx_workspace_bytes(ctypes.byref(shape)))
+def moe_mx_workspace_bytes(shape: MoeShape, with_backward: bool = False) -> int:
+    return int(lib().moe_mx_workspace_bytes(ctypes.byref(shape), int(bool(with_backward))))
+
+
+def mx_bwd_weights_struct(Wg_q, Wu_q, Wd_q, Wg_s, Wu_s, Wd_s) -> MoeMxBwdWeights:
+    return MoeMxBwdWeights(_p(Wg_q), _p(Wu_q), _p(Wd_q), _p(Wg_s), _p(Wu_s), _p(Wd_s))
+
+
+def moe_mx_quantize_weights_bwd(shape, weights: MoeWeights, mx: MoeMxBwdWeights, stream=None,
+                                raise_on_error=True):
+    st = lib().moe_mx_quantize_weights_bwd(ctypes.byref(shape), ctypes.byref(weights),
+                                           ctypes.byref(mx), _stream(stream))
+    return _check("moe_mx_quantize_weights_bwd", st, raise_on_error)
+
+
+def moe_backward_mx(shape, dY, X, W_r, weights: MoeWeights, mx: MoeMxBwdWeights, topk_idx, topk_w,
+                    plan: MoePlanBufs, dX, grads: MoeGrads, ws, ws_bytes=None, stream=None,
+                    raise_on_error=True):
+    nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
+    st = lib().moe_backward_mx(ctypes.byref(shape), _p(dY), _p(X), _p(W_r), ctypes.byref(weights),
+                               ctypes.byref(mx), _p(topk_idx), _p(topk_w), ctypes.byref(plan),
+                               _p(dX), ctypes.byref(grads), _p(ws), nbytes, _stream(stream))
+    return _check("moe_backward_mx", st, raise_on_error)
 
 
 def moe_mx_workspace_region(shape: MoeShape, which: int):
@@ -246,11 +278,12 @@ def moe_mx_quantize_weights(shape, weights: MoeWeights, mx: MoeMxWeights, stream
 
 def moe_forward_mx(shape, X, weights: MoeWeights, mx: MoeMxWeights, topk_idx, topk_w,
                    plan: MoePlanBufs, Y, ws, ws_bytes=None, stream=None, raise_on_error=True,
-                   events: MoeStageEvents = None):
+                   events: MoeStageEvents = None, save_for_backward=False):
     nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
     st = lib().moe_forward_mx(ctypes.byref(shape), _p(X), ctypes.byref(weights), ctypes.byref(mx),
-                              _p(topk_idx), _p(topk_w), ctypes.byref(plan), _p(Y), _p(ws), nbytes,
-                              _stream(stream), None if events is None else ctypes.byref(events))
+                              _p(topk_idx), _p(topk_w), ctypes.byref(plan), _p(Y),
+                              int(bool(save_for_backward)), _p(ws), nbytes, _stream(stream),
+                              None if events is None else ctypes.byref(events))
     return _check("moe_forward_mx", st, raise_on_error)
 
 

@@ -29,6 +29,8 @@ struct Layout {
     size_t bwd_total;
     size_t xq, xs, hq, hsc;   // MXFP8 forward: quantised X and H (over the backward regions)
     size_t mx_total;
+    size_t dyq, dys, daq, das, dbq, dbs;   // MXFP8 backward: quantised dY, dA, dB
+    size_t mxb_total;
     long act_rows;             // rows of the per-route activation buffers
     int dg_parts;
 };
@@ -87,6 +89,14 @@ Layout make_layout(const moe_shape &s, long ring_rows = -1) {
     L.hq = take(R * f);
     L.hsc = take(R * f / 32);
     L.mx_total = o;
+    o = L.bwd_total;
+    L.dyq = take(T * d);
+    L.dys = take(T * d / 32);
+    L.daq = take(R * f);
+    L.das = take(R * f / 32);
+    L.dbq = take(R * f);
+    L.dbs = take(R * f / 32);
+    L.mxb_total = o;
     return L;
 }
 
@@ -771,9 +781,11 @@ moe_status moe_backward_ring(const moe_shape *shape, const moe_bf16 *dY, const m
     return MOE_OK;
 }
 
-size_t moe_mx_workspace_bytes(const moe_shape *shape) {
+size_t moe_mx_workspace_bytes(const moe_shape *shape, int with_backward) {
     if (check_shape(shape) != MOE_OK || check_mx_shape(shape) != MOE_OK) return 0;
-    return make_layout(*shape).mx_total;
+    const Layout L = make_layout(*shape);
+    if (!with_backward) return L.mx_total;
+    return L.mxb_total > L.mx_total ? L.mxb_total : L.mx_total;
 }
 
 moe_status moe_mx_workspace_region(const moe_shape *shape, moe_ws_tensor which, size_t *offset,
@@ -793,7 +805,13 @@ moe_status moe_mx_workspace_region(const moe_shape *shape, moe_ws_tensor which, 
         case MOE_WS_XS: *offset = L.xs; *bytes = T * d / 32; break;
         case MOE_WS_HQ: *offset = L.hq; *bytes = R * f; break;
         case MOE_WS_HS: *offset = L.hsc; *bytes = R * f / 32; break;
-        default: return MOE_EINVAL;
+        case MOE_WS_DYQ: *offset = L.dyq; *bytes = T * d; break;
+        case MOE_WS_DYS: *offset = L.dys; *bytes = T * d / 32; break;
+        case MOE_WS_DAQ: *offset = L.daq; *bytes = R * f; break;
+        case MOE_WS_DAS: *offset = L.das; *bytes = R * f / 32; break;
+        case MOE_WS_DBQ: *offset = L.dbq; *bytes = R * f; break;
+        case MOE_WS_DBS: *offset = L.dbs; *bytes = R * f / 32; break;
+        default: return moe_workspace_region(shape, 1, which, offset, bytes);
     }
     return MOE_OK;
 }
@@ -818,8 +836,8 @@ moe_status moe_mx_quantize_weights(const moe_shape *shape, const moe_weights *we
 
 moe_status moe_forward_mx(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
                           const moe_mx_weights *mx, const int32_t *topk_idx, const float *topk_w,
-                          const moe_plan_bufs *plan, moe_bf16 *Y, void *ws, size_t ws_bytes,
-                          moe_stream stream, const moe_stage_events *events) {
+                          const moe_plan_bufs *plan, moe_bf16 *Y, int save_for_backward, void *ws,
+                          size_t ws_bytes, moe_stream stream, const moe_stage_events *events) {
     moe_status st = check_shape(shape);
     if (st != MOE_OK) return st;
     if ((st = check_mx_shape(shape)) != MOE_OK) return st;
@@ -850,6 +868,7 @@ moe_status moe_forward_mx(const moe_shape *shape, const moe_bf16 *X, const moe_w
         g.B = mx->Wg_q; g.Bs = mx->Wg_s; g.B2 = mx->Wu_q; g.Bs2 = mx->Wu_s;
         g.K = d; g.N = f; g.offsets = plan->offsets; g.E = E;
         g.C = hq; g.Cs = hs;
+        if (save_for_backward) { g.Sa = at<uint16_t>(ws, L.A); g.Sb = at<uint16_t>(ws, L.B); }
         g.a_bytes = (uint32_t)((long)(T > 0 ? T : 1) * d);
         g.as_bytes = (uint32_t)((long)(T > 0 ? T : 1) * d / 32);
         g.b_bytes = (uint32_t)((long)E * f * d);
@@ -857,7 +876,7 @@ moe_status moe_forward_mx(const moe_shape *shape, const moe_bf16 *X, const moe_w
         MOE_TRY(launch_gemm_mx_up(g, R, E, s));
     }
     MOE_TRY(mk.mark(2));
-    if (fs > 0) MOE_TRY(shared_up(*shape, L, ws, X, weights, false, s));
+    if (fs > 0) MOE_TRY(shared_up(*shape, L, ws, X, weights, save_for_backward != 0, s));
     MOE_TRY(mk.mark(3));
     {   // routed down
         MxGemmArgs g;
@@ -877,6 +896,96 @@ moe_status moe_forward_mx(const moe_shape *shape, const moe_bf16 *X, const moe_w
     MOE_TRY(launch_combine(at<uint16_t>(ws, L.Yexp), fs > 0 ? at<uint16_t>(ws, L.Ysh) : nullptr,
                            topk_w, plan->route_pos, T, d, k, Y, s));
     MOE_TRY(mk.mark(6));
+    return MOE_OK;
+}
+
+moe_status moe_mx_quantize_weights_bwd(const moe_shape *shape, const moe_weights *weights,
+                                       const moe_mx_bwd_weights *mx, moe_stream stream) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if ((st = check_mx_shape(shape)) != MOE_OK) return st;
+    if (!weights || !ptr_ok(weights->W_gate) || !ptr_ok(weights->W_up) || !ptr_ok(weights->W_down))
+        return MOE_EINVAL;
+    if (!mx || !ptr_ok(mx->Wg_q) || !ptr_ok(mx->Wu_q) || !ptr_ok(mx->Wd_q) || !ptr_ok(mx->Wg_s) ||
+        !ptr_ok(mx->Wu_s) || !ptr_ok(mx->Wd_s))
+        return MOE_EINVAL;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const long E = shape->E, d = shape->d, f = shape->f;
+    // each weight row is already contiguous along the axis its backward
+    // product contracts: W_gate / W_up [E, d, f] along f, W_down [E, f, d] along d
+    MOE_TRY(launch_mx_quant_rows(weights->W_gate, E * d, (int)f, mx->Wg_q, mx->Wg_s, s));
+    MOE_TRY(launch_mx_quant_rows(weights->W_up, E * d, (int)f, mx->Wu_q, mx->Wu_s, s));
+    MOE_TRY(launch_mx_quant_rows(weights->W_down, E * f, (int)d, mx->Wd_q, mx->Wd_s, s));
+    return MOE_OK;
+}
+
+moe_status moe_backward_mx(const moe_shape *shape, const moe_bf16 *dY, const moe_bf16 *X,
+                           const moe_bf16 *W_r, const moe_weights *weights,
+                           const moe_mx_bwd_weights *mx, const int32_t *topk_idx, const float *topk_w,
+                           const moe_plan_bufs *plan, moe_bf16 *dX, const moe_grads *grads, void *ws,
+                           size_t ws_bytes, moe_stream stream) {
+    moe_status st = check_backward_args(shape, dY, X, W_r, weights, topk_idx, topk_w, plan, dX, grads);
+    if (st != MOE_OK) return st;
+    if ((st = check_mx_shape(shape)) != MOE_OK) return st;
+    if (!mx || !ptr_ok(mx->Wg_q) || !ptr_ok(mx->Wu_q) || !ptr_ok(mx->Wd_q) || !ptr_ok(mx->Wg_s) ||
+        !ptr_ok(mx->Wu_s) || !ptr_ok(mx->Wd_s))
+        return MOE_EINVAL;
+    if (!ptr_ok(ws)) return MOE_EINVAL;
+    const Layout L = make_layout(*shape);
+    if (ws_bytes < L.mxb_total || ws_bytes < L.mx_total) return MOE_ENOSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int T = (int)shape->T, d = (int)shape->d, E = (int)shape->E, k = (int)shape->k;
+    const int f = (int)shape->f;
+    const long R = (long)T * k;
+    const long Tn = T > 0 ? T : 1, Rn = R > 0 ? R : 1;
+    const Window all{plan->offsets, 0, (int)R};
+    const bool shared = shape->f_shared > 0;
+    float *dZ = grads->dZ ? grads->dZ : at<float>(ws, L.dZ);
+    uint8_t *dyq = at<uint8_t>(ws, L.dyq), *dys = at<uint8_t>(ws, L.dys);
+    uint8_t *daq = at<uint8_t>(ws, L.daq), *das = at<uint8_t>(ws, L.das);
+    uint8_t *dbq = at<uint8_t>(ws, L.dbq), *dbs = at<uint8_t>(ws, L.dbs);
+
+    MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, at<int>(ws, L.rowidx),
+                        at<float>(ws, L.wperm), at<uint16_t>(ws, L.zeros), s));
+    // the reverse-combine's activation quantisation: dY once per token, before the gather
+    MOE_TRY(launch_mx_quant_rows(dY, T, d, dyq, dys, s));
+    {   // dh' = Q(dY) Q(W_down)^T with the gated-activation backward; dA, dB quantised along f
+        MxGemmArgs g;
+        g.A = dyq; g.As = dys; g.a_rows = at<int>(ws, L.rowidx); g.a_nrows = (int)Tn;
+        g.B = mx->Wd_q; g.Bs = mx->Wd_s;
+        g.K = d; g.N = f; g.offsets = plan->offsets; g.E = E;
+        g.C = daq; g.Cs = das; g.C2 = dbq; g.Cs2 = dbs;
+        g.Cb = at<uint16_t>(ws, L.dA); g.Cb2 = at<uint16_t>(ws, L.dB); g.Cb3 = at<uint16_t>(ws, L.Hw);
+        g.E1 = at<uint16_t>(ws, L.A); g.E2 = at<uint16_t>(ws, L.B);
+        g.rowscale = at<float>(ws, L.wperm);
+        g.dgpart = at<float>(ws, L.dgpart); g.dg_ld = L.dg_parts;
+        g.a_bytes = (uint32_t)(Tn * d);
+        g.as_bytes = (uint32_t)(Tn * d / 32);
+        g.b_bytes = (uint32_t)((long)E * f * d);
+        g.bs_bytes = (uint32_t)((long)E * f * d / 32);
+        MOE_TRY(launch_gemm_mx_dgrad(g, R, E, s));
+    }
+    MOE_TRY(launch_softmax_bwd(at<float>(ws, L.dgpart), L.dg_parts, plan->route_pos, topk_w, topk_idx,
+                               T, k, E, at<float>(ws, L.dg), dZ, s));
+    {   // dXperm = Q(dA) Q(W_gate)^T + Q(dB) Q(W_up)^T
+        MxGemmArgs g;
+        g.A = daq; g.As = das; g.A2 = dbq; g.As2 = dbs; g.a_nrows = (int)Rn;
+        g.B = mx->Wg_q; g.Bs = mx->Wg_s; g.B2 = mx->Wu_q; g.Bs2 = mx->Wu_s;
+        g.K = f; g.N = d; g.offsets = plan->offsets; g.E = E;
+        g.Cb = at<uint16_t>(ws, L.dXperm);
+        g.a_bytes = (uint32_t)(Rn * f);
+        g.as_bytes = (uint32_t)(Rn * f / 32);
+        g.b_bytes = (uint32_t)((long)E * d * f);
+        g.bs_bytes = (uint32_t)((long)E * d * f / 32);
+        MOE_TRY(launch_gemm_mx_dx(g, R, E, s));
+    }
+    // weight gradients in BF16 on the unquantised operands
+    for (int i = 0; i < 3; ++i)
+        MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, i), E, s));
+    if (shared) MOE_TRY(shared_backward(*shape, L, ws, dY, X, weights, grads, StageMarks{nullptr, s}, s));
+    MOE_TRY(launch_dwr(X, dZ, T, d, E, at<float>(ws, L.dwr_part), grads->dW_r, s));
+    MOE_TRY(launch_reverse_combine(at<uint16_t>(ws, L.dXperm), shared ? at<uint16_t>(ws, L.dXsh) : nullptr,
+                                   dZ, W_r, plan->route_pos, T, d, k, E, nullptr, dX, s));
     return MOE_OK;
 }
 

@@ -6,6 +6,13 @@
 //            H = silu(g) * u, quantised to MXFP8 along f (the activation
 //            quantisation fused into the gated activation) -> Hq, Hs
 //   MX_DOWN  Yexp = Hq[p] . Wd_q[e][n] -> bf16
+//   MX_DGRAD dh' = dYq[tok(p)] . Wd_qd[e][n] (W_down rows quantised along d),
+//            then the gated-activation backward on the saved A, B: dg partials
+//            <dh', h>, dA = w dh' B silu'(A), dB = w dh' silu(A), Hw = w h;
+//            dA and dB go out in bf16 (for the weight gradients) and
+//            quantised to MXFP8 along f (for the dX product)
+//   MX_DX    dXperm = dAq[p] . Wg_qf[e][n] + dBq[p] . Wu_qf[e][n] (one K loop
+//            over both halves; W_gate / W_up rows quantised along f) -> bf16
 //
 // Every operand is a matrix of K-contiguous byte rows (A: token or position
 // rows; B: one row per output column, the pre-quantised weight layout) with
@@ -42,7 +49,7 @@ constexpr int TILE = BM * BK;                      // bytes per operand per stag
 constexpr int LD_PER_OP = TILE / 1024 / NWAVES;    // 1 KB direct loads per operand per wave per step
 static_assert(WN == 64 || WN == 128, "gate/up column pairs need 64- or 128-column wave tiles");
 
-enum MxMode { MX_UP = 0, MX_DOWN = 1 };
+enum MxMode { MX_UP = 0, MX_DOWN = 1, MX_DGRAD = 2, MX_DX = 3 };
 
 typedef int i32x8_t __attribute__((ext_vector_type(8)));
 
@@ -142,7 +149,6 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
     // ungathered A) are linear in q, so one VGPR per parity of q serves all
     // loads; a gathered A needs one per load.
     const __amdgpu_buffer_rsrc_t rA = make_rsrc(g.A, g.a_bytes);
-    const __amdgpu_buffer_rsrc_t rAs = make_rsrc(g.As, g.as_bytes);
     // (B resources are built per load from the selected base: a conditional
     // between two resource values is not accepted by the host compilation)
     const int l8 = lane >> 3;
@@ -150,7 +156,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
     const uint32_t col_odd = 16u * (uint32_t)((lane & 7) ^ ((4 + (l8 >> 1)) & 7));
     const uint32_t K = (uint32_t)g.K;
     const uint32_t b_lane_even = (uint32_t)l8 * K + col_even, b_lane_odd = (uint32_t)l8 * K + col_odd;
-    constexpr bool GATHER = (MODE == MX_UP);
+    constexpr bool GATHER = (MODE == MX_UP || MODE == MX_DGRAD);
     uint32_t a_off[LD_PER_OP];   // gathered A only
 #pragma unroll
     for (int i = 0; i < LD_PER_OP; ++i) {
@@ -174,8 +180,12 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
         }
     }
 
-    const int nk = g.K / BK;
-    auto issue = [&](int kt, uint8_t *la, uint8_t *lb, uint32_t *sa, uint32_t *sb) {
+    const int nk_half = g.K / BK;
+    const int nk = (MODE == MX_DX) ? 2 * nk_half : nk_half;
+    auto issue = [&](int kt_all, uint8_t *la, uint8_t *lb, uint32_t *sa, uint32_t *sb) {
+        // MX_DX: the second half of the K loop reads dBq against the W_up rows
+        const bool second = (MODE == MX_DX) && kt_all >= nk_half;
+        const int kt = second ? kt_all - nk_half : kt_all;
         const uint32_t kb = (uint32_t)kt * BK;
 #pragma unroll
         for (int i = 0; i < LD_PER_OP; ++i) {
@@ -186,7 +196,8 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
             } else {
                 // rows past the region (or the operand) hold results that are never stored
                 const uint32_t arow = (uint32_t)(row0 + 8 * q);
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (LDSP void *)(la + q * 1024), 16,
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(second ? g.A2 : g.A, g.a_bytes),
+                                                         (LDSP void *)(la + q * 1024), 16,
                                                          (q & 1) ? b_lane_odd : b_lane_even,
                                                          arow * K + kb, 0, 0);
             }
@@ -196,7 +207,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
             const int q = LD_PER_OP * wave + i;
             // B row of instruction q less the lane part l8 (uniform); MX_UP: tile
             // rows 8 q .. 8 q + 7 lie in column group q / 4, gate or up
-            const bool up = (MODE == MX_UP) && ((q >> 2) & 1);
+            const bool up = ((MODE == MX_UP) && ((q >> 2) & 1)) || second;
             const uint32_t brow = (MODE == MX_UP)
                 ? (uint32_t)(e * g.N + n0 + (q >> 3) * 32 + 8 * (q & 3))
                 : (uint32_t)(e * g.N + n0 + 8 * q);
@@ -209,10 +220,11 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
         for (int i = 0; i < SC_PER_WAVE; ++i) {
             const int c = SC_PER_WAVE * wave + i;
             if (c < 4) {
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rAs, (LDSP void *)(sa + 64 * c), 4, sc_off[i],
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(second ? g.As2 : g.As, g.as_bytes),
+                                                         (LDSP void *)(sa + 64 * c), 4, sc_off[i],
                                                          4 * kt, 0, 0);
             } else {
-                const bool up = (MODE == MX_UP) && (c - 4 >= 2);
+                const bool up = ((MODE == MX_UP) && (c - 4 >= 2)) || second;
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(up ? g.Bs2 : g.Bs, g.bs_bytes),
                                                          (LDSP void *)(sb + 64 * (c - 4)), 4,
                                                          sc_off[i], 4 * kt, 0, 0);
@@ -344,11 +356,92 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
                         *reinterpret_cast<u32x2_t *>(g.C + (long)p * g.N + fcol0 + c) =
                             e4m3_pack8(hv, s);
                         if ((lane & 3) == 0) g.Cs[(long)p * hs_row + fcol0 / 32] = (uint8_t)(s + 127);
+                        if (g.Sa) {   // pre-activations for the backward
+                            st_u32x4(g.Sa + (long)p * g.N + fcol0 + c, pack_bf8(a));
+                            st_u32x4(g.Sb + (long)p * g.N + fcol0 + c, pack_bf8(b));
+                        }
                     }
                 }
             }
         }
-    } else {
+    } else if constexpr (MODE == MX_DGRAD) {
+        // per row: the gated-activation backward on the saved A, B, then dA
+        // and dB out in bf16 and quantised along f (a 32-column block is 4
+        // neighbouring lanes of one row); <dh', h> summed over the row's
+        // columns in a fixed order (lanes, then waves)
+        constexpr int LPR = WN / 8, RPP = 64 / LPR;
+        static_assert(WAVES_N <= 4, "one dg partial array per wave column");
+        auto red_of = [&](int w) {
+            return reinterpret_cast<float *>(w == 0 ? sc_a0 : w == 1 ? sc_b0 : w == 2 ? sc_a1 : sc_b1);
+        };
+        const long fs_row = g.N / 32;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            stage(i);
+            // not unrolled: a body this size unrolled 8 x 4 times makes the
+            // compiler keep i dynamic and the accumulators in scratch
+#pragma unroll 1
+            for (int t = 0; t < 32 / RPP; ++t) {
+                const int row = lane / LPR + RPP * t, c = 8 * (lane % LPR);
+                const int rl = wm * WM + 32 * i + row;
+                const int p = row0 + rl;
+                const int pl = min(p, row_end - 1);
+                const f32x8 dhp = read8(row, c);
+                const float wv = g.rowscale[pl];
+                const int col = n0 + wn * WN + c;
+                const long o = (long)pl * g.N + col;
+                const u32x4_t av = ld_u32x4(g.E1 + o), bv = ld_u32x4(g.E2 + o);
+                f32x8 dav, dbv, hw;
+                float prod = 0.f, amax_a = 0.f, amax_b = 0.f;
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const float a = (k & 1) ? bf_hi(av[k >> 1]) : bf_lo(av[k >> 1]);
+                    const float b = (k & 1) ? bf_hi(bv[k >> 1]) : bf_lo(bv[k >> 1]);
+                    const float sg = 1.0f / (1.0f + expf(-a));
+                    const float sl = a * sg;
+                    const float h = sl * b;
+                    prod = prod + dhp[k] * h;
+                    const float dh = wv * dhp[k];
+                    dav[k] = dh * b * (sg * (1.0f + a * (1.0f - sg)));
+                    dbv[k] = dh * sl;
+                    hw[k] = wv * h;
+                    amax_a = fmaxf(amax_a, fabsf(dav[k]));
+                    amax_b = fmaxf(amax_b, fabsf(dbv[k]));
+                }
+                amax_a = fmaxf(amax_a, shfl_xor_f(amax_a, 1));
+                amax_a = fmaxf(amax_a, shfl_xor_f(amax_a, 2));
+                amax_b = fmaxf(amax_b, shfl_xor_f(amax_b, 1));
+                amax_b = fmaxf(amax_b, shfl_xor_f(amax_b, 2));
+                const int sa = mx_shared_exp(amax_a), sb = mx_shared_exp(amax_b);
+                if (p < row_end) {
+                    st_u32x4(g.Cb + o, pack_bf8(dav));
+                    st_u32x4(g.Cb2 + o, pack_bf8(dbv));
+                    st_u32x4(g.Cb3 + o, pack_bf8(hw));
+                    *reinterpret_cast<u32x2_t *>(g.C + o) = e4m3_pack8(dav, sa);
+                    *reinterpret_cast<u32x2_t *>(g.C2 + o) = e4m3_pack8(dbv, sb);
+                    if ((lane & 3) == 0) {
+                        g.Cs[(long)p * fs_row + col / 32] = (uint8_t)(sa + 127);
+                        g.Cs2[(long)p * fs_row + col / 32] = (uint8_t)(sb + 127);
+                    }
+                } else {
+                    prod = 0.f;
+                }
+#pragma unroll
+                for (int m = 1; m < LPR; m <<= 1) prod = prod + shfl_xor_f(prod, m);
+                if (lane % LPR == 0) red_of(wn)[rl] = prod;
+            }
+        }
+        __syncthreads();
+        if (g.dgpart && tid < BM) {
+            const int p = row0 + tid;
+            if (p < row_end) {
+                float sum = red_of(0)[tid];
+#pragma unroll
+                for (int w = 1; w < WAVES_N; ++w) sum = sum + red_of(w)[tid];
+                g.dgpart[(long)p * g.dg_ld + ntile] = sum;
+            }
+        }
+    } else {   // MX_DOWN, MX_DX: bf16 rows
         constexpr int LPR = WN / 8, RPP = 64 / LPR;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
@@ -384,4 +477,12 @@ hipError_t launch_gemm_mx_up(const MxGemmArgs &g, long rows, int groups, hipStre
 }
 hipError_t launch_gemm_mx_down(const MxGemmArgs &g, long rows, int groups, hipStream_t st) {
     return launch_mx_mode<MX_DOWN>(g, mx_mtiles(rows, groups), g.N / BN, st);
+}
+
+hipError_t launch_gemm_mx_dgrad(const MxGemmArgs &g, long rows, int groups, hipStream_t st) {
+    return launch_mx_mode<MX_DGRAD>(g, mx_mtiles(rows, groups), g.N / BN, st);
+}
+
+hipError_t launch_gemm_mx_dx(const MxGemmArgs &g, long rows, int groups, hipStream_t st) {
+    return launch_mx_mode<MX_DX>(g, mx_mtiles(rows, groups), g.N / BN, st);
 }

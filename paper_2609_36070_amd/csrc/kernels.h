@@ -95,14 +95,29 @@ struct MxGemmArgs {
     int K = 0, N = 0;                  // MX_UP: N = f (tile columns pair gate and up)
     const int *offsets = nullptr;      // [E+1] expert regions
     int E = 0;
-    uint8_t *C = nullptr;              // MX_UP: Hq [rows][N]
-    uint8_t *Cs = nullptr;             // MX_UP: Hs [rows][N/32]
-    uint16_t *Cb = nullptr;            // MX_DOWN: bf16 [rows][N]
+    const uint8_t *A2 = nullptr;       // MX_DX: second K half of A (dBq) and its scales
+    const uint8_t *As2 = nullptr;
+    uint8_t *C = nullptr;              // MX_UP: Hq [rows][N]; MX_DGRAD: dAq
+    uint8_t *Cs = nullptr;             // MX_UP: Hs [rows][N/32]; MX_DGRAD: dAs
+    uint8_t *C2 = nullptr;             // MX_DGRAD: dBq, dBs
+    uint8_t *Cs2 = nullptr;
+    uint16_t *Cb = nullptr;            // MX_DOWN, MX_DX: bf16 [rows][N]; MX_DGRAD: dA bf16
+    uint16_t *Cb2 = nullptr;           // MX_DGRAD: dB bf16
+    uint16_t *Cb3 = nullptr;           // MX_DGRAD: w * h bf16
+    uint16_t *Sa = nullptr;            // MX_UP: keep the gate / up pre-activations (bf16)
+    uint16_t *Sb = nullptr;
+    const uint16_t *E1 = nullptr;      // MX_DGRAD: saved pre-activations A, B (bf16)
+    const uint16_t *E2 = nullptr;
+    const float *rowscale = nullptr;   // MX_DGRAD: router weight per row
+    float *dgpart = nullptr;           // MX_DGRAD: <dh', h> partial per row and n-tile
+    int dg_ld = 0;
     uint32_t a_bytes = 0, as_bytes = 0, b_bytes = 0, bs_bytes = 0;   // operand extents (< 4 GiB)
     int tiles_m = 0;
 };
 hipError_t launch_gemm_mx_up(const MxGemmArgs &g, long rows, int groups, hipStream_t st);
 hipError_t launch_gemm_mx_down(const MxGemmArgs &g, long rows, int groups, hipStream_t st);
+hipError_t launch_gemm_mx_dgrad(const MxGemmArgs &g, long rows, int groups, hipStream_t st);
+hipError_t launch_gemm_mx_dx(const MxGemmArgs &g, long rows, int groups, hipStream_t st);
 hipError_t launch_mx_quant_rows(const uint16_t *X, long rows, int K, uint8_t *q, uint8_t *sc,
                                 hipStream_t st);
 hipError_t launch_mx_quant_weights(const uint16_t *W, int E, int K, int N, uint8_t *q, uint8_t *sc,

@@ -39,3 +39,12 @@ DEV u32x2_t e4m3_pack8(const float (&v)[8], int s) {
     const uint32_t w1 = e4m3_pair(t[4], t[5]) | (e4m3_pair(t[6], t[7]) << 16);
     return u32x2_t{w0, w1};
 }
+
+// The same for 8 values held in a vector register.
+DEV u32x2_t e4m3_pack8(const f32x8 &v, int s) {
+    const uint32_t w0 = e4m3_pair(ldexpf(v[0], -s), ldexpf(v[1], -s)) |
+                        (e4m3_pair(ldexpf(v[2], -s), ldexpf(v[3], -s)) << 16);
+    const uint32_t w1 = e4m3_pair(ldexpf(v[4], -s), ldexpf(v[5], -s)) |
+                        (e4m3_pair(ldexpf(v[6], -s), ldexpf(v[7], -s)) << 16);
+    return u32x2_t{w0, w1};
+}

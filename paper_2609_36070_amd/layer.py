@@ -74,7 +74,7 @@ class DeviceLayer:
         if nbytes == 0:
             raise ValueError(f"unsupported shape {w}")
         if mx:
-            mx_bytes = B.moe_mx_workspace_bytes(self.shape)
+            mx_bytes = B.moe_mx_workspace_bytes(self.shape, self.with_backward)
             if mx_bytes == 0:
                 raise ValueError(f"shape unsupported in MXFP8 {w}")
             nbytes = max(nbytes, mx_bytes)
@@ -108,6 +108,16 @@ class DeviceLayer:
             self.Wd_sc = torch.empty((E, d, f // 32), dtype=u8, device=dev)
             self.mx_weights = B.mx_weights_struct(self.Wg_q, self.Wu_q, self.Wd_q, self.Wg_sc,
                                                   self.Wu_sc, self.Wd_sc)
+            if self.with_backward:
+                # backward layouts: each weight row quantised along its own axis
+                self.Wg_qb = torch.empty((E, d, f), dtype=u8, device=dev)
+                self.Wu_qb = torch.empty((E, d, f), dtype=u8, device=dev)
+                self.Wd_qb = torch.empty((E, f, d), dtype=u8, device=dev)
+                self.Wg_scb = torch.empty((E, d, f // 32), dtype=u8, device=dev)
+                self.Wu_scb = torch.empty((E, d, f // 32), dtype=u8, device=dev)
+                self.Wd_scb = torch.empty((E, f, d // 32), dtype=u8, device=dev)
+                self.mx_bwd_weights = B.mx_bwd_weights_struct(self.Wg_qb, self.Wu_qb, self.Wd_qb,
+                                                              self.Wg_scb, self.Wu_scb, self.Wd_scb)
             self.quantize_mx()
 
     # -- the four calls of the path --------------------------------------
@@ -153,17 +163,28 @@ class DeviceLayer:
     def quantize_mx(self, stream=None):
         """Pre-quantise the routed weights to MXFP8 (once per weight update)."""
         B.moe_mx_quantize_weights(self.shape, self.weights, self.mx_weights, stream=stream)
+        if self.with_backward:
+            B.moe_mx_quantize_weights_bwd(self.shape, self.weights, self.mx_bwd_weights,
+                                          stream=stream)
 
-    def forward_mx(self, stream=None, events=None):
+    def forward_mx(self, stream=None, events=None, save_for_backward=None):
+        save = self.with_backward if save_for_backward is None else save_for_backward
         B.moe_forward_mx(self.shape, self.X, self.weights, self.mx_weights, self.topk_idx,
                          self.topk_w, self.plan_bufs, self.Y, self.ws, stream=stream,
-                         events=events)
+                         events=events, save_for_backward=save)
+
+    def backward_mx(self, stream=None):
+        B.moe_backward_mx(self.shape, self.dY, self.X, self.W_r, self.weights, self.mx_bwd_weights,
+                          self.topk_idx, self.topk_w, self.plan_bufs, self.dX, self.grads, self.ws,
+                          stream=stream)
 
     def step_mx(self, stream=None, fwd_events=None):
-        """Route, plan and the MXFP8 forward."""
+        """Route, plan, the MXFP8 forward (and the MXFP8 backward)."""
         self.route(stream)
         self.plan(stream)
         self.forward_mx(stream=stream, events=fwd_events)
+        if self.with_backward:
+            self.backward_mx(stream)
 
     def step(self, stream=None, fwd_events=None, bwd_events=None):
         """One pass of the whole path: route, plan, forward (and backward)."""

@@ -238,8 +238,14 @@ def test_mx_workspace_and_validation():
     for which in (B.WS_ERROR, B.WS_YEXP, B.WS_YSH, B.WS_XQ, B.WS_XS, B.WS_HQ, B.WS_HS):
         off, nb = B.moe_mx_workspace_region(sh, which)
         assert off % 256 == 0 and off + nb <= mx_bytes
-    with pytest.raises(B.MoeError):
-        B.moe_mx_workspace_region(sh, B.WS_A)
+    off, nb = B.moe_mx_workspace_region(sh, B.WS_A)               # the shared layout's regions
+    assert (off, nb) == B.moe_workspace_region(sh, True, B.WS_A)
+    mxb = B.moe_mx_workspace_bytes(sh, True)
+    assert mxb >= B.moe_workspace_bytes(sh, True) + 64 * 256 + 2 * 128 * 256
+    for which in (B.WS_DYQ, B.WS_DYS, B.WS_DAQ, B.WS_DAS, B.WS_DBQ, B.WS_DBS):
+        off, nb = B.moe_mx_workspace_region(sh, which)
+        assert off % 256 == 0 and off + nb <= mxb
+        assert off >= B.moe_workspace_bytes(sh, True)           # past every BF16 region
     assert B.moe_mx_workspace_bytes(B.make_shape(1 << 20, 4096, 8, 2, 256)) == 0   # T*d >= 2^32
     w = B.MoeWeights(None, None, None, FAKE, FAKE, FAKE)          # routed bf16 weights unused
     mx = B.MoeMxWeights(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
@@ -248,7 +254,7 @@ def test_mx_workspace_and_validation():
 
     def fwd(shape=sh, X=FAKE, weights=w, q=mx, Y=FAKE, nb=big):
         return L.moe_forward_mx(ctypes.byref(shape), X, ctypes.byref(weights), ctypes.byref(q),
-                                FAKE, FAKE, ctypes.byref(plan), Y, FAKE, nb, None, None)
+                                FAKE, FAKE, ctypes.byref(plan), Y, 0, FAKE, nb, None, None)
 
     assert fwd(nb=mx_bytes - 1) == B.MOE_ENOSPACE
     assert fwd(X=None) == B.MOE_EINVAL
@@ -263,6 +269,22 @@ def test_mx_workspace_and_validation():
                                      ctypes.byref(mx), None) == B.MOE_EINVAL
     assert L.moe_mx_quantize_weights(ctypes.byref(sh), ctypes.byref(wq),
                                      ctypes.byref(B.MoeMxWeights()), None) == B.MOE_EINVAL
+    assert L.moe_mx_quantize_weights_bwd(ctypes.byref(sh), ctypes.byref(wq),
+                                         ctypes.byref(B.MoeMxBwdWeights()), None) == B.MOE_EINVAL
+    # backward: workspace, weights and gradient checks
+    wb = B.MoeWeights(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+    qb = B.MoeMxBwdWeights(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+    g = B.MoeGrads(FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE)
+
+    def bwd(q=qb, grads=g, nb=big, dX=FAKE):
+        return L.moe_backward_mx(ctypes.byref(sh), FAKE, FAKE, FAKE, ctypes.byref(wb), ctypes.byref(q),
+                                 FAKE, FAKE, ctypes.byref(plan), dX, ctypes.byref(grads), FAKE, nb,
+                                 None)
+
+    assert bwd(nb=mxb - 1) == B.MOE_ENOSPACE
+    assert bwd(q=B.MoeMxBwdWeights(FAKE, FAKE, None, FAKE, FAKE, FAKE)) == B.MOE_EINVAL
+    assert bwd(grads=B.MoeGrads(FAKE, None, FAKE, FAKE, None, FAKE, FAKE, FAKE)) == B.MOE_EINVAL
+    assert bwd(dX=MISALIGNED) == B.MOE_EINVAL
 
 
 def test_oracle_is_not_imported_by_the_package():
