@@ -216,6 +216,11 @@ DEV void signal_done(int *ctr) {
     if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Epilogue outputs are streamed out with non-temporal stores: they are
+// read by a later launch, not by this one, and allocating them in L2 would
+// evict operand panels that concurrently running tiles still share.
+DEV void st_nt(void *p, u32x4_t v) { __builtin_nontemporal_store(v, reinterpret_cast<u32x4_t *>(p)); }
+
 template <int MODE, bool GROUPED, bool PERSISTENT = false>
 DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int *__restrict__ b_rows,
                    int vb, int nvb) {
@@ -295,10 +300,11 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
     }
 
     // ---------------- direct-load set-up ----------------
-    // Each thread issues 2 loads per operand per K step.  Load i of wave w is
-    // wave-instruction q = 2 w + i (0..15), writing 1 KB of the stage's tile.
-    //   row tile: instruction q covers rows 16 q .. 16 q + 15; lane -> row
-    //             16 q + lane / 4, physical chunk lane & 3.
+    // Each thread issues LD_PER_OP (4) loads per operand per K step.  Load i
+    // of wave w is wave-instruction q = LD_PER_OP w + i (0..31), writing 1 KB
+    // of the stage's tile.
+    //   row tile: instruction q covers rows 8 q .. 8 q + 7; lane -> row
+    //             8 q + lane / 8, physical 16-byte chunk lane & 7.
     //   col tile: instruction q covers k rows 2 q, 2 q + 1; lane -> k row
     //             2 q + lane / 32, physical 16-byte slot lane & 31.
     const uint16_t *a_row[LD_PER_OP];   // row tile: row base (+ chunk), K offset added per step
@@ -373,17 +379,41 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
     auto issue = [&](int kt, uint16_t *la, uint16_t *lb) {
         // WGRAD k rows come through the plan's token index: fetch every index
         // this K step needs first (scalar loads, one wait), then issue the
-        // direct loads.
+        // direct loads.  A wave's k rows are consecutive plan positions, so
+        // inside the expert's range they take one 4-index load per 4 rows.
         int pa[LD_PER_OP], pb[LD_PER_OP];
         if constexpr (MODE == WGRAD) {
             int ia[2 * LD_PER_OP], ib[2 * LD_PER_OP];
+            // this wave's k rows are the 2 LD_PER_OP consecutive positions from r0
+            const int r0 = kt * BK + 2 * LD_PER_OP * wave;
+            if (kt * BK + BK <= klen) {
+                // the whole step lies in the expert's range: one scalar load per operand
+                static_assert(LD_PER_OP % 2 == 0, "4-index scalar loads");
 #pragma unroll
-            for (int i = 0; i < LD_PER_OP; ++i) {
+                for (int q = 0; q < 2 * LD_PER_OP; q += 4) {
+                    if (a_rows) {
+                        const int4 v = *reinterpret_cast<const int4 *>(a_rows + kbeg + r0 + q);
+                        ia[q] = v.x; ia[q + 1] = v.y; ia[q + 2] = v.z; ia[q + 3] = v.w;
+                    } else {
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const int p = kbeg + min(kt * BK + 2 * (LD_PER_OP * wave + i) + h, klen - 1);
-                    ia[2 * i + h] = a_rows ? a_rows[p] : p;
-                    ib[2 * i + h] = b_rows ? b_rows[p] : p;
+                        for (int u = 0; u < 4; ++u) ia[q + u] = kbeg + r0 + q + u;
+                    }
+                    if (b_rows) {
+                        const int4 v = *reinterpret_cast<const int4 *>(b_rows + kbeg + r0 + q);
+                        ib[q] = v.x; ib[q + 1] = v.y; ib[q + 2] = v.z; ib[q + 3] = v.w;
+                    } else {
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) ib[q + u] = kbeg + r0 + q + u;
+                    }
+                }
+            } else {
+                // the expert's last step: positions past its end are clamped to
+                // its last row (their loads read zeros instead)
+#pragma unroll
+                for (int q = 0; q < 2 * LD_PER_OP; ++q) {
+                    const int p = kbeg + min(r0 + q, klen - 1);
+                    ia[q] = a_rows ? a_rows[p] : p;
+                    ib[q] = b_rows ? b_rows[p] : p;
                 }
             }
 #pragma unroll
@@ -547,10 +577,10 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
 #pragma unroll
                         for (int k = 0; k < 8; ++k) h[k] = silu_f(a[k]) * b[k];
                         const long o = (long)p * g.ldc + fcol0 + c;
-                        if (g.C) st_u32x4(g.C + o, pack_bf8(h));
+                        if (g.C) st_nt(g.C + o, pack_bf8(h));
                         if (g.C2) {
-                            st_u32x4(g.C2 + o, pack_bf8(a));
-                            st_u32x4(g.C3 + o, pack_bf8(b));
+                            st_nt(g.C2 + o, pack_bf8(a));
+                            st_nt(g.C3 + o, pack_bf8(b));
                         }
                     }
                 }
@@ -565,30 +595,50 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
                 const int row = lane / LPR + RPP * t, c = 8 * (lane % LPR);
                 const int p = row0 + wm * WM + 32 * i + row;
                 const f32x8 v = read8(row, c);
-                if (p < row_end) st_u32x4(g.C + (long)p * g.ldc + n0 + wn * WN + c, pack_bf8(v));
+                if (p < row_end) st_nt(g.C + (long)p * g.ldc + n0 + wn * WN + c, pack_bf8(v));
             }
         }
     } else if constexpr (MODE == BWD_DGRAD) {
         float *red = reinterpret_cast<float *>(lds_a0) + WPA * 32 * SP;  // [WAVES_N][BM]
+        // The forward's a and b (and the row's gate weight) of each 32-row
+        // group are loaded one group ahead, so their round trips overlap the
+        // previous group's work instead of each waiting in turn.  Rows past
+        // the region's end load its last row and are never stored.
+        constexpr int NP = 32 / RPP;
+        u32x4_t av[2][NP], bv[2][NP];
+        float wvs[2][NP];
+        auto fetch_ab = [&](int i, u32x4_t (&a)[NP], u32x4_t (&b)[NP], float (&wv)[NP]) {
+#pragma unroll
+            for (int t = 0; t < NP; ++t) {
+                const int row = lane / LPR + RPP * t, c = 8 * (lane % LPR);
+                const int p = min(row0 + wm * WM + 32 * i + row, row_end - 1);
+                const long o = (long)p * g.ldc + n0 + wn * WN + c;
+                a[t] = ld_u32x4(g.E1 + o);
+                b[t] = ld_u32x4(g.E2 + o);
+                wv[t] = g.rowscale ? g.rowscale[p] : 1.0f;
+            }
+        };
+        fetch_ab(0, av[0], bv[0], wvs[0]);
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
+            if (i + 1 < TM) fetch_ab(i + 1, av[(i + 1) & 1], bv[(i + 1) & 1], wvs[(i + 1) & 1]);
             stage(i);
 #pragma unroll
-            for (int t = 0; t < 32 / RPP; ++t) {
+            for (int t = 0; t < NP; ++t) {
                 const int row = lane / LPR + RPP * t, c = 8 * (lane % LPR);
                 const int rl = wm * WM + 32 * i + row;
                 const int p = row0 + rl;
                 const f32x8 dhp = read8(row, c);
                 float prod = 0.f;
                 if (p < row_end) {
-                    const float wv = g.rowscale ? g.rowscale[p] : 1.0f;
+                    const float wv = wvs[i & 1][t];
                     const long o = (long)p * g.ldc + n0 + wn * WN + c;
-                    const u32x4_t av = ld_u32x4(g.E1 + o), bv = ld_u32x4(g.E2 + o);
+                    const u32x4_t ap = av[i & 1][t], bp = bv[i & 1][t];
                     f32x8 da, db, hw;
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
-                        const float a = (k & 1) ? bf_hi(av[k >> 1]) : bf_lo(av[k >> 1]);
-                        const float b = (k & 1) ? bf_hi(bv[k >> 1]) : bf_lo(bv[k >> 1]);
+                        const float a = (k & 1) ? bf_hi(ap[k >> 1]) : bf_lo(ap[k >> 1]);
+                        const float b = (k & 1) ? bf_hi(bp[k >> 1]) : bf_lo(bp[k >> 1]);
                         const float sg = 1.0f / (1.0f + expf(-a));
                         const float sl = a * sg;
                         const float h = sl * b;
@@ -598,9 +648,9 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
                         db[k] = dh * sl;
                         hw[k] = wv * h;
                     }
-                    st_u32x4(g.C + o, pack_bf8(da));
-                    st_u32x4(g.C2 + o, pack_bf8(db));
-                    if (g.C3) st_u32x4(g.C3 + o, pack_bf8(hw));
+                    st_nt(g.C + o, pack_bf8(da));
+                    st_nt(g.C2 + o, pack_bf8(db));
+                    if (g.C3) st_nt(g.C3 + o, pack_bf8(hw));
                 }
                 // sum over the LPR lanes holding this row's WN columns (fixed butterfly order)
 #pragma unroll
@@ -636,7 +686,7 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
 #pragma unroll
                     for (int q = 0; q < 16; ++q) old[q] = o[(8 * (q >> 2) + (q & 3)) * ld];
 #pragma unroll
-                    for (int q = 0; q < 16; ++q) o[(8 * (q >> 2) + (q & 3)) * ld] = old[q] + acc[i][j][q];
+                    for (int q = 0; q < 16; ++q) __builtin_nontemporal_store(old[q] + acc[i][j][q], &o[(8 * (q >> 2) + (q & 3)) * ld]);
                 }
         } else {
 #pragma unroll
@@ -645,7 +695,7 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
                 for (int j = 0; j < TN; ++j) {
                     float *o = out + (long)(32 * i) * ld + 32 * j;
 #pragma unroll
-                    for (int q = 0; q < 16; ++q) o[(8 * (q >> 2) + (q & 3)) * ld] = acc[i][j][q];
+                    for (int q = 0; q < 16; ++q) __builtin_nontemporal_store(acc[i][j][q], &o[(8 * (q >> 2) + (q & 3)) * ld]);
                 }
         }
     }
