@@ -93,7 +93,7 @@ def measured_traffic(kernel, workload):
     """HBM bytes per launch recorded under profiles/ for this kernel and workload.
 
     Returns None unless the record was taken on the current kernel sources
-    (same hash of the csrc directory): counters of an older kernel say nothing
+    (same hash of the BF16 GEMM sources): counters of an older kernel say nothing
     about this one.
     """
     import glob
