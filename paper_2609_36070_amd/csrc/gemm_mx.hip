@@ -375,22 +375,44 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
             return reinterpret_cast<float *>(w == 0 ? sc_a0 : w == 1 ? sc_b0 : w == 2 ? sc_a1 : sc_b1);
         };
         const long fs_row = g.N / 32;
+        // The saved a, b and the row's gate weight of pass u = (i, t) are
+        // loaded PF passes ahead through a small register queue, so their
+        // round trips overlap the passes in between instead of each pass
+        // waiting for its own.  Rows past the region's end read its last row.
+        constexpr int NP = 32 / RPP, NU = TM * NP, PF = 4;
+        u32x4_t qa[PF], qb[PF];
+        float qw[PF];
+        auto fetch = [&](int u, u32x4_t &a, u32x4_t &b, float &w) {
+            const int row = lane / LPR + RPP * (u % NP), c = 8 * (lane % LPR);
+            const int pl = min(row0 + wm * WM + 32 * (u / NP) + row, row_end - 1);
+            const long o = (long)pl * g.N + n0 + wn * WN + c;
+            a = ld_u32x4(g.E1 + o);
+            b = ld_u32x4(g.E2 + o);
+            w = g.rowscale[pl];
+        };
+#pragma unroll
+        for (int q = 0; q < PF; ++q)
+            if (q < NU) fetch(q, qa[q], qb[q], qw[q]);
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             stage(i);
             // not unrolled: a body this size unrolled 8 x 4 times makes the
             // compiler keep i dynamic and the accumulators in scratch
 #pragma unroll 1
-            for (int t = 0; t < 32 / RPP; ++t) {
+            for (int t = 0; t < NP; ++t) {
+                const int u = i * NP + t;
+                const u32x4_t av = qa[0], bv = qb[0];
+                const float wv = qw[0];
+#pragma unroll
+                for (int q = 0; q + 1 < PF; ++q) { qa[q] = qa[q + 1]; qb[q] = qb[q + 1]; qw[q] = qw[q + 1]; }
+                if (u + PF < NU) fetch(u + PF, qa[PF - 1], qb[PF - 1], qw[PF - 1]);
                 const int row = lane / LPR + RPP * t, c = 8 * (lane % LPR);
                 const int rl = wm * WM + 32 * i + row;
                 const int p = row0 + rl;
                 const int pl = min(p, row_end - 1);
                 const f32x8 dhp = read8(row, c);
-                const float wv = g.rowscale[pl];
                 const int col = n0 + wn * WN + c;
                 const long o = (long)pl * g.N + col;
-                const u32x4_t av = ld_u32x4(g.E1 + o), bv = ld_u32x4(g.E2 + o);
                 f32x8 dav, dbv, hw;
                 float prod = 0.f, amax_a = 0.f, amax_b = 0.f;
 #pragma unroll
