@@ -255,6 +255,101 @@ __global__ __launch_bounds__(256) void reverse_combine_kernel(const uint16_t *__
     }
 }
 
+// The same sum for a small expert count (E = 8 EG, EG <= 2): one thread owns
+// an 8-column chunk of dX for a group of tokens and keeps the 8 x E router
+// weights of its chunk in registers, so W_r is read once per group instead of
+// once per token; dZ rows are uniform loads.  The arithmetic and its order
+// are those of reverse_combine_kernel, so the results are identical.
+constexpr int RC_TG = 8;      // tokens per block
+constexpr int RC_BT = 128;    // threads per block, one column chunk each
+
+template <int EG>
+__global__ __launch_bounds__(RC_BT) void reverse_combine_small_e_kernel(
+        const uint16_t *__restrict__ dXperm, const uint16_t *__restrict__ dXsh,
+        const float *__restrict__ dZ, const uint16_t *__restrict__ Wr,
+        const int *__restrict__ route_pos, int T, int d, int k, int R,
+        const float *__restrict__ dXacc, uint16_t *__restrict__ dX) {
+    constexpr int E = 8 * EG;
+    const int nc = d / 8;
+    const int c = blockIdx.y * RC_BT + threadIdx.x;
+    if (c >= nc) return;   // nothing below synchronises the block
+    u32x4_t w[8][EG];
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+#pragma unroll
+        for (int g = 0; g < EG; ++g) w[q][g] = ld_u32x4(Wr + (long)(8 * c + q) * E + 8 * g);
+    const int t0 = blockIdx.x * RC_TG;
+    const int t1 = min(T, t0 + RC_TG);
+    for (int t = t0; t < t1; ++t) {
+        float dz[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) dz[e] = dZ[(long)t * E + e];
+        float acc[8];
+        if (dXacc) {
+            const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(dXacc + (long)t * d + 8 * c);
+            const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(dXacc + (long)t * d + 8 * c + 4);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                acc[q] = lo[q];
+                acc[4 + q] = hi[q];
+            }
+        } else {
+            int pos[16];
+#pragma unroll
+            for (int s2 = 0; s2 < 16; ++s2) {
+                pos[s2] = -1;
+                if (s2 < k) {
+                    const int p = route_pos[(long)t * k + s2];
+                    pos[s2] = (p >= 0 && p < R) ? p : -1;
+                }
+            }
+            u32x4_t rows[16];
+#pragma unroll
+            for (int s2 = 0; s2 < 16; ++s2)
+                if (s2 < k) rows[s2] = ld_u32x4(dXperm + (long)max(pos[s2], 0) * d + 8 * c);
+            if (dXsh) {
+                const u32x4_t v = ld_u32x4(dXsh + (long)t * d + 8 * c);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    acc[2 * q] = bf_lo(v[q]);
+                    acc[2 * q + 1] = bf_hi(v[q]);
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+            }
+#pragma unroll
+            for (int s2 = 0; s2 < 16; ++s2) {
+                if (s2 < k && pos[s2] >= 0) {
+                    const u32x4_t v = rows[s2];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        acc[2 * q] = acc[2 * q] + bf_lo(v[q]);
+                        acc[2 * q + 1] = acc[2 * q + 1] + bf_hi(v[q]);
+                    }
+                }
+            }
+        }
+        float racc[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            racc[q] = 0.f;
+#pragma unroll
+            for (int g = 0; g < EG; ++g)
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    racc[q] = racc[q] + dz[8 * g + 2 * h] * bf_lo(w[q][g][h]);
+                    racc[q] = racc[q] + dz[8 * g + 2 * h + 1] * bf_hi(w[q][g][h]);
+                }
+        }
+        u32x4_t o;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            o[q] = pack_bf2(acc[2 * q] + racc[2 * q], acc[2 * q + 1] + racc[2 * q + 1]);
+        st_u32x4(dX + (long)t * d + 8 * c, o);
+    }
+}
+
 // Bounded-memory execution: per-route rows of the positions [w0, w1) live in
 // a ring (row p at ring row p - w0).  For every token, the routes that fall
 // in the window are added to an fp32 per-token accumulator in ascending slot
@@ -343,46 +438,73 @@ __global__ __launch_bounds__(256) void clip_offsets_kernel(const int *__restrict
     for (int e = threadIdx.x; e <= E; e += 256) out[e] = min(max(offsets[e], w0), w1);
 }
 
-// dW_r = X^T dZ in two fixed-order stages.  Stage 1: block (column block,
-// token chunk) -> part[chunk][i][e]; stage 2 sums the chunks in order.
-constexpr int DWR_TC = 256;   // tokens per chunk
-constexpr int DWR_EG = 16;    // experts per register group
+// dW_r = X^T dZ in two fixed-order stages.  Stage 1: block (512-column
+// block, chunk of 256 tokens) -> part[chunk][i][e]; within the block each
+// wave sums 64 consecutive tokens for 8 columns per lane and 8 experts at a
+// time, and the 4 waves' sums are added in wave order.  Stage 2 sums the
+// chunks in order.
+constexpr int DWR_TC = 256;   // tokens per chunk (4 waves x 64)
+constexpr int DWR_TW = 64;    // tokens per wave
+constexpr int DWR_CB = 512;   // columns per block (64 lanes x 8)
+constexpr int DWR_TB = 8;     // token rows loaded together
 
 __global__ __launch_bounds__(256) void dwr_partial_kernel(const uint16_t *__restrict__ X,
                                                           const float *__restrict__ dZ, int T,
                                                           int d, int E,
                                                           float *__restrict__ part) {
-    __shared__ float dzs[DWR_TC][DWR_EG];
-    const int i = (blockIdx.x * 256 + threadIdx.x) * 2;  // two columns per thread
+    __shared__ float red[4][64 * 65];   // [wave][lane * 65 + 8 column + expert], padded rows
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int i0 = blockIdx.x * DWR_CB + 8 * lane;
     const int ch = blockIdx.y;
-    const int t0 = ch * DWR_TC;
-    const int t1 = min(T, t0 + DWR_TC);
-    for (int e0 = 0; e0 < E; e0 += DWR_EG) {
-        __syncthreads();
-        for (int q = threadIdx.x; q < DWR_TC * DWR_EG; q += 256) {
-            const int tt = q / DWR_EG, ee = q % DWR_EG;
-            dzs[tt][ee] = (t0 + tt < t1 && e0 + ee < E) ? dZ[(long)(t0 + tt) * E + e0 + ee] : 0.f;
-        }
-        __syncthreads();
-        float a0[DWR_EG], a1[DWR_EG];
+    const int tw0 = ch * DWR_TC + wave * DWR_TW;
+    const int tw1 = min(T, tw0 + DWR_TW);
+    const bool col_ok = i0 < d;
+    for (int e0 = 0; e0 < E; e0 += 8) {
+        float acc[8][8];   // [column][expert]
 #pragma unroll
-        for (int ee = 0; ee < DWR_EG; ++ee) { a0[ee] = 0.f; a1[ee] = 0.f; }
-        if (i < d) {
-            for (int t = t0; t < t1; ++t) {
-                const uint32_t xv = *reinterpret_cast<const uint32_t *>(X + (long)t * d + i);
-                const float x0 = bf_lo(xv), x1 = bf_hi(xv);
+        for (int c = 0; c < 8; ++c)
 #pragma unroll
-                for (int ee = 0; ee < DWR_EG; ++ee) {
-                    a0[ee] = a0[ee] + x0 * dzs[t - t0][ee];
-                    a1[ee] = a1[ee] + x1 * dzs[t - t0][ee];
-                }
+            for (int e = 0; e < 8; ++e) acc[c][e] = 0.f;
+        for (int tb = tw0; tb < tw1; tb += DWR_TB) {
+            u32x4_t xv[DWR_TB];
+#pragma unroll
+            for (int u = 0; u < DWR_TB; ++u) {
+                const int t = min(tb + u, tw1 - 1);
+                xv[u] = col_ok ? ld_u32x4(X + (long)t * d + i0) : u32x4_t{0, 0, 0, 0};
             }
 #pragma unroll
-            for (int ee = 0; ee < DWR_EG; ++ee) {
-                if (e0 + ee < E) {
-                    part[((long)ch * d + i) * E + e0 + ee] = a0[ee];
-                    part[((long)ch * d + i + 1) * E + e0 + ee] = a1[ee];
+            for (int u = 0; u < DWR_TB; ++u) {
+                if (tb + u < tw1) {
+                    const int t = tb + u;
+                    float dz[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) dz[e] = e0 + e < E ? dZ[(long)t * E + e0 + e] : 0.f;
+#pragma unroll
+                    for (int h = 0; h < 4; ++h) {
+                        const float x0 = bf_lo(xv[u][h]), x1 = bf_hi(xv[u][h]);
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            acc[2 * h][e] = acc[2 * h][e] + x0 * dz[e];
+                            acc[2 * h + 1][e] = acc[2 * h + 1][e] + x1 * dz[e];
+                        }
+                    }
                 }
+            }
+        }
+        __syncthreads();   // the previous expert group's reads of red are done
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) red[wave][lane * 65 + 8 * c + e] = acc[c][e];
+        __syncthreads();
+        // 4096 sums of this block: entry q = 64 lane + 8 c + e, wave order fixed
+        for (int q = threadIdx.x; q < 64 * 64; q += 256) {
+            const int l = q >> 6, c = (q >> 3) & 7, e = q & 7;
+            const int i = blockIdx.x * DWR_CB + 8 * l + c;
+            if (i < d && e0 + e < E) {
+                const int r = l * 65 + 8 * c + e;
+                part[((long)ch * d + i) * E + e0 + e] = red[0][r] + red[1][r] + red[2][r] + red[3][r];
             }
         }
     }
@@ -441,6 +563,16 @@ hipError_t launch_reverse_combine(const uint16_t *dXperm, const uint16_t *dXsh, 
                                   const uint16_t *W_r, const int *route_pos, int T, int d, int k,
                                   int E, const float *dXacc, uint16_t *dX, hipStream_t st) {
     if (T == 0) return hipSuccess;
+    if (E == 8 || E == 16) {
+        const dim3 grid((unsigned)((T + RC_TG - 1) / RC_TG), (unsigned)((d / 8 + RC_BT - 1) / RC_BT));
+        if (E == 8)
+            reverse_combine_small_e_kernel<1><<<grid, dim3(RC_BT), 0, st>>>(
+                dXperm, dXsh, dZ, W_r, route_pos, T, d, k, T * k, dXacc, dX);
+        else
+            reverse_combine_small_e_kernel<2><<<grid, dim3(RC_BT), 0, st>>>(
+                dXperm, dXsh, dZ, W_r, route_pos, T, d, k, T * k, dXacc, dX);
+        return hipGetLastError();
+    }
     reverse_combine_kernel<<<dim3(rows_grid(T)), dim3(256), 0, st>>>(dXperm, dXsh, dZ, W_r, route_pos,
                                                                       T, d, k, E, T * k, dXacc, dX);
     return hipGetLastError();
@@ -465,7 +597,7 @@ hipError_t launch_dwr(const uint16_t *X, const float *dZ, int T, int d, int E, f
     const int nch = dwr_nchunks(T);
     const long n = (long)d * E;
     if (nch > 0) {
-        dim3 grid((unsigned)((d / 2 + 255) / 256), (unsigned)nch);
+        dim3 grid((unsigned)((d + DWR_CB - 1) / DWR_CB), (unsigned)nch);
         dwr_partial_kernel<<<grid, dim3(256), 0, st>>>(X, dZ, T, d, E, part);
     }
     dwr_reduce_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st>>>(part, nch, n, dWr);

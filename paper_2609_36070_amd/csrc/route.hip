@@ -46,23 +46,42 @@ __global__ __launch_bounds__(256) void route_kernel(const uint16_t *__restrict__
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+    // CU chunks per pass: all their loads first, then the MFMAs in chunk
+    // order (so the sums are those of one chunk at a time)
+    constexpr int CU = NT <= 2 ? 4 : NT <= 4 ? 2 : 1;
     const int nchunks = d / 64;
-    for (int c = w; c < nchunks; c += 4) {
-        const int kb = c * 64 + 16 * g;
-        u32x4_t a0 = {0, 0, 0, 0}, a1 = {0, 0, 0, 0};
-        if (tok_ok) {
-            a0 = ld_u32x4(xrow + kb);
-            a1 = ld_u32x4(xrow + kb + 8);
+    for (int c0 = w; c0 < nchunks; c0 += 4 * CU) {
+        u32x4_t a0[CU], a1[CU], b0[CU][NT], b1[CU][NT];
+#pragma unroll
+        for (int u = 0; u < CU; ++u) {
+            const int c = c0 + 4 * u;
+            const int kb = min(c, nchunks - 1) * 64 + 16 * g;
+            a0[u] = u32x4_t{0, 0, 0, 0};
+            a1[u] = u32x4_t{0, 0, 0, 0};
+            if (tok_ok && c < nchunks) {
+                a0[u] = ld_u32x4(xrow + kb);
+                a1[u] = ld_u32x4(xrow + kb + 8);
+            }
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                const uint16_t *wrow = WrT + (long)(16 * nt + r) * d + kb;
+                b0[u][nt] = ld_u32x4(wrow);
+                b1[u][nt] = ld_u32x4(wrow + 8);
+            }
         }
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-            const uint16_t *wrow = WrT + (long)(16 * nt + r) * d + kb;
-            u32x4_t b0 = ld_u32x4(wrow);
-            u32x4_t b1 = ld_u32x4(wrow + 8);
-            acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8_t, a0), __builtin_bit_cast(bf16x8_t, b0), acc[nt], 0, 0, 0);
-            acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8_t, a1), __builtin_bit_cast(bf16x8_t, b1), acc[nt], 0, 0, 0);
+        for (int u = 0; u < CU; ++u) {
+            if (c0 + 4 * u < nchunks) {
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) {
+                    acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8_t, a0[u]), __builtin_bit_cast(bf16x8_t, b0[u][nt]),
+                        acc[nt], 0, 0, 0);
+                    acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8_t, a1[u]), __builtin_bit_cast(bf16x8_t, b1[u][nt]),
+                        acc[nt], 0, 0, 0);
+                }
+            }
         }
     }
     // 16x16 accumulator layout: lane (g, r) register q holds row 4g+q, column r.
