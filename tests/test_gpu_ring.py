@@ -77,6 +77,8 @@ def test_ring_parity(ring_rows):
     (Workload("k_equals_E", T=300, d=256, E=4, k=4, f=512, bias_std=0.5, backward=True), 256),
     (Workload("empty_experts", T=40, d=256, E=64, k=1, f=256, bias_std=3.0, backward=True), 16),
     (Workload("many_tiles", T=700, d=768, E=3, k=2, f=768, backward=True), 600),
+    (Workload("sixteen_experts", T=333, d=768, E=16, k=5, f=256, f_s=256, bias_std=0.5,
+              backward=True), 500),
 ], ids=lambda v: v.name if isinstance(v, Workload) else str(v))
 def test_ring_edge_shapes(w, ring_rows):
     full, ring, inp = run_pair(w, ring_rows, seed=12)

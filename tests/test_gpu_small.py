@@ -68,6 +68,12 @@ def test_ragged_forward_backward():
     Workload("k_equals_E", T=300, d=256, E=4, k=4, f=512, bias_std=0.5, backward=True),
     Workload("empty_experts", T=40, d=256, E=64, k=1, f=256, bias_std=3.0, backward=True),
     Workload("many_tiles", T=700, d=768, E=3, k=2, f=768, backward=True),
+    # the small-expert-count reverse combine: 16 experts with a token count
+    # that leaves a partial token group and a partial 128-chunk column block;
+    # 8 experts over two column blocks, the second partial
+    Workload("sixteen_experts", T=333, d=768, E=16, k=5, f=256, f_s=256, bias_std=0.5,
+             backward=True),
+    Workload("eight_experts_wide", T=77, d=1280, E=8, k=2, f=256, bias_std=0.5, backward=True),
 ], ids=lambda w: w.name)
 def test_edge_shapes(w):
     L, inp, Zo, idx_g, w_orc = forward_parity(w, seed=2)
