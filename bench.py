@@ -431,46 +431,47 @@ def main():
     log(f"[bench] {args.warmup} warm-up steps done")
 
     nf, nb = len(B.FWD_STAGES) + 1, len(B.BWD_STAGES) + 1
-    per_step = []
-    for _ in range(args.steps):
-        ev = {"route": H.create(), "plan": H.create(),
-              "fwd": [H.create() for _ in range(nf)],
-              "bwd": [H.create() for _ in range(nb)] if w.backward else [],
-              "end": H.create()}
-        per_step.append(ev)
-    t_start, t_stop = H.create(), H.create()
 
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    H.record(t_start, stream)
-    for ev in per_step:
-        fe = B.MoeStageEvents()
-        for i, e in enumerate(ev["fwd"]):
-            fe.ev[i] = e
-        be = None
-        if w.backward:
-            be = B.MoeStageEvents()
-            for i, e in enumerate(ev["bwd"]):
+    def run_steps(n, fwd_slots, bwd_slots, stage_marks):
+        """n steps; events at the listed forward / backward stage boundaries
+        (and, with stage_marks, before route, plan and after each step).
+        Returns the events and the total GPU time of the n steps."""
+        evs = []
+        for _ in range(n):
+            evs.append({"route": H.create() if stage_marks else None,
+                        "plan": H.create() if stage_marks else None,
+                        "fwd": {i: H.create() for i in fwd_slots},
+                        "bwd": {i: H.create() for i in bwd_slots} if w.backward else {}})
+        t0, t1 = H.create(), H.create()
+        torch.cuda.synchronize()
+        H.record(t0, stream)
+        for ev in evs:
+            fe = B.MoeStageEvents() if ev["fwd"] else None
+            for i, e in ev["fwd"].items():
+                fe.ev[i] = e
+            be = B.MoeStageEvents() if ev["bwd"] else None
+            for i, e in ev["bwd"].items():
                 be.ev[i] = e
-        H.record(ev["route"], stream)
-        L.route()
-        H.record(ev["plan"], stream)
-        L.plan()
-        L.forward(events=fe)
-        if w.backward:
-            L.backward(events=be)
-        H.record(ev["end"], stream)
-    H.record(t_stop, stream)
-    H.sync(t_stop)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    ms_total = H.ms(t_start, t_stop)
-    ms_step = ms_total / args.steps
-    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step (events), wall {1e3 * wall / args.steps:.3f}")
+            if stage_marks:
+                H.record(ev["route"], stream)
+            L.route()
+            if stage_marks:
+                H.record(ev["plan"], stream)
+            L.plan()
+            L.forward(events=fe)
+            if w.backward:
+                L.backward(events=be)
+        H.record(t1, stream)
+        H.sync(t1)
+        torch.cuda.synchronize()
+        return evs, H.ms(t0, t1)
 
-    # per-stage averages
+    # Per-stage breakdown, from steps with an event at every stage boundary.
+    # Each recorded event leaves the GPU idle for a few microseconds, so
+    # these steps are not the timed ones.
+    staged, _ = run_steps(max(2, min(5, args.steps)), range(nf), range(nb) if w.backward else [], True)
     stages = {"route": 0.0, "plan": 0.0}
-    for ev in per_step:
+    for ev in staged:
         stages["route"] += H.ms(ev["route"], ev["plan"])
         stages["plan"] += H.ms(ev["plan"], ev["fwd"][0])
         for i, name in enumerate(B.FWD_STAGES):
@@ -478,22 +479,41 @@ def main():
         if w.backward:
             for i, name in enumerate(B.BWD_STAGES):
                 stages["bwd." + name] = stages.get("bwd." + name, 0.0) + H.ms(ev["bwd"][i], ev["bwd"][i + 1])
-    stages = {k: v / args.steps for k, v in stages.items()}
+    stages = {k: v / len(staged) for k, v in stages.items()}
 
     fwd_fl, bwd_fl = stage_flops(w)
-    # kernels that run as exactly one instance per launch shape, with their FLOPs per launch
+    # kernels that run as exactly one instance per launch shape: (phase, first
+    # stage, end stage, launches, FLOPs per launch)
+    fi, bi = B.FWD_STAGES.index, B.BWD_STAGES.index
     kern = {
-        "gemm up/gate+SwiGLU (routed)": (stages["fwd.up_routed"], 1, fwd_fl["up_routed"][0]),
-        "gemm down (routed)": (stages["fwd.down_routed"], 1, fwd_fl["down_routed"][0]),
+        "gemm up/gate+SwiGLU (routed)": ("fwd", fi("up_routed"), fi("up_routed") + 1, 1,
+                                         fwd_fl["up_routed"][0]),
+        "gemm down (routed)": ("fwd", fi("down_routed"), fi("down_routed") + 1, 1,
+                               fwd_fl["down_routed"][0]),
     }
     if w.backward:
-        kern["gemm dgrad+SwiGLU bwd (routed)"] = (stages["bwd.dgrad_routed"], 1,
+        kern["gemm dgrad+SwiGLU bwd (routed)"] = ("bwd", bi("dgrad_routed"), bi("dgrad_routed") + 1, 1,
                                                   bwd_fl["dgrad_routed"][0])
-        kern["gemm dX (routed)"] = (stages["bwd.dx_routed"], 1, bwd_fl["dx_routed"][0])
-        kern["gemm weight grad (routed)"] = (stages["bwd.wgrad_gate_up"] + stages["bwd.wgrad_down"],
-                                             3, 2.0 * w.T * w.k * w.d * w.f)
-    dom = max(kern, key=lambda k: kern[k][0])
-    t_ms, n_launch, fl = kern[dom]
+        kern["gemm dX (routed)"] = ("bwd", bi("dx_routed"), bi("dx_routed") + 1, 1,
+                                    bwd_fl["dx_routed"][0])
+        kern["gemm weight grad (routed)"] = ("bwd", bi("wgrad_gate_up"), bi("wgrad_down") + 1, 3,
+                                             2.0 * w.T * w.k * w.d * w.f)
+
+    def stage_span(k):
+        ph, i0, i1 = kern[k][:3]
+        names = B.FWD_STAGES if ph == "fwd" else B.BWD_STAGES
+        return sum(stages[ph + "." + names[i]] for i in range(i0, i1))
+
+    dom = max(kern, key=stage_span)
+    ph, i0, i1, n_launch, fl = kern[dom]
+
+    # Timed steps: events only around the dominant kernel.
+    slots = [i0, i1]
+    timed, ms_total = run_steps(args.steps, slots if ph == "fwd" else [],
+                                slots if ph == "bwd" else [], False)
+    ms_step = ms_total / args.steps
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step (events)")
+    t_ms = sum(H.ms(ev[ph][i0], ev[ph][i1]) for ev in timed) / args.steps
     avg_ms = t_ms / n_launch
     achieved = fl / (avg_ms * 1e-3) / 1e12
     roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
