@@ -216,6 +216,9 @@ DEV void signal_done(int *ctr) {
     if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Four consecutive plan indices; plan positions carry no alignment beyond 4 bytes.
+typedef int idx4_t __attribute__((ext_vector_type(4), aligned(4)));
+
 // Epilogue outputs are streamed out with non-temporal stores: they are
 // read by a later launch, not by this one, and allocating them in L2 would
 // evict operand panels that concurrently running tiles still share.
@@ -392,15 +395,15 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
 #pragma unroll
                 for (int q = 0; q < 2 * LD_PER_OP; q += 4) {
                     if (a_rows) {
-                        const int4 v = *reinterpret_cast<const int4 *>(a_rows + kbeg + r0 + q);
-                        ia[q] = v.x; ia[q + 1] = v.y; ia[q + 2] = v.z; ia[q + 3] = v.w;
+                        const idx4_t v = *reinterpret_cast<const idx4_t *>(a_rows + kbeg + r0 + q);
+                        ia[q] = v[0]; ia[q + 1] = v[1]; ia[q + 2] = v[2]; ia[q + 3] = v[3];
                     } else {
 #pragma unroll
                         for (int u = 0; u < 4; ++u) ia[q + u] = kbeg + r0 + q + u;
                     }
                     if (b_rows) {
-                        const int4 v = *reinterpret_cast<const int4 *>(b_rows + kbeg + r0 + q);
-                        ib[q] = v.x; ib[q + 1] = v.y; ib[q + 2] = v.z; ib[q + 3] = v.w;
+                        const idx4_t v = *reinterpret_cast<const idx4_t *>(b_rows + kbeg + r0 + q);
+                        ib[q] = v[0]; ib[q + 1] = v[1]; ib[q + 2] = v[2]; ib[q + 3] = v[3];
                     } else {
 #pragma unroll
                         for (int u = 0; u < 4; ++u) ib[q + u] = kbeg + r0 + q + u;
