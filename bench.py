@@ -377,8 +377,8 @@ def main():
                          "kernel for scaling HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no "
-              f"multi-GPU path.", file=sys.stderr)
+        print(f"bench.py measures one GPU's share of the layer only (got --gpus {args.gpus}); "
+              f"there is no multi-GPU path.", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -1,0 +1,47 @@
+"""Host-side logic of bench.py (CPU only, no GPU)."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+import bench
+from paper_2609_36070_amd.workloads import WORKLOADS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.mark.parametrize("n", [2, 8])
+def test_more_than_one_gpu_is_refused_before_any_gpu_work(n):
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", str(n)],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""          # no JSON line
+
+
+@pytest.mark.parametrize("name", ["large_shared_train", "tiny"])
+def test_stage_flops_add_up_to_the_step_convention(name):
+    """The per-stage FLOPs (used for the per-stage rates and the roofline)
+    partition the step's 6 T (k f + f_s) d forward and twice that backward."""
+    w = WORKLOADS[name]
+    fwd, bwd = bench.stage_flops(w)
+    assert sum(v[0] for v in fwd.values()) == pytest.approx(w.fwd_flops(), rel=1e-12)
+    assert sum(v[0] for v in bwd.values()) == pytest.approx(2.0 * w.fwd_flops(), rel=1e-12)
+
+
+def test_traffic_record_is_reported_only_for_the_current_sources(monkeypatch):
+    recs = [p for p in os.listdir(os.path.join(ROOT, "profiles")) if p.startswith("traffic_")]
+    assert recs, "a traffic record is committed under profiles/"
+    with open(os.path.join(ROOT, "profiles", recs[0])) as fh:
+        rec = json.load(fh)
+    for key in ("kernel", "workload", "read_bytes_per_launch", "write_bytes_per_launch",
+                "fetch_scale", "write_scale", "source_sha256", "commands"):
+        assert key in rec, key
+    monkeypatch.setattr(bench, "source_sha256", lambda: rec["source_sha256"])
+    got = bench.measured_traffic(rec["kernel"], rec["workload"])
+    assert got == rec["read_bytes_per_launch"] + rec["write_bytes_per_launch"]
+    monkeypatch.setattr(bench, "source_sha256", lambda: "0" * 64)
+    assert bench.measured_traffic(rec["kernel"], rec["workload"]) is None
+    assert bench.measured_traffic("no such kernel", rec["workload"]) is None
