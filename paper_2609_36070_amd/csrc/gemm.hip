@@ -862,6 +862,8 @@ struct FusedFwd {
 
 __shared__ int s_ticket;
 __shared__ int s_tilebase[257];
+__shared__ int s_cpos[FUSED_TB * 16];     // combine item: route positions (-1: none)
+__shared__ float s_cwt[FUSED_TB * 16];    // and gate weights, [token][slot]
 
 DEV void fused_combine(const FusedFwd &fa, int blk) {
     const int t0 = blk * FUSED_TB;
@@ -874,6 +876,9 @@ DEV void fused_combine(const FusedFwd &fa, int blk) {
     if (tid < npairs) {
         const long j = (long)t0 * fa.k + tid;
         const int p = fa.route_pos[j], e = fa.topk_idx[j];
+        // the item's positions and weights, read once for all its column chunks
+        s_cpos[tid] = (p >= 0 && p < fa.R) ? p : -1;
+        s_cwt[tid] = fa.topk_w[j];
         if (p >= 0 && p < fa.R && e >= 0 && e < fa.E)
             poll_count(fa.down_done_r + s_tilebase[e] + (p - fa.offsets[e]) / BM, fa.need_r, fa.err);
     } else if (fa.Ysh && tid < npairs + 2) {
@@ -900,9 +905,8 @@ DEV void fused_combine(const FusedFwd &fa, int blk) {
                 pos[h][s] = -1;
                 wt[h][s] = 0.f;
                 if (s < fa.k) {
-                    const int p = fa.route_pos[(long)tt[h] * fa.k + s];
-                    pos[h][s] = (p >= 0 && p < fa.R) ? p : -1;
-                    wt[h][s] = fa.topk_w[(long)tt[h] * fa.k + s];
+                    pos[h][s] = s_cpos[(tt[h] - t0) * fa.k + s];
+                    wt[h][s] = s_cwt[(tt[h] - t0) * fa.k + s];
                 }
             }
         }
