@@ -181,6 +181,20 @@ def moe_forward_mx(X, W, idx, w):
 
 
 
+def mx_qdq_token_blocks(v):
+    """One expert's rows (in its plan order) after an MXFP8 round trip along
+    the token axis: blocks of 32 consecutive rows from the expert's first row,
+    one scale per column of a block; the last block is completed with zero
+    rows (which leave its maximum unchanged) that are dropped again."""
+    v = np.asarray(v, F64)
+    n = v.shape[0]
+    if n == 0:
+        return v
+    pad = (-n) % BLOCK
+    vp = np.concatenate([v, np.zeros((pad,) + v.shape[1:], F64)], axis=0)
+    return mx_qdq(vp, 0)[:n]
+
+
 def bf16_round(v):
     """Round to the nearest bfloat16 (8 significand bits), ties to even, via
     float32 (the GPU rounds its fp32 results the same way)."""
@@ -189,7 +203,7 @@ def bf16_round(v):
     return b.astype(np.uint32).view(np.float32).astype(F64)
 
 
-def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True):
+def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True, wgrad_mx=False):
     """Backward of the layer with MXFP8 routed experts (teacher-forced on idx, w).
 
     Readings (§3.4 "MXFP8 Support" names MXFP8 training and fused activation
@@ -210,6 +224,14 @@ def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True):
       (the gradient passes straight through the quantiser);
     * the router-weight gradient, the softmax backward, dW_r, the shared expert
       (BF16) and dX's router term are those of the BF16 backward.
+
+    With wgrad_mx (the opt-in MXFP8 weight gradients), the weight-gradient
+    products run in MXFP8 too.  They contract over the expert's tokens, so
+    each operand is quantised along the token axis, per expert
+    (mx_qdq_token_blocks): X and dY as given, and dA, dB, w h in bf16, as
+    they are stored between the two backward GEMM stages:
+      dW_gate = Q_t(X_e)^T Q_t(dA_e), dW_up = Q_t(X_e)^T Q_t(dB_e),
+      dW_down = Q_t(w h)^T Q_t(dY_e).
 
     quant=False replaces every quantise-dequantise by the identity, which must
     reproduce moe_oracle.moe_backward.
@@ -245,9 +267,15 @@ def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True):
         dh = we * dhp
         dA = dh * b * O._dsilu(a)
         dB = dh * O.silu(a)
-        dWg[e] = X[ts].T @ dA
-        dWu[e] = X[ts].T @ dB
-        dWd[e] = (we * h).T @ dY[ts]
+        if quant and wgrad_mx:
+            xt = mx_qdq_token_blocks(X[ts])
+            dWg[e] = xt.T @ mx_qdq_token_blocks(bf16_round(dA))
+            dWu[e] = xt.T @ mx_qdq_token_blocks(bf16_round(dB))
+            dWd[e] = mx_qdq_token_blocks(bf16_round(we * h)).T @ mx_qdq_token_blocks(dY[ts])
+        else:
+            dWg[e] = X[ts].T @ dA
+            dWu[e] = X[ts].T @ dB
+            dWd[e] = (we * h).T @ dY[ts]
         np.add.at(dX, ts, qdq(dA, 1) @ qdq(Wg, 1).T + qdq(dB, 1) @ qdq(Wu, 1).T)
     dz_sel = O.softmax_restricted_backward(np.asarray(w, F64), dg)
     dZ = np.zeros((T, W_r.shape[1]), F64)
@@ -326,9 +354,10 @@ def mx_token_backward(X, W_r, W, idx, w, dY, tokens):
     return dX, dZ, dg
 
 
-def mx_expert_weight_grad_columns(X, W, idx, w, dY, e, cols):
+def mx_expert_weight_grad_columns(X, W, idx, w, dY, e, cols, wgrad_mx=False):
     """dW_gate[e][:, cols], dW_up[e][:, cols] and dW_down[e][cols, :] of
-    moe_backward_mx."""
+    moe_backward_mx (token-axis blocks are per column, so the selected
+    columns need only their own operand columns)."""
     X = np.asarray(X, F64)
     dY = np.asarray(dY, F64)
     ts, ss = np.nonzero(np.asarray(idx) == e)
@@ -344,4 +373,9 @@ def mx_expert_weight_grad_columns(X, W, idx, w, dY, e, cols):
     dA = dh * b * O._dsilu(a)
     dB = dh * O.silu(a)
     h = O.silu(a) * b
+    if wgrad_mx:
+        qt = mx_qdq_token_blocks
+        xt = qt(X[ts])
+        return (xt.T @ qt(bf16_round(dA)), xt.T @ qt(bf16_round(dB)),
+                qt(bf16_round(we * h)).T @ qt(dY[ts]))
     return X[ts].T @ dA, X[ts].T @ dB, (we * h).T @ dY[ts]
