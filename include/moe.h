@@ -124,7 +124,18 @@ typedef enum {
     MOE_WS_DAS = 17,    /* E8M0 [T*k, f/32]                                 */
     MOE_WS_DBQ = 18,    /* E4M3 [T*k, f]  gradient wrt B                    */
     MOE_WS_DBS = 19,    /* E8M0 [T*k, f/32]                                 */
-    MOE_WS_COUNT = 20
+    /* MXFP8 weight gradients only (moe_backward_mx with wgrad_mxfp8 = 1).
+     * Expert e's plan rows sit at padded positions [poff[e], poff[e] + count)
+     * of a token axis of P = roundup(T*k + 128 E, 128) positions; poff[e] is
+     * a multiple of 128, and positions past an expert's rows hold zeros. */
+    MOE_WS_POFF = 20,   /* int32 [E+1]    padded expert offsets             */
+    MOE_WS_XTQ = 21,    /* E4M3 [d, P]    X^T by token, 32-blocks along P   */
+    MOE_WS_XTS = 22,    /* E8M0 [d, P/32]                                   */
+    MOE_WS_DYTQ = 23,   /* E4M3 [d, P]    dY^T likewise                     */
+    MOE_WS_DYTS = 24,   /* E8M0 [d, P/32]                                   */
+    /* Backward (either layout): */
+    MOE_WS_HW = 25,     /* bf16 [T*k, f]  gate weight times silu(A) * B     */
+    MOE_WS_COUNT = 26
 } moe_ws_tensor;
 
 /* MXFP8 routed-expert weights (§3.4 "MXFP8 Support"), written once by
@@ -235,13 +246,15 @@ moe_status moe_mx_quantize_weights(const moe_shape *shape, const moe_weights *we
                                    const moe_mx_weights *mx, moe_stream stream);
 
 /* Workspace bytes of moe_forward_mx (with_backward = 0; it also serves
- * moe_route and moe_plan) or of moe_forward_mx with save_for_backward = 1
- * followed by moe_backward_mx (with_backward = 1); 0 for an invalid or
- * unsupported shape.  Pure host function. */
+ * moe_route and moe_plan), of moe_forward_mx with save_for_backward = 1
+ * followed by moe_backward_mx (with_backward = 1), or of the same with the
+ * MXFP8 weight gradients (with_backward = 2; adds the token-axis operands,
+ * (2 d + 3 f) P bytes of codes and 1/32 of that of scales, P as for
+ * MOE_WS_POFF); 0 for an invalid or unsupported shape.  Pure host function. */
 size_t moe_mx_workspace_bytes(const moe_shape *shape, int with_backward);
 
 /* Byte offset and size of a region of the MXFP8 workspace: the MXFP8 regions
- * MOE_WS_XQ .. MOE_WS_DBS, or any region of moe_workspace_region's
+ * MOE_WS_XQ .. MOE_WS_DYTS, or any region of moe_workspace_region's
  * backward layout (the MXFP8 paths use it for the rest). */
 moe_status moe_mx_workspace_region(const moe_shape *shape, moe_ws_tensor which, size_t *offset,
                                    size_t *bytes);
@@ -292,17 +305,26 @@ moe_status moe_forward_mx(const moe_shape *shape, const moe_bf16 *X, const moe_w
  *   - the gated-activation backward in that GEMM's epilogue writes dA, dB
  *     in bf16 and also quantised along f, and dXperm = Q(dA) Q(W_gate)^T +
  *     Q(dB) Q(W_up)^T runs in MXFP8;
- *   - the weight gradients contract over each expert's ragged token set
- *     and stay BF16 on X, dY and the bf16 dA, dB, w h; the shared expert,
- *     the router gradient and dX's router term are those of moe_backward.
+ *   - the weight gradients contract over each expert's ragged token set;
+ *     with wgrad_mxfp8 = 0 they stay BF16 on X, dY and the bf16 dA, dB,
+ *     w h; with wgrad_mxfp8 = 1 these operands are quantised along the
+ *     token axis (blocks of 32 plan rows from each expert's first row; the
+ *     quantisation the expert-grouped GEMMs need for a contraction over
+ *     tokens) and dW_gate = Q_t(X_e)^T Q_t(dA_e), dW_up = Q_t(X_e)^T Q_t(dB_e),
+ *     dW_down = Q_t(w h)^T Q_t(dY_e) run on the block-scaled matrix cores;
+ *   - the shared expert, the router gradient and dX's router term are those
+ *     of moe_backward.
  * Needs the ws of a preceding moe_forward_mx with save_for_backward = 1 (at
- * least moe_mx_workspace_bytes(shape, 1) bytes) and the same inputs.
- * `weights` as for moe_backward. */
+ * least moe_mx_workspace_bytes(shape, 1 + wgrad_mxfp8) bytes) and the same
+ * inputs.  `weights` as for moe_backward.  wgrad_mxfp8 is 0 or 1 (else
+ * MOE_EINVAL); with 1, d*P and f*P must stay below 2^32 (P as for
+ * MOE_WS_POFF; else MOE_EUNSUPPORTED). */
 moe_status moe_backward_mx(const moe_shape *shape, const moe_bf16 *dY, const moe_bf16 *X,
                            const moe_bf16 *W_r, const moe_weights *weights,
                            const moe_mx_bwd_weights *mx, const int32_t *topk_idx,
                            const float *topk_w, const moe_plan_bufs *plan, moe_bf16 *dX,
-                           const moe_grads *grads, void *ws, size_t ws_bytes, moe_stream stream);
+                           const moe_grads *grads, int wgrad_mxfp8, void *ws, size_t ws_bytes,
+                           moe_stream stream);
 
 /* Materialised dispatch (§3.1 "Scheduling", local part): Xperm[p] =
  * X[perm[p] / k] for p < T*k.  moe_forward does not need it (its GEMMs read

@@ -22,6 +22,8 @@ MOE_OK, MOE_EINVAL, MOE_EUNSUPPORTED, MOE_ENOSPACE, MOE_EHIP = range(5)
 WS_ERROR, WS_A, WS_B, WS_H, WS_YEXP, WS_YSH, WS_DG, WS_DA, WS_DB, WS_DXPERM = range(10)
 WS_XQ, WS_XS, WS_HQ, WS_HS = range(10, 14)
 WS_DYQ, WS_DYS, WS_DAQ, WS_DAS, WS_DBQ, WS_DBS = range(14, 20)
+WS_POFF, WS_XTQ, WS_XTS, WS_DYTQ, WS_DYTS = range(20, 25)
+WS_HW = 25
 
 EXPORTS = ("moe_workspace_bytes", "moe_workspace_region", "moe_route", "moe_plan",
            "moe_schedule_workspace_bytes", "moe_schedule", "moe_dispatch", "moe_forward",
@@ -115,7 +117,7 @@ def lib():
                                                   c_void_p]
         L.moe_backward_mx.argtypes = [P(MoeShape), c_void_p, c_void_p, c_void_p, P(MoeWeights),
                                       P(MoeMxBwdWeights), c_void_p, c_void_p, P(MoePlanBufs),
-                                      c_void_p, P(MoeGrads), c_void_p, c_size_t, c_void_p]
+                                      c_void_p, P(MoeGrads), c_int, c_void_p, c_size_t, c_void_p]
         L.moe_forward_fused.argtypes = [P(MoeShape), c_void_p, P(MoeWeights), c_void_p, c_void_p,
                                         P(MoePlanBufs), c_void_p, c_int, c_void_p, c_size_t,
                                         c_void_p]
@@ -236,8 +238,10 @@ def mx_weights_struct(Wg_q, Wu_q, Wd_q, Wg_s, Wu_s, Wd_s) -> MoeMxWeights:
     return MoeMxWeights(_p(Wg_q), _p(Wu_q), _p(Wd_q), _p(Wg_s), _p(Wu_s), _p(Wd_s))
 
 
-def moe_mx_workspace_bytes(shape: MoeShape, with_backward: bool = False) -> int:
-    return int(lib().moe_mx_workspace_bytes(ctypes.byref(shape), int(bool(with_backward))))
+def moe_mx_workspace_bytes(shape: MoeShape, with_backward: int = 0) -> int:
+    """with_backward: 0 forward, 1 with the MXFP8 backward, 2 with its MXFP8
+    weight gradients too."""
+    return int(lib().moe_mx_workspace_bytes(ctypes.byref(shape), int(with_backward)))
 
 
 def mx_bwd_weights_struct(Wg_q, Wu_q, Wd_q, Wg_s, Wu_s, Wd_s) -> MoeMxBwdWeights:
@@ -253,11 +257,12 @@ def moe_mx_quantize_weights_bwd(shape, weights: MoeWeights, mx: MoeMxBwdWeights,
 
 def moe_backward_mx(shape, dY, X, W_r, weights: MoeWeights, mx: MoeMxBwdWeights, topk_idx, topk_w,
                     plan: MoePlanBufs, dX, grads: MoeGrads, ws, ws_bytes=None, stream=None,
-                    raise_on_error=True):
+                    raise_on_error=True, wgrad_mxfp8=False):
     nbytes = ws.numel() * ws.element_size() if ws_bytes is None else ws_bytes
     st = lib().moe_backward_mx(ctypes.byref(shape), _p(dY), _p(X), _p(W_r), ctypes.byref(weights),
                                ctypes.byref(mx), _p(topk_idx), _p(topk_w), ctypes.byref(plan),
-                               _p(dX), ctypes.byref(grads), _p(ws), nbytes, _stream(stream))
+                               _p(dX), ctypes.byref(grads), int(wgrad_mxfp8), _p(ws), nbytes,
+                               _stream(stream))
     return _check("moe_backward_mx", st, raise_on_error)
 
 

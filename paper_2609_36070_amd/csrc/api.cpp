@@ -31,6 +31,11 @@ struct Layout {
     size_t mx_total;
     size_t dyq, dys, daq, das, dbq, dbs;   // MXFP8 backward: quantised dY, dA, dB
     size_t mxb_total;
+    // MXFP8 weight gradients: padded expert offsets and the token-axis codes
+    // and scales of X, dY, dA, dB and w h, [C][tpad] and [C][tpad / 32]
+    size_t poff, xt, xts, dyt, dyts, dat, dats, dbt, dbts, hwt, hwts;
+    size_t mxw_total;
+    long tpad;                 // their row pitch: the padded token positions' bound
     long act_rows;             // rows of the per-route activation buffers
     int dg_parts;
 };
@@ -97,6 +102,21 @@ Layout make_layout(const moe_shape &s, long ring_rows = -1) {
     L.dbq = take(R * f);
     L.dbs = take(R * f / 32);
     L.mxb_total = o;
+    // each expert's rows padded to 128 positions: at most R + 127 E in all
+    L.tpad = (long)((R + 128 * E + 127) / 128 * 128);
+    const size_t P = (size_t)L.tpad;
+    L.poff = take((E + 1) * 4);
+    L.xt = take(d * P);
+    L.xts = take(d * P / 32);
+    L.dyt = take(d * P);
+    L.dyts = take(d * P / 32);
+    L.dat = take(f * P);
+    L.dats = take(f * P / 32);
+    L.dbt = take(f * P);
+    L.dbts = take(f * P / 32);
+    L.hwt = take(f * P);
+    L.hwts = take(f * P / 32);
+    L.mxw_total = o;
     return L;
 }
 
@@ -185,6 +205,14 @@ moe_status check_mx_shape(const moe_shape *s) {
     const int64_t lim = int64_t(1) << 32;
     if (s->T * s->d >= lim || s->T * s->k * s->f >= lim || s->E * s->f * s->d >= lim)
         return MOE_EUNSUPPORTED;
+    return MOE_OK;
+}
+
+// MXFP8 weight gradients: their token-axis operands too.
+moe_status check_mx_wgrad_shape(const moe_shape *s) {
+    const int64_t lim = int64_t(1) << 32;
+    const int64_t tpad = (s->T * s->k + 128 * s->E + 127) / 128 * 128;
+    if (s->d * tpad >= lim || s->f * tpad >= lim) return MOE_EUNSUPPORTED;
     return MOE_OK;
 }
 
@@ -483,6 +511,7 @@ moe_status moe_workspace_region(const moe_shape *shape, int with_backward, moe_w
         case MOE_WS_DA: *offset = L.dA; *bytes = R * f * 2; break;
         case MOE_WS_DB: *offset = L.dB; *bytes = R * f * 2; break;
         case MOE_WS_DXPERM: *offset = L.dXperm; *bytes = R * d * 2; break;
+        case MOE_WS_HW: *offset = L.Hw; *bytes = R * f * 2; break;
         default: return MOE_EINVAL;
     }
     if (!with_backward && *offset >= L.fwd_total) return MOE_EINVAL;
@@ -783,8 +812,10 @@ moe_status moe_backward_ring(const moe_shape *shape, const moe_bf16 *dY, const m
 
 size_t moe_mx_workspace_bytes(const moe_shape *shape, int with_backward) {
     if (check_shape(shape) != MOE_OK || check_mx_shape(shape) != MOE_OK) return 0;
+    if (with_backward < 0 || with_backward > 2) return 0;
     const Layout L = make_layout(*shape);
     if (!with_backward) return L.mx_total;
+    if (with_backward == 2) return check_mx_wgrad_shape(shape) == MOE_OK ? L.mxw_total : 0;
     return L.mxb_total > L.mx_total ? L.mxb_total : L.mx_total;
 }
 
@@ -811,6 +842,11 @@ moe_status moe_mx_workspace_region(const moe_shape *shape, moe_ws_tensor which, 
         case MOE_WS_DAS: *offset = L.das; *bytes = R * f / 32; break;
         case MOE_WS_DBQ: *offset = L.dbq; *bytes = R * f; break;
         case MOE_WS_DBS: *offset = L.dbs; *bytes = R * f / 32; break;
+        case MOE_WS_POFF: *offset = L.poff; *bytes = (size_t)(shape->E + 1) * 4; break;
+        case MOE_WS_XTQ: *offset = L.xt; *bytes = d * (size_t)L.tpad; break;
+        case MOE_WS_XTS: *offset = L.xts; *bytes = d * (size_t)L.tpad / 32; break;
+        case MOE_WS_DYTQ: *offset = L.dyt; *bytes = d * (size_t)L.tpad; break;
+        case MOE_WS_DYTS: *offset = L.dyts; *bytes = d * (size_t)L.tpad / 32; break;
         default: return moe_workspace_region(shape, 1, which, offset, bytes);
     }
     return MOE_OK;
@@ -922,17 +958,20 @@ moe_status moe_mx_quantize_weights_bwd(const moe_shape *shape, const moe_weights
 moe_status moe_backward_mx(const moe_shape *shape, const moe_bf16 *dY, const moe_bf16 *X,
                            const moe_bf16 *W_r, const moe_weights *weights,
                            const moe_mx_bwd_weights *mx, const int32_t *topk_idx, const float *topk_w,
-                           const moe_plan_bufs *plan, moe_bf16 *dX, const moe_grads *grads, void *ws,
-                           size_t ws_bytes, moe_stream stream) {
+                           const moe_plan_bufs *plan, moe_bf16 *dX, const moe_grads *grads,
+                           int wgrad_mxfp8, void *ws, size_t ws_bytes, moe_stream stream) {
     moe_status st = check_backward_args(shape, dY, X, W_r, weights, topk_idx, topk_w, plan, dX, grads);
     if (st != MOE_OK) return st;
     if ((st = check_mx_shape(shape)) != MOE_OK) return st;
+    if (wgrad_mxfp8 != 0 && wgrad_mxfp8 != 1) return MOE_EINVAL;
+    if (wgrad_mxfp8 && (st = check_mx_wgrad_shape(shape)) != MOE_OK) return st;
     if (!mx || !ptr_ok(mx->Wg_q) || !ptr_ok(mx->Wu_q) || !ptr_ok(mx->Wd_q) || !ptr_ok(mx->Wg_s) ||
         !ptr_ok(mx->Wu_s) || !ptr_ok(mx->Wd_s))
         return MOE_EINVAL;
     if (!ptr_ok(ws)) return MOE_EINVAL;
     const Layout L = make_layout(*shape);
     if (ws_bytes < L.mxb_total || ws_bytes < L.mx_total) return MOE_ENOSPACE;
+    if (wgrad_mxfp8 && ws_bytes < L.mxw_total) return MOE_ENOSPACE;
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int T = (int)shape->T, d = (int)shape->d, E = (int)shape->E, k = (int)shape->k;
     const int f = (int)shape->f;
@@ -979,9 +1018,44 @@ moe_status moe_backward_mx(const moe_shape *shape, const moe_bf16 *dY, const moe
         g.bs_bytes = (uint32_t)((long)E * d * f / 32);
         MOE_TRY(launch_gemm_mx_dx(g, R, E, s));
     }
-    // weight gradients in BF16 on the unquantised operands
-    for (int i = 0; i < 3; ++i)
-        MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, i), E, s));
+    if (wgrad_mxfp8) {
+        // weight gradients in MXFP8: the operands quantised along the token
+        // axis per expert (blocks of 32 from each expert's first row, each
+        // expert's region padded to 128 positions), then dW = A . B^T over
+        // the expert's padded range on the block-scaled matrix cores
+        int *poff = at<int>(ws, L.poff);
+        const long P = L.tpad;
+        const int *rowidx = at<int>(ws, L.rowidx);
+        MOE_TRY(launch_mx_pad_offsets(plan->offsets, E, poff, s));
+        MOE_TRY(launch_mx_quant_tokens(X, d, T, rowidx, plan->offsets, poff, E, d, P, P,
+                                       at<uint8_t>(ws, L.xt), at<uint8_t>(ws, L.xts), s));
+        MOE_TRY(launch_mx_quant_tokens(dY, d, T, rowidx, plan->offsets, poff, E, d, P, P,
+                                       at<uint8_t>(ws, L.dyt), at<uint8_t>(ws, L.dyts), s));
+        MOE_TRY(launch_mx_quant_tokens(at<uint16_t>(ws, L.dA), f, R, nullptr, plan->offsets, poff, E,
+                                       f, P, P, at<uint8_t>(ws, L.dat), at<uint8_t>(ws, L.dats), s));
+        MOE_TRY(launch_mx_quant_tokens(at<uint16_t>(ws, L.dB), f, R, nullptr, plan->offsets, poff, E,
+                                       f, P, P, at<uint8_t>(ws, L.dbt), at<uint8_t>(ws, L.dbts), s));
+        MOE_TRY(launch_mx_quant_tokens(at<uint16_t>(ws, L.Hw), f, R, nullptr, plan->offsets, poff, E,
+                                       f, P, P, at<uint8_t>(ws, L.hwt), at<uint8_t>(ws, L.hwts), s));
+        auto wg = [&](size_t a, size_t as, int M, size_t b, size_t bs, int N, float *out) {
+            MxGemmArgs g;
+            g.A = at<uint8_t>(ws, a); g.As = at<uint8_t>(ws, as); g.a_nrows = M;
+            g.B = at<uint8_t>(ws, b); g.Bs = at<uint8_t>(ws, bs);
+            g.M = M; g.N = N; g.K = (int)P; g.offsets = poff; g.E = E; g.Cf = out;
+            g.a_bytes = (uint32_t)((long)M * P);
+            g.as_bytes = (uint32_t)((long)M * P / 32);
+            g.b_bytes = (uint32_t)((long)N * P);
+            g.bs_bytes = (uint32_t)((long)N * P / 32);
+            return launch_gemm_mx_wgrad(g, E, s);
+        };
+        MOE_TRY(wg(L.xt, L.xts, d, L.dat, L.dats, f, grads->dW_gate));
+        MOE_TRY(wg(L.xt, L.xts, d, L.dbt, L.dbts, f, grads->dW_up));
+        MOE_TRY(wg(L.hwt, L.hwts, f, L.dyt, L.dyts, d, grads->dW_down));
+    } else {
+        // weight gradients in BF16 on the unquantised operands
+        for (int i = 0; i < 3; ++i)
+            MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, i), E, s));
+    }
     if (shared) MOE_TRY(shared_backward(*shape, L, ws, dY, X, weights, grads, StageMarks{nullptr, s}, s));
     MOE_TRY(launch_dwr(X, dZ, T, d, E, at<float>(ws, L.dwr_part), grads->dW_r, s));
     MOE_TRY(launch_reverse_combine(at<uint16_t>(ws, L.dXperm), shared ? at<uint16_t>(ws, L.dXsh) : nullptr,

@@ -77,3 +77,38 @@ inline long raster_grid(long tiles_m, int ntn) {
     const long groups = (tiles_m + RASTER_GM - 1) / RASTER_GM;
     return 8 * ((groups + 7) / 8) * RASTER_GM * ntn;
 }
+
+// Weight-gradient raster.  A tile's cost is its expert's route count, so
+// XCDs that each ran whole experts would wait for the heaviest one (or idle
+// outright when a window of the bounded-memory backward holds only some of
+// the experts).  Instead each expert's ntm x ntn tiles are cut into blocks of
+// 4 x 4 tiles, the blocks of all experts are numbered expert by expert, and
+// block h goes to XCD h % 8: every XCD gets an equal share of each expert
+// (up to one block), and the 32 tiles an XCD runs at once are two such
+// blocks, each sharing 4 A and 4 B panels in that XCD's L2.
+// Grid: 8 * 16 * ceil(groups * blocks_per_expert / 8) workgroups.
+constexpr int WG_BM = 4, WG_BN = 4;
+__host__ __device__ __forceinline__ int wgrad_blocks_per_expert(int ntm, int ntn) {
+    return ((ntm + WG_BM - 1) / WG_BM) * ((ntn + WG_BN - 1) / WG_BN);
+}
+DEV bool map_tile_wgrad(int b, int groups, int ntm, int ntn, int &cm, int &nt) {
+    constexpr int NX = 8, PER = WG_BM * WG_BN;
+    const int nbm = (ntm + WG_BM - 1) / WG_BM;
+    const int nb = wgrad_blocks_per_expert(ntm, ntn);
+    const int j = b / NX;                        // position in this XCD's sequence
+    const int h = (j / PER) * NX + b % NX;       // block
+    const int t = j % PER;                       // tile within the block, m fastest
+    const int e = h / nb, lb = h % nb;
+    if (e >= groups) return false;
+    const int mt = (lb % nbm) * WG_BM + t % WG_BM;
+    nt = (lb / nbm) * WG_BN + t / WG_BM;
+    if (mt >= ntm || nt >= ntn) return false;
+    cm = e * ntm + mt;
+    return true;
+}
+
+// Workgroups of a launch whose tiles map_tile_wgrad places.
+inline long wgrad_grid(long groups, int ntm, int ntn) {
+    const long nblk = groups * wgrad_blocks_per_expert(ntm, ntn);
+    return 8L * WG_BM * WG_BN * ((nblk + 7) / 8);
+}

@@ -136,34 +136,6 @@ DEV bf16x8_t frag_col(const uint16_t *t, int n0, int ks, int lane) {
 }
 
 
-// Weight-gradient raster.  A tile's cost is its expert's route count, so
-// XCDs that each ran whole experts would wait for the heaviest one (or idle
-// outright when a window of the bounded-memory backward holds only some of
-// the experts).  Instead each expert's ntm x ntn tiles are cut into blocks of
-// 4 x 4 tiles, the blocks of all experts are numbered expert by expert, and
-// block h goes to XCD h % 8: every XCD gets an equal share of each expert
-// (up to one block), and the 32 tiles an XCD runs at once are two such
-// blocks, each sharing 4 A and 4 B panels in that XCD's L2.
-// Grid: 8 * 16 * ceil(groups * blocks_per_expert / 8) workgroups.
-constexpr int WG_BM = 4, WG_BN = 4;
-__host__ __device__ __forceinline__ int wgrad_blocks_per_expert(int ntm, int ntn) {
-    return ((ntm + WG_BM - 1) / WG_BM) * ((ntn + WG_BN - 1) / WG_BN);
-}
-DEV bool map_tile_wgrad(int b, int groups, int ntm, int ntn, int &cm, int &nt) {
-    constexpr int NX = 8, PER = WG_BM * WG_BN;
-    const int nbm = (ntm + WG_BM - 1) / WG_BM;
-    const int nb = wgrad_blocks_per_expert(ntm, ntn);
-    const int j = b / NX;                        // position in this XCD's sequence
-    const int h = (j / PER) * NX + b % NX;       // block
-    const int t = j % PER;                       // tile within the block, m fastest
-    const int e = h / nb, lb = h % nb;
-    if (e >= groups) return false;
-    const int mt = (lb % nbm) * WG_BM + t % WG_BM;
-    nt = (lb / nbm) * WG_BN + t / WG_BM;
-    if (mt >= ntm || nt >= ntn) return false;
-    cm = e * ntm + mt;
-    return true;
-}
 
 // Two LDS stages, each operand its own object: the compiler then knows the
 // tile being read never aliases the tile being filled and does not stall the
@@ -778,9 +750,8 @@ hipError_t launch_gemm_bwd_dx(const GemmArgs &g, long rows, int groups, hipStrea
     return launch_mode<BWD_DX>(g, mtiles(g, rows, groups), g.N / BN, st);
 }
 hipError_t launch_gemm_wgrad(const GemmArgs &g, int groups, hipStream_t st) {
-    const long nblk = (long)groups * wgrad_blocks_per_expert(g.M / BM, g.N / BN);
     return launch_mode<WGRAD>(g, groups * (g.M / BM), g.N / BN, st,
-                              8L * WG_BM * WG_BN * ((nblk + 7) / 8));
+                              wgrad_grid(groups, g.M / BM, g.N / BN));
 }
 
 hipError_t launch_gemm_wgrad_batch(const GemmArgs *wg, int nw, int groups, const GemmArgs *up,
@@ -794,8 +765,7 @@ hipError_t launch_gemm_wgrad_batch(const GemmArgs *wg, int nw, int groups, const
         if (!g.offsets) return hipErrorInvalidValue;
         const int ntm = g.M / BM, ntn = g.N / BN;
         g.tiles_m = groups * ntm;
-        const long nblk = (long)groups * wgrad_blocks_per_expert(ntm, ntn);
-        const long blocks = 8L * WG_BM * WG_BN * ((nblk + 7) / 8);
+        const long blocks = wgrad_grid(groups, ntm, ntn);
         if ((long)g.tiles_m * ntn <= 0) continue;
         bt.g[bt.n] = g;
         bt.start[bt.n] = (int)at;

@@ -13,6 +13,10 @@
 //            quantised to MXFP8 along f (for the dX product)
 //   MX_DX    dXperm = dAq[p] . Wg_qf[e][n] + dBq[p] . Wu_qf[e][n] (one K loop
 //            over both halves; W_gate / W_up rows quantised along f) -> bf16
+//   MX_WGRAD dW[e][m][n] = sum over e's padded token positions t of
+//            A[m][t] B[n][t]: both operands quantised along the token axis
+//            (X^T or (w h)^T, and dA^T, dB^T or dY^T) -> fp32, one tile per
+//            (expert, m tile, n tile), K = the expert's padded range
 //
 // Every operand is a matrix of K-contiguous byte rows (A: token or position
 // rows; B: one row per output column, the pre-quantised weight layout) with
@@ -24,9 +28,9 @@
 //
 // Pipeline as in the BF16 kernels: 256 x 256 block tile, K step 128 bytes,
 // two LDS stages filled by direct global->LDS loads (128-byte rows, chunk
-// XOR (row >> 1) & 7), 8 waves of 128 x 64, fragments double-buffered in
-// registers, tiles rastered XCD-aware.  Scale words (4 blocks of a row per K
-// step) are loaded into registers one step ahead, together with the tiles.
+// XOR (row >> 1) & 7), 4 waves of 128 x 128 (accumulators in AGPRs), tiles
+// rastered XCD-aware.  The scale words of a K step (4 blocks of a row) go
+// to LDS by the same direct loads, one stage ahead, together with the tiles.
 #include "common.h"
 #include "kernels.h"
 #include "mx_common.h"
@@ -49,7 +53,7 @@ constexpr int TILE = BM * BK;                      // bytes per operand per stag
 constexpr int LD_PER_OP = TILE / 1024 / NWAVES;    // 1 KB direct loads per operand per wave per step
 static_assert(WN == 64 || WN == 128, "gate/up column pairs need 64- or 128-column wave tiles");
 
-enum MxMode { MX_UP = 0, MX_DOWN = 1, MX_DGRAD = 2, MX_DX = 3 };
+enum MxMode { MX_UP = 0, MX_DOWN = 1, MX_DGRAD = 2, MX_DX = 3, MX_WGRAD = 4 };
 
 typedef int i32x8_t __attribute__((ext_vector_type(8)));
 
@@ -98,37 +102,52 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
     // ---------------- tile: expert region and rows ----------------
-    const int ntn = (MODE == MX_UP) ? g.N / (BN / 2) : g.N / BN;
-    int mt = 0, ntile = 0;
-    if (!map_tile(blockIdx.x, g.tiles_m, ntn, mt, ntile)) return;
-    const int n0 = ntile * ((MODE == MX_UP) ? BN / 2 : BN);
-    if (tid == 0) s_info[0] = -1;
-    __syncthreads();
-    if (tid < 64) {
-        int cum = 0;
-        for (int base = 0; base < g.E; base += 64) {
-            const int ee = base + lane;
-            const int cnt = ee < g.E ? g.offsets[ee + 1] - g.offsets[ee] : 0;
-            const int tiles = cnt > 0 ? (cnt + BM - 1) / BM : 0;
-            int x = tiles;
+    int e = 0, row0 = 0, row_end = 0, n0 = 0, ntile = 0;
+    uint32_t kbase = 0;   // MX_WGRAD: byte offset of the expert's padded token range
+    int nk_w = 0;         // MX_WGRAD: K steps over that range
+    if constexpr (MODE == MX_WGRAD) {
+        const int ntm = g.M / BM;
+        int cm = 0;
+        if (!map_tile_wgrad(blockIdx.x, g.E, ntm, g.N / BN, cm, ntile)) return;
+        e = cm / ntm;
+        row0 = (cm % ntm) * BM;
+        row_end = g.M;
+        n0 = ntile * BN;
+        kbase = (uint32_t)uniform(g.offsets[e]);
+        nk_w = (uniform(g.offsets[e + 1]) - (int)kbase) / BK;
+    } else {
+        const int ntn = (MODE == MX_UP) ? g.N / (BN / 2) : g.N / BN;
+        int mt = 0;
+        if (!map_tile(blockIdx.x, g.tiles_m, ntn, mt, ntile)) return;
+        n0 = ntile * ((MODE == MX_UP) ? BN / 2 : BN);
+        if (tid == 0) s_info[0] = -1;
+        __syncthreads();
+        if (tid < 64) {
+            int cum = 0;
+            for (int base = 0; base < g.E; base += 64) {
+                const int ee = base + lane;
+                const int cnt = ee < g.E ? g.offsets[ee + 1] - g.offsets[ee] : 0;
+                const int tiles = cnt > 0 ? (cnt + BM - 1) / BM : 0;
+                int x = tiles;
 #pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const int y = __shfl_up(x, off, 64);
-                if (lane >= off) x += y;
+                for (int off = 1; off < 64; off <<= 1) {
+                    const int y = __shfl_up(x, off, 64);
+                    if (lane >= off) x += y;
+                }
+                const int excl = cum + x - tiles;
+                if (ee < g.E && mt >= excl && mt < excl + tiles) {
+                    s_info[0] = ee;
+                    s_info[1] = mt - excl;
+                }
+                cum += __shfl(x, 63, 64);
             }
-            const int excl = cum + x - tiles;
-            if (ee < g.E && mt >= excl && mt < excl + tiles) {
-                s_info[0] = ee;
-                s_info[1] = mt - excl;
-            }
-            cum += __shfl(x, 63, 64);
         }
+        __syncthreads();
+        e = uniform(s_info[0]);
+        if (e < 0) return;
+        row0 = uniform(g.offsets[e] + uniform(s_info[1]) * BM);
+        row_end = uniform(g.offsets[e + 1]);
     }
-    __syncthreads();
-    const int e = uniform(s_info[0]);
-    if (e < 0) return;
-    const int row0 = uniform(g.offsets[e] + uniform(s_info[1]) * BM);
-    const int row_end = uniform(g.offsets[e + 1]);
     const long ks_row = g.K / 32;     // scale bytes per row
 
     // physical A row of tile row r (rows past the region's end repeat its last
@@ -174,19 +193,20 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
             sc_off[i] = (uint32_t)a_phys(64 * c + lane) * (uint32_t)ks_row;
         } else {
             const int wd = 64 * (c - 4) + lane;               // B scale word
-            const uint32_t brow = (MODE == MX_UP) ? (uint32_t)(e * g.N + n0 + (wd & 127))
-                                                  : (uint32_t)(e * g.N + n0 + wd);
+            const uint32_t brow = (MODE == MX_UP)      ? (uint32_t)(e * g.N + n0 + (wd & 127))
+                                : (MODE == MX_WGRAD) ? (uint32_t)(n0 + wd)
+                                                     : (uint32_t)(e * g.N + n0 + wd);
             sc_off[i] = brow * (uint32_t)ks_row;
         }
     }
 
     const int nk_half = g.K / BK;
-    const int nk = (MODE == MX_DX) ? 2 * nk_half : nk_half;
+    const int nk = (MODE == MX_DX) ? 2 * nk_half : (MODE == MX_WGRAD) ? nk_w : nk_half;
     auto issue = [&](int kt_all, uint8_t *la, uint8_t *lb, uint32_t *sa, uint32_t *sb) {
         // MX_DX: the second half of the K loop reads dBq against the W_up rows
         const bool second = (MODE == MX_DX) && kt_all >= nk_half;
         const int kt = second ? kt_all - nk_half : kt_all;
-        const uint32_t kb = (uint32_t)kt * BK;
+        const uint32_t kb = kbase + (uint32_t)kt * BK;
 #pragma unroll
         for (int i = 0; i < LD_PER_OP; ++i) {
             const int q = LD_PER_OP * wave + i;
@@ -210,7 +230,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
             const bool up = ((MODE == MX_UP) && ((q >> 2) & 1)) || second;
             const uint32_t brow = (MODE == MX_UP)
                 ? (uint32_t)(e * g.N + n0 + (q >> 3) * 32 + 8 * (q & 3))
-                : (uint32_t)(e * g.N + n0 + 8 * q);
+                : (uint32_t)((MODE == MX_WGRAD ? 0 : e * g.N) + n0 + 8 * q);
             __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(up ? g.B2 : g.B, g.b_bytes),
                                                      (LDSP void *)(lb + q * 1024), 16,
                                                      (q & 1) ? b_lane_odd : b_lane_even,
@@ -222,12 +242,12 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
             if (c < 4) {
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(second ? g.As2 : g.As, g.as_bytes),
                                                          (LDSP void *)(sa + 64 * c), 4, sc_off[i],
-                                                         4 * kt, 0, 0);
+                                                         kbase / 32 + 4 * kt, 0, 0);
             } else {
                 const bool up = ((MODE == MX_UP) && (c - 4 >= 2)) || second;
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(up ? g.Bs2 : g.Bs, g.bs_bytes),
                                                          (LDSP void *)(sb + 64 * (c - 4)), 4,
-                                                         sc_off[i], 4 * kt, 0, 0);
+                                                         sc_off[i], kbase / 32 + 4 * kt, 0, 0);
             }
         }
     };
@@ -463,6 +483,23 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
                 g.dgpart[(long)p * g.dg_ld + ntile] = sum;
             }
         }
+    } else if constexpr (MODE == MX_WGRAD) {
+        // fp32 rows of dW[e]; M and N are multiples of the tile, so every
+        // staged row is a real one
+        constexpr int LPR = WN / 8, RPP = 64 / LPR;
+        float *out = g.Cf + (long)e * g.M * g.N;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            stage(i);
+#pragma unroll
+            for (int t = 0; t < 32 / RPP; ++t) {
+                const int row = lane / LPR + RPP * t, c = 8 * (lane % LPR);
+                const f32x8 v = read8(row, c);
+                float *o = out + (long)(row0 + wm * WM + 32 * i + row) * g.N + n0 + wn * WN + c;
+                *reinterpret_cast<f32x4_t *>(o) = f32x4_t{v[0], v[1], v[2], v[3]};
+                *reinterpret_cast<f32x4_t *>(o + 4) = f32x4_t{v[4], v[5], v[6], v[7]};
+            }
+        }
     } else {   // MX_DOWN, MX_DX: bf16 rows
         constexpr int LPR = WN / 8, RPP = 64 / LPR;
 #pragma unroll
@@ -507,4 +544,11 @@ hipError_t launch_gemm_mx_dgrad(const MxGemmArgs &g, long rows, int groups, hipS
 
 hipError_t launch_gemm_mx_dx(const MxGemmArgs &g, long rows, int groups, hipStream_t st) {
     return launch_mx_mode<MX_DX>(g, mx_mtiles(rows, groups), g.N / BN, st);
+}
+
+hipError_t launch_gemm_mx_wgrad(const MxGemmArgs &g, int groups, hipStream_t st) {
+    if (groups <= 0 || g.M <= 0 || g.N <= 0 || g.E != groups) return hipSuccess;
+    const unsigned grid = (unsigned)wgrad_grid(groups, g.M / BM, g.N / BN);
+    gemm_mx_kernel<MX_WGRAD><<<dim3(grid), dim3(NTHREADS), 0, st>>>(g, nullptr);
+    return hipGetLastError();
 }

@@ -113,11 +113,27 @@ struct MxGemmArgs {
     int dg_ld = 0;
     uint32_t a_bytes = 0, as_bytes = 0, b_bytes = 0, bs_bytes = 0;   // operand extents (< 4 GiB)
     int tiles_m = 0;
+    // MX_WGRAD: dW[e] = A[:, k_e] . B[:, k_e]^T over expert e's padded token
+    // range k_e = [offsets[e], offsets[e+1]) (multiples of 128); A [M][K] and
+    // B [N][K] hold token-axis codes, K is their row pitch in bytes
+    int M = 0;
+    float *Cf = nullptr;               // MX_WGRAD: fp32 [E][M][N]
 };
 hipError_t launch_gemm_mx_up(const MxGemmArgs &g, long rows, int groups, hipStream_t st);
 hipError_t launch_gemm_mx_down(const MxGemmArgs &g, long rows, int groups, hipStream_t st);
 hipError_t launch_gemm_mx_dgrad(const MxGemmArgs &g, long rows, int groups, hipStream_t st);
 hipError_t launch_gemm_mx_dx(const MxGemmArgs &g, long rows, int groups, hipStream_t st);
+hipError_t launch_gemm_mx_wgrad(const MxGemmArgs &g, int groups, hipStream_t st);
+// Token-axis MXFP8 operands of the weight gradients: for each expert, the rows
+// of its plan region (through `rows`: position -> source row, or the position
+// itself) in 32-row blocks from the region's start, written transposed as
+// [C][pitch] codes and [C][pitch / 32] scales at the expert's padded offset
+// poff[e] (multiples of 128; positions past the region's rows are zeros).
+// src has nsrc rows of pitch ld; max_pos (a multiple of 128) bounds poff[E].
+hipError_t launch_mx_pad_offsets(const int *offsets, int E, int *poff, hipStream_t st);
+hipError_t launch_mx_quant_tokens(const uint16_t *src, long ld, long nsrc, const int *rows,
+                                  const int *offsets, const int *poff, int E, int C, long pitch,
+                                  long max_pos, uint8_t *q, uint8_t *sc, hipStream_t st);
 hipError_t launch_mx_quant_rows(const uint16_t *X, long rows, int K, uint8_t *q, uint8_t *sc,
                                 hipStream_t st);
 hipError_t launch_mx_quant_weights(const uint16_t *W, int E, int K, int N, uint8_t *q, uint8_t *sc,

@@ -15,6 +15,11 @@
 //   mx_quant_weights: [E][K][N] bf16 weights -> K-contiguous [E][N][K] codes
 //                     and [E][N][K/32] scales (a 32 x 256 tile transposed
 //                     through LDS), the operand layout of the fp8 GEMMs.
+//   mx_quant_tokens:  the weight-gradient operands, which contract over an
+//                     expert's tokens: rows of the expert's plan region in
+//                     32-row blocks from its first row, written transposed
+//                     (token-contiguous) at the expert's region padded to
+//                     128 positions, the K step of the fp8 GEMM.
 #include "common.h"
 #include "kernels.h"
 #include "mx_common.h"
@@ -95,6 +100,105 @@ __global__ __launch_bounds__(256) void mx_quant_weights_kernel(const uint16_t *_
     sc[((long)e * N + n) * (K / 32) + k0 / 32] = (uint8_t)(s + 127);
 }
 
+// Padded expert regions: poff[e] = sum over e' < e of count(e') rounded up
+// to 128; poff[E] = the padded total.  One wave, a scan per 64 experts.
+__global__ __launch_bounds__(64) void mx_pad_offsets_kernel(const int *__restrict__ offsets, int E,
+                                                           int *__restrict__ poff) {
+    const int lane = threadIdx.x;
+    int cum = 0;
+    for (int base = 0; base < E; base += 64) {
+        const int e = base + lane;
+        const int n = e < E ? offsets[e + 1] - offsets[e] : 0;
+        const int padded = (n + 127) / 128 * 128;
+        int x = padded;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int y = __shfl_up(x, off, 64);
+            if (lane >= off) x += y;
+        }
+        if (e < E) poff[e] = cum + x - padded;
+        cum += __shfl(x, 63, 64);
+    }
+    if (lane == 0) poff[E] = cum;
+}
+
+// Grid (C / 256, max_pos / 128).  Block: 256 threads; thread t owns column
+// c0 + t of the 128 padded positions [p0, p0 + 128) of one expert: four
+// 32-position blocks, each staged through LDS (32 rows x 256 columns), whose
+// codes stay in registers until one 128-byte row segment and one word of 4
+// scales are written.
+template <bool GATHER>
+__global__ __launch_bounds__(256) void mx_quant_tokens_kernel(const uint16_t *__restrict__ src, long ld,
+                                                              long nsrc, const int *__restrict__ rows,
+                                                              const int *__restrict__ offsets,
+                                                              const int *__restrict__ poff, int E,
+                                                              long pitch, uint8_t *__restrict__ q,
+                                                              uint8_t *__restrict__ sc) {
+    __shared__ __attribute__((aligned(16))) uint16_t tile[32 * WQ_PITCH];
+    __shared__ int s_row[128];
+    const int t = threadIdx.x;
+    const int c0 = blockIdx.x * WQ_TN;
+    const int p0 = blockIdx.y * 128;
+    if (p0 >= poff[E]) return;                 // past the padded total (uniform)
+    // the expert whose padded region holds p0: the last e with poff[e] <= p0
+    int lo = 0, hi = E - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (poff[mid] <= p0) lo = mid;
+        else hi = mid - 1;
+    }
+    const int base = offsets[lo], cnt = offsets[lo + 1] - base;
+    if (t < 128) {
+        const int local = p0 - poff[lo] + t;
+        int r = -1;                             // padding: zeros
+        if (local < cnt) {
+            r = GATHER ? rows[base + local] : base + local;
+            r = r < 0 ? 0 : (r >= nsrc ? (int)nsrc - 1 : r);   // a malformed plan stays in bounds
+        }
+        s_row[t] = r;
+    }
+    uint32_t codes[32];
+    uint32_t scw = 0;
+#pragma unroll
+    for (int sb = 0; sb < 4; ++sb) {
+        __syncthreads();                        // s_row written / tile free
+        // 32 rows x 256 columns: 1024 chunks of 8 bf16, 4 per thread, coalesced
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {
+            const int ch = it * 256 + t;
+            const int r = ch / 32, c = 8 * (ch % 32);
+            const int row = s_row[32 * sb + r];
+            u32x4_t v = u32x4_t{0, 0, 0, 0};
+            if (row >= 0) v = ld_u32x4(src + (long)row * ld + c0 + c);
+            st_u32x4(tile + r * WQ_PITCH + c, v);
+        }
+        __syncthreads();
+        float v[32];
+        float amax = 0.f;
+#pragma unroll
+        for (int r = 0; r < 32; ++r) {
+            v[r] = bf2f(tile[r * WQ_PITCH + t]);
+            amax = fmaxf(amax, fabsf(v[r]));
+        }
+        const int s = mx_shared_exp(amax);
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+            float part[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) part[j] = v[8 * h + j];
+            const u32x2_t w = e4m3_pack8(part, s);
+            codes[8 * sb + 2 * h] = w[0];
+            codes[8 * sb + 2 * h + 1] = w[1];
+        }
+        scw |= (uint32_t)(s + 127) << (8 * sb);
+    }
+    uint8_t *dst = q + (long)(c0 + t) * pitch + p0;
+#pragma unroll
+    for (int w = 0; w < 8; ++w)
+        st_u32x4(dst + 16 * w, u32x4_t{codes[4 * w], codes[4 * w + 1], codes[4 * w + 2], codes[4 * w + 3]});
+    *reinterpret_cast<uint32_t *>(sc + (long)(c0 + t) * (pitch / 32) + p0 / 32) = scw;
+}
+
 }  // namespace
 
 hipError_t launch_mx_quant_rows(const uint16_t *X, long rows, int K, uint8_t *q, uint8_t *sc,
@@ -110,5 +214,22 @@ hipError_t launch_mx_quant_weights(const uint16_t *W, int E, int K, int N, uint8
                                    hipStream_t st) {
     if (E <= 0) return hipSuccess;
     mx_quant_weights_kernel<<<dim3(N / WQ_TN, K / 32, E), dim3(256), 0, st>>>(W, K, N, q, sc);
+    return hipGetLastError();
+}
+
+hipError_t launch_mx_pad_offsets(const int *offsets, int E, int *poff, hipStream_t st) {
+    mx_pad_offsets_kernel<<<dim3(1), dim3(64), 0, st>>>(offsets, E, poff);
+    return hipGetLastError();
+}
+
+hipError_t launch_mx_quant_tokens(const uint16_t *src, long ld, long nsrc, const int *rows,
+                                  const int *offsets, const int *poff, int E, int C, long pitch,
+                                  long max_pos, uint8_t *q, uint8_t *sc, hipStream_t st) {
+    if (max_pos <= 0 || C <= 0 || E <= 0 || nsrc <= 0) return hipSuccess;
+    const dim3 grid((unsigned)(C / WQ_TN), (unsigned)(max_pos / 128));
+    if (rows)
+        mx_quant_tokens_kernel<true><<<grid, dim3(256), 0, st>>>(src, ld, nsrc, rows, offsets, poff, E, pitch, q, sc);
+    else
+        mx_quant_tokens_kernel<false><<<grid, dim3(256), 0, st>>>(src, ld, nsrc, rows, offsets, poff, E, pitch, q, sc);
     return hipGetLastError();
 }

@@ -32,11 +32,13 @@ class DeviceLayer:
     """All tensors of one layer instance on the GPU, laid out as the C ABI expects."""
 
     def __init__(self, w: Workload, inputs: dict, device="cuda", with_backward=None, mx=False,
-                 ring_rows=None):
+                 ring_rows=None, mx_wgrad=False):
         """ring_rows: run forward/backward in bounded memory, with the per-route
-        activations in a ring of that many rows (None: room for all T*k routes)."""
+        activations in a ring of that many rows (None: room for all T*k routes).
+        mx_wgrad: the MXFP8 backward computes its weight gradients in MXFP8."""
         self.w = w
         self.mx = mx
+        self.mx_wgrad = bool(mx_wgrad)
         self.ring_rows = ring_rows
         self.device = torch.device(device)
         self.with_backward = w.backward if with_backward is None else with_backward
@@ -74,7 +76,8 @@ class DeviceLayer:
         if nbytes == 0:
             raise ValueError(f"unsupported shape {w}")
         if mx:
-            mx_bytes = B.moe_mx_workspace_bytes(self.shape, self.with_backward)
+            mx_bytes = B.moe_mx_workspace_bytes(
+                self.shape, (2 if self.mx_wgrad else 1) if self.with_backward else 0)
             if mx_bytes == 0:
                 raise ValueError(f"shape unsupported in MXFP8 {w}")
             nbytes = max(nbytes, mx_bytes)
@@ -176,7 +179,7 @@ class DeviceLayer:
     def backward_mx(self, stream=None):
         B.moe_backward_mx(self.shape, self.dY, self.X, self.W_r, self.weights, self.mx_bwd_weights,
                           self.topk_idx, self.topk_w, self.plan_bufs, self.dX, self.grads, self.ws,
-                          stream=stream)
+                          stream=stream, wgrad_mxfp8=self.mx_wgrad)
 
     def step_mx(self, stream=None, fwd_events=None):
         """Route, plan, the MXFP8 forward (and the MXFP8 backward)."""

@@ -56,9 +56,11 @@ def test_workspace_sizes(name):
     R = w.T * w.k
     assert fwd >= R * w.f * 2 * 3 + R * w.d * 2           # A, B, H, Yexp at least
     assert bwd >= fwd + R * w.d * 2                       # plus dXperm
-    for which in range(B.WS_DXPERM + 1):
+    for which in list(range(B.WS_DXPERM + 1)) + [B.WS_HW]:
         off, nb = B.moe_workspace_region(sh, True, which)
         assert off % 256 == 0 and off + nb <= bwd
+    off, nb = B.moe_workspace_region(sh, True, B.WS_HW)
+    assert nb == R * w.f * 2 and off >= fwd                  # backward only
 
 
 def test_workspace_zero_for_bad_shapes():
@@ -247,6 +249,18 @@ def test_mx_workspace_and_validation():
         assert off % 256 == 0 and off + nb <= mxb
         assert off >= B.moe_workspace_bytes(sh, True)           # past every BF16 region
     assert B.moe_mx_workspace_bytes(B.make_shape(1 << 20, 4096, 8, 2, 256)) == 0   # T*d >= 2^32
+    # MXFP8 weight gradients: the token-axis operands after everything else
+    mxw = B.moe_mx_workspace_bytes(sh, 2)
+    P = (sh.T * sh.k + 128 * sh.E + 127) // 128 * 128
+    assert mxw >= mxb + (2 * sh.d + 3 * sh.f) * P
+    for which, size in ((B.WS_POFF, (sh.E + 1) * 4), (B.WS_XTQ, sh.d * P), (B.WS_XTS, sh.d * P // 32),
+                        (B.WS_DYTQ, sh.d * P), (B.WS_DYTS, sh.d * P // 32)):
+        off, nb = B.moe_mx_workspace_region(sh, which)
+        assert nb == size and off % 256 == 0 and off >= mxb and off + nb <= mxw, which
+    assert B.moe_mx_workspace_bytes(sh, 3) == 0 and B.moe_mx_workspace_bytes(sh, -1) == 0
+    # d * P >= 2^32 while T*d, T*k*f and E*f*d stay below it
+    big_t = B.make_shape(1 << 18, 4096, 8, 8, 256, 256)
+    assert B.moe_mx_workspace_bytes(big_t, 1) > 0 and B.moe_mx_workspace_bytes(big_t, 2) == 0
     w = B.MoeWeights(None, None, None, FAKE, FAKE, FAKE)          # routed bf16 weights unused
     mx = B.MoeMxWeights(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
     plan = B.MoePlanBufs(FAKE, FAKE, FAKE, FAKE)
@@ -276,12 +290,15 @@ def test_mx_workspace_and_validation():
     qb = B.MoeMxBwdWeights(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
     g = B.MoeGrads(FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE)
 
-    def bwd(q=qb, grads=g, nb=big, dX=FAKE):
-        return L.moe_backward_mx(ctypes.byref(sh), FAKE, FAKE, FAKE, ctypes.byref(wb), ctypes.byref(q),
-                                 FAKE, FAKE, ctypes.byref(plan), dX, ctypes.byref(grads), FAKE, nb,
-                                 None)
+    def bwd(q=qb, grads=g, nb=big, dX=FAKE, wgrad=0, shape=sh):
+        return L.moe_backward_mx(ctypes.byref(shape), FAKE, FAKE, FAKE, ctypes.byref(wb),
+                                 ctypes.byref(q), FAKE, FAKE, ctypes.byref(plan), dX,
+                                 ctypes.byref(grads), wgrad, FAKE, nb, None)
 
     assert bwd(nb=mxb - 1) == B.MOE_ENOSPACE
+    assert bwd(nb=mxw - 1, wgrad=1) == B.MOE_ENOSPACE             # room for the token-axis operands
+    assert bwd(wgrad=2) == B.MOE_EINVAL
+    assert bwd(wgrad=1, shape=big_t) == B.MOE_EUNSUPPORTED
     assert bwd(q=B.MoeMxBwdWeights(FAKE, FAKE, None, FAKE, FAKE, FAKE)) == B.MOE_EINVAL
     assert bwd(grads=B.MoeGrads(FAKE, None, FAKE, FAKE, None, FAKE, FAKE, FAKE)) == B.MOE_EINVAL
     assert bwd(dX=MISALIGNED) == B.MOE_EINVAL

@@ -3,9 +3,10 @@ pre-activations kept, then moe_backward_mx (§3.4 "MXFP8 Support").
 
 Byte work is bit-exact against the oracle wherever both sides quantise the
 same values: dY (per token along d) and the backward weight layouts (W_gate,
-W_up along f; W_down along d).  dA and dB are quantised from the GPU's own
-fp32 values, so they and everything downstream are floats checked against
-the oracle's MXFP8 backward to the usual per-tensor bar.
+W_up along f; W_down along d), and, with the MXFP8 weight gradients, X and dY
+along each expert's tokens.  dA, dB and w h are quantised from the GPU's own
+values, so they and everything downstream are floats checked against the
+oracle's MXFP8 backward to the usual per-tensor bar.
 """
 import numpy as np
 import pytest
@@ -16,15 +17,16 @@ from oracle import mx_oracle as M
 from paper_2609_36070_amd import binding as B
 from paper_2609_36070_amd.layer import DeviceLayer
 from paper_2609_36070_amd.workloads import WORKLOADS, Workload, make_inputs
-from tests.parity import assert_close, check_route_and_plan, say, to_np, weights_dict
+from tests.parity import REL_TOL, assert_close, check_route_and_plan, say, to_np, weights_dict
 
 pytestmark = pytest.mark.gpu
 
 
-def mx_train_layer(w, seed):
+def mx_train_layer(w, seed, wgrad=False):
     inp = make_inputs(w, seed)
-    say(f"[gpu] mx train {w.name} T={w.T} d={w.d} E={w.E} k={w.k} f={w.f} f_s={w.f_s} seed={seed}")
-    L = DeviceLayer(w, inp, mx=True)
+    say(f"[gpu] mx train {w.name} T={w.T} d={w.d} E={w.E} k={w.k} f={w.f} f_s={w.f_s} seed={seed}"
+        f" mxfp8 wgrad={wgrad}")
+    L = DeviceLayer(w, inp, mx=True, mx_wgrad=wgrad)
     assert L.with_backward
     L.step_mx()
     torch.cuda.synchronize()
@@ -40,17 +42,99 @@ def check_bwd_weight_codes(L, inp, experts):
             assert np.array_equal(to_np(sc[e]), scales), f"{key}[{e}] scales"
 
 
-def mx_backward_parity(w, seed):
-    L, inp = mx_train_layer(w, seed)
+def padded_offsets(L, w):
+    """The padded expert offsets: each count rounded up to 128 positions."""
+    counts = to_np(L.counts).astype(np.int64)
+    poff = np.zeros(w.E + 1, np.int64)
+    poff[1:] = np.cumsum((counts + 127) // 128 * 128)
+    assert np.array_equal(to_np(L.mx_ws_tensor(B.WS_POFF, torch.int32, (w.E + 1,))), poff)
+    return poff
+
+
+def check_token_codes(L, inp, w, idx_g, experts, cols=None):
+    """X^T and dY^T quantised along each expert's tokens (32-position blocks
+    from the expert's first row, zeros past its rows), bit-exact against the
+    oracle's quantiser on the same values; cols: a sample of the d columns."""
+    poff = padded_offsets(L, w)
+    _, nbytes = B.moe_mx_workspace_region(L.shape, B.WS_XTQ)
+    P = nbytes // w.d
+    assert P % 128 == 0 and P >= poff[-1]
+    cols = np.arange(w.d) if cols is None else np.asarray(cols)
+    sel = torch.as_tensor(cols, device=L.ws.device)
+    for key, qw, sw in (("X", B.WS_XTQ, B.WS_XTS), ("dY", B.WS_DYTQ, B.WS_DYTS)):
+        q = to_np(L.mx_ws_tensor(qw, torch.uint8, (w.d, P))[sel])
+        sc = to_np(L.mx_ws_tensor(sw, torch.uint8, (w.d, P // 32))[sel])
+        for e in experts:
+            ts = np.nonzero(idx_g == e)[0]              # the expert's rows in plan order
+            n = int(poff[e + 1] - poff[e])
+            v = np.zeros((n, cols.size))
+            v[:ts.size] = inp[key][np.ix_(ts, cols)]
+            codes, scales = M.mx_quantize(v, axis=0)
+            assert np.array_equal(q[:, poff[e]:poff[e + 1]], codes.T), f"{key}^T[{e}] codes"
+            assert np.array_equal(sc[:, poff[e] // 32:poff[e + 1] // 32], scales.T), \
+                f"{key}^T[{e}] scales"
+
+
+def assert_close_fro(name, gpu, ref, rel=REL_TOL):
+    """||gpu - ref||_F <= rel ||ref||_F: the end-to-end bar for the MXFP8
+    weight gradients.  An operand element whose E4M3 rounding goes the other
+    way on one side moves by a whole code step, and a contraction over one
+    expert's tokens does not average that single step away, so the
+    element-wise bar applies to the teacher-forced products instead."""
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    err, scale = np.linalg.norm(gpu - ref), np.linalg.norm(ref)
+    say(f"  {name}: ||err||_F={err:.3e} ||ref||_F={scale:.3e} max|err|={np.abs(gpu - ref).max():.3e}")
+    assert err <= rel * scale if scale > 0 else err <= 1e-6, name
+
+
+def teacher_forced_wgrad(L, inp, w, idx_g, e, cols=None):
+    """dW_gate[e][:, cols], dW_up[e][:, cols], dW_down[e][cols, :] from the
+    GPU's own bf16 dA, dB and w h: the oracle's token-axis quantiser and
+    products, with every rounding decision taken on the values the kernels
+    quantise (token-axis blocks are per column, so a column sample needs only
+    its own operand columns)."""
+    R = w.T * w.k
+    offs = to_np(L.offsets)
+    ts = np.nonzero(idx_g == e)[0]
+    sel = torch.arange(w.f, device=L.ws.device) if cols is None else \
+        torch.as_tensor(np.asarray(cols), device=L.ws.device)
+
+    def rows(which):
+        t = L.mx_ws_tensor(which, torch.bfloat16, (R, w.f))[offs[e]:offs[e + 1]]
+        return to_np(t[:, sel]).astype(np.float64)
+    qt = M.mx_qdq_token_blocks
+    xt = qt(inp["X"][ts])
+    return (xt.T @ qt(rows(B.WS_DA)), xt.T @ qt(rows(B.WS_DB)),
+            qt(rows(B.WS_HW)).T @ qt(inp["dY"][ts]))
+
+
+def mx_backward_parity(w, seed, wgrad=False):
+    L, inp = mx_train_layer(w, seed, wgrad)
     Zo, idx_g = check_route_and_plan(L, inp, w)
     w_orc = O.gate_weights(Zo, idx_g)
     check_bwd_weight_codes(L, inp, range(w.E))
     dyq, dys = M.mx_quantize(inp["dY"], axis=1)
     assert np.array_equal(to_np(L.mx_ws_tensor(B.WS_DYQ, torch.uint8, (w.T, w.d))), dyq)
     assert np.array_equal(to_np(L.mx_ws_tensor(B.WS_DYS, torch.uint8, (w.T, w.d // 32))), dys)
-    g = M.moe_backward_mx(inp["X"], inp["W_r"], weights_dict(inp), idx_g, w_orc, inp["dY"])
-    for n in ("dX", "dW_gate", "dW_up", "dW_down", "dZ", "dW_r"):
+    if wgrad:
+        check_token_codes(L, inp, w, idx_g, range(w.E))
+    g = M.moe_backward_mx(inp["X"], inp["W_r"], weights_dict(inp), idx_g, w_orc, inp["dY"],
+                          wgrad_mx=wgrad)
+    for n in ("dX", "dZ", "dW_r"):
         assert_close(n, to_np(getattr(L, n)), g[n])
+    wg = ("dW_gate", "dW_up", "dW_down")
+    if wgrad:
+        tf = [np.zeros(getattr(L, n).shape) for n in wg]
+        for e in range(w.E):
+            for i, v in enumerate(teacher_forced_wgrad(L, inp, w, idx_g, e)):
+                tf[i][e] = v
+        for n, ref in zip(wg, tf):
+            assert_close(f"{n} (the GPU's dA, dB, w h)", to_np(getattr(L, n)), ref)
+            assert_close_fro(n, to_np(getattr(L, n)), g[n])
+    else:
+        for n in wg:
+            assert_close(n, to_np(getattr(L, n)), g[n])
     R = w.T * w.k
     dg_pos = to_np(L.mx_ws_tensor(B.WS_DG, torch.float32, (R,)))
     rp = to_np(L.route_pos)[:R]
@@ -62,24 +146,57 @@ def mx_backward_parity(w, seed):
     return L, inp
 
 
-def test_mx_backward_ragged():
+@pytest.mark.parametrize("wgrad", [False, True], ids=["bf16_wgrad", "mxfp8_wgrad"])
+def test_mx_backward_ragged(wgrad):
     mx_backward_parity(Workload("mx_ragged_train", T=1000, d=512, E=6, k=2, f=512, f_s=256,
-                                bias_std=0.5, backward=True), seed=31)
+                                bias_std=0.5, backward=True), seed=31, wgrad=wgrad)
 
 
-@pytest.mark.parametrize("w", [
+EDGE = [
     Workload("mx_one_token", T=1, d=256, E=8, k=3, f=256, f_s=256, backward=True),
     Workload("mx_k_equals_E", T=300, d=256, E=4, k=4, f=512, bias_std=0.5, backward=True),
     Workload("mx_empty_experts", T=40, d=256, E=64, k=1, f=256, bias_std=3.0, backward=True),
     Workload("mx_many_tiles", T=700, d=768, E=3, k=2, f=768, backward=True),
-], ids=lambda w: w.name)
+]
+
+
+@pytest.mark.parametrize("w", EDGE, ids=lambda w: w.name)
 def test_mx_backward_edge_shapes(w):
     mx_backward_parity(w, seed=32)
 
 
-def test_mx_backward_no_tokens():
+@pytest.mark.parametrize("w", EDGE + [
+    Workload("mx_wgrad_block_edges", T=160, d=512, E=5, k=3, f=256, f_s=256, bias_std=1.0,
+             backward=True),
+], ids=lambda w: w.name)
+def test_mx_wgrad_edge_shapes(w):
+    """MXFP8 weight gradients: one token per expert, every expert holding
+    every token, empty experts, several tiles each way, ragged counts."""
+    mx_backward_parity(w, seed=34, wgrad=True)
+
+
+def test_mx_wgrad_changes_only_weight_gradients():
+    """The switch changes the three routed weight gradients and nothing else
+    (bit-exact), and they stay close to the BF16 ones."""
+    w = Workload("mx_switch_train", T=600, d=512, E=4, k=2, f=512, f_s=256, bias_std=0.5,
+                 backward=True)
+    L, _ = mx_train_layer(w, 35, wgrad=True)
+    names = ("Y", "dX", "dW_r", "dZ", "dWg_s", "dWu_s", "dWd_s")
+    on = {n: getattr(L, n).clone() for n in names + ("dW_gate", "dW_up", "dW_down")}
+    L.mx_wgrad = False
+    L.step_mx()
+    torch.cuda.synchronize()
+    for n in names:
+        assert torch.equal(getattr(L, n), on[n]), n
+    for n in ("dW_gate", "dW_up", "dW_down"):
+        assert not torch.equal(getattr(L, n), on[n]), n
+        assert_close(f"{n} mxfp8 vs bf16", to_np(on[n]), to_np(getattr(L, n)), rel=0.2)
+
+
+@pytest.mark.parametrize("wgrad", [False, True], ids=["bf16_wgrad", "mxfp8_wgrad"])
+def test_mx_backward_no_tokens(wgrad):
     w = Workload("mx_none_train", T=0, d=256, E=4, k=2, f=256, f_s=256, backward=True)
-    L = DeviceLayer(w, make_inputs(w, 0), mx=True)
+    L = DeviceLayer(w, make_inputs(w, 0), mx=True, mx_wgrad=wgrad)
     for n in ("dW_gate", "dW_up", "dW_down", "dW_r", "dWg_s", "dWu_s", "dWd_s"):
         getattr(L, n).fill_(3.0)
     L.step_mx()
@@ -88,10 +205,11 @@ def test_mx_backward_no_tokens():
         assert torch.count_nonzero(getattr(L, n)) == 0, n
 
 
-def test_mx_backward_determinism():
+@pytest.mark.parametrize("wgrad", [False, True], ids=["bf16_wgrad", "mxfp8_wgrad"])
+def test_mx_backward_determinism(wgrad):
     w = Workload("mx_det_train", T=1000, d=512, E=6, k=2, f=512, f_s=256, bias_std=0.5,
                  backward=True)
-    L, _ = mx_train_layer(w, 33)
+    L, _ = mx_train_layer(w, 33, wgrad)
     names = ("Y", "dX", "dW_gate", "dW_up", "dW_down", "dW_r", "dZ", "dWg_s", "dWu_s", "dWd_s")
     first = {n: getattr(L, n).clone() for n in names}
     for _ in range(3):
@@ -101,15 +219,20 @@ def test_mx_backward_determinism():
             assert torch.equal(getattr(L, n), first[n]), n
 
 
-def test_mx_training_step_full_size_sampled():
+@pytest.mark.parametrize("wgrad", [False, True], ids=["bf16_wgrad", "mxfp8_wgrad"])
+def test_mx_training_step_full_size_sampled(wgrad):
     """The training workload in MXFP8: the backward weight codes of two
-    experts bit-exact; sampled token rows of dX, dZ and dg, and weight-gradient
-    columns of two experts, against the oracle's per-token / per-column MXFP8
-    backward."""
+    experts bit-exact (with the MXFP8 weight gradients also X^T and dY^T of
+    two experts on sampled columns); sampled token rows of dX, dZ and dg, and
+    weight-gradient columns of two experts, against the oracle's per-token /
+    per-column MXFP8 backward."""
     w = WORKLOADS["large_shared_train"]
-    L, inp = mx_train_layer(w, 0)
+    L, inp = mx_train_layer(w, 0, wgrad)
     check_bwd_weight_codes(L, inp, [0, w.E - 1])
     Zo, idx_g = check_route_and_plan(L, inp, w)
+    if wgrad:
+        check_token_codes(L, inp, w, idx_g, [0, w.E - 1],
+                          cols=np.r_[0:32, 3000:3008, w.d - 32:w.d])
     w_orc = O.gate_weights(Zo, idx_g)
     W = weights_dict(inp, as_f64=True)
     rng = np.random.default_rng(6)
@@ -123,8 +246,17 @@ def test_mx_training_step_full_size_sampled():
     assert_close("dg[sampled tokens]", dg_pos[rp[toks]], dg)
     cols = np.array([0, 777, w.f - 1])
     for e in (0, w.E - 1):
-        a, b, c = M.mx_expert_weight_grad_columns(inp["X"], W, idx_g, w_orc, inp["dY"], e, cols)
-        assert_close(f"dW_gate[{e}][:, cols]", to_np(L.dW_gate[e])[:, cols], a)
-        assert_close(f"dW_up[{e}][:, cols]", to_np(L.dW_up[e])[:, cols], b)
-        assert_close(f"dW_down[{e}][cols, :]", to_np(L.dW_down[e])[cols, :], c)
+        a, b, c = M.mx_expert_weight_grad_columns(inp["X"], W, idx_g, w_orc, inp["dY"], e, cols,
+                                                  wgrad_mx=wgrad)
+        got = (to_np(L.dW_gate[e])[:, cols], to_np(L.dW_up[e])[:, cols],
+               to_np(L.dW_down[e])[cols, :])
+        names = (f"dW_gate[{e}][:, cols]", f"dW_up[{e}][:, cols]", f"dW_down[{e}][cols, :]")
+        if wgrad:
+            for n, gv, ref in zip(names, got, teacher_forced_wgrad(L, inp, w, idx_g, e, cols)):
+                assert_close(f"{n} (the GPU's dA, dB, w h)", gv, ref)
+            for n, gv, ref in zip(names, got, (a, b, c)):
+                assert_close_fro(n, gv, ref)
+        else:
+            for n, gv, ref in zip(names, got, (a, b, c)):
+                assert_close(n, gv, ref)
     assert L.error_word() == 0
