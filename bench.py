@@ -198,37 +198,48 @@ def mx_forward_timing(H, stream, inputs, steps, warmup):
 
 def mx_training_timing(H, stream, inputs, steps, warmup):
     """route + plan + moe_forward_mx (pre-activations kept) + moe_backward_mx
-    on the training workload; the routed weights are pre-quantised once (both
-    layouts), outside the timing."""
+    on the training workload, with the weight gradients in BF16 and, on the
+    same layer, in MXFP8 (wgrad_mxfp8), in alternating blocks of `steps`
+    steps; the routed weights are pre-quantised once (both layouts), outside
+    the timing."""
     import torch
     from paper_2609_36070_amd.layer import DeviceLayer
     from paper_2609_36070_amd.workloads import WORKLOADS
     w = WORKLOADS["large_shared_train"]
-    L = DeviceLayer(w, inputs, mx=True)
-    for _ in range(warmup):
-        L.step_mx()
+    L = DeviceLayer(w, inputs, mx=True, mx_wgrad=True)
+    for wg in (False, True):
+        L.mx_wgrad = wg
+        for _ in range(warmup):
+            L.step_mx()
     torch.cuda.synchronize()
     a, m, b = H.create(), H.create(), H.create()
-    fwd = bwd = 0.0
-    for _ in range(steps):
-        H.record(a, stream)
-        L.route()
-        L.plan()
-        L.forward_mx()
-        H.record(m, stream)
-        L.backward_mx()
-        H.record(b, stream)
-        H.sync(b)
-        fwd += H.ms(a, m)
-        bwd += H.ms(m, b)
+    tot = {False: [0.0, 0.0, 0], True: [0.0, 0.0, 0]}
+    for wg in (False, True, False, True):
+        L.mx_wgrad = wg
+        for _ in range(steps):
+            H.record(a, stream)
+            L.route()
+            L.plan()
+            L.forward_mx()
+            H.record(m, stream)
+            L.backward_mx()
+            H.record(b, stream)
+            H.sync(b)
+            tot[wg][0] += H.ms(a, m)
+            tot[wg][1] += H.ms(m, b)
+            tot[wg][2] += 1
     for e in (a, m, b):
         H.destroy(e)
-    fwd /= steps
-    bwd /= steps
     flops = w.fwd_flops() + w.bwd_flops()
-    out = {"workload": w.name, "forward_ms": round(fwd, 4), "backward_ms": round(bwd, 4),
-           "ms_per_step": round(fwd + bwd, 4),
-           "tflops": round(flops / ((fwd + bwd) * 1e-3) / 1e12, 2), "error_word": L.error_word()}
+
+    def entry(wg):
+        fwd, bwd, n = tot[wg]
+        fwd, bwd = fwd / n, bwd / n
+        return {"forward_ms": round(fwd, 4), "backward_ms": round(bwd, 4),
+                "ms_per_step": round(fwd + bwd, 4),
+                "tflops": round(flops / ((fwd + bwd) * 1e-3) / 1e12, 2)}
+    out = {"workload": w.name, **entry(False), "wgrad_mxfp8": entry(True),
+           "error_word": L.error_word()}
     del L
     torch.cuda.synchronize()
     return out
@@ -550,8 +561,12 @@ def main():
     if not args.no_mx and w.name == "large_shared_train":
         mxt = mx_training_timing(H, stream, inputs, max(3, args.steps // 2), 2)
         mxt["speedup_vs_bf16_step"] = round(ms_step / mxt["ms_per_step"], 3)
+        mw = mxt["wgrad_mxfp8"]
+        mw["speedup_vs_bf16_step"] = round(ms_step / mw["ms_per_step"], 3)
         log(f"[bench] MXFP8 training step: {mxt['ms_per_step']:.3f} ms (forward {mxt['forward_ms']:.3f}, "
             f"backward {mxt['backward_ms']:.3f}; {mxt['tflops']} TFLOP/s), BF16 step {ms_step:.3f} ms")
+        log(f"[bench]   with MXFP8 weight gradients: {mw['ms_per_step']:.3f} ms (backward "
+            f"{mw['backward_ms']:.3f}; {mw['tflops']} TFLOP/s, {mw['speedup_vs_bf16_step']}x the BF16 step)")
 
     fused = None
     if not args.no_fused:
