@@ -124,9 +124,27 @@ __global__ __launch_bounds__(64) void mx_pad_offsets_kernel(const int *__restric
 
 // Grid (C / 256, max_pos / 128).  Block: 256 threads; thread t owns column
 // c0 + t of the 128 padded positions [p0, p0 + 128) of one expert: four
-// 32-position blocks, each staged through LDS (32 rows x 256 columns), whose
-// codes stay in registers until one 128-byte row segment and one word of 4
-// scales are written.
+// 32-position blocks, each staged through LDS (32 rows x 256 columns; the
+// next block's rows are loaded into registers meanwhile).  The codes stay in
+// registers until all four blocks are done; then they go through LDS once
+// more, so that every store instruction writes whole 128-byte row segments
+// (8 columns per wave instruction) instead of 16 bytes in 64 rows.
+constexpr int TQ_OPITCH = 144;   // LDS bytes per column of codes (+16: conflict-free 16-byte writes)
+
+// Rows 32 sb .. 32 sb + 31 of the block's 128 positions (r < 0: zeros), 8
+// bf16 columns per chunk, 4 chunks per thread.
+DEV void tq_fetch(const uint16_t *__restrict__ src, long ld, const int *s_row, int sb, int c0, int t,
+                  u32x4_t *v) {
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const int ch = it * 256 + t;
+        const int r = ch / 32, c = 8 * (ch % 32);
+        const int row = s_row[32 * sb + r];
+        v[it] = u32x4_t{0, 0, 0, 0};
+        if (row >= 0) v[it] = ld_u32x4(src + (long)row * ld + c0 + c);
+    }
+}
+
 template <bool GATHER>
 __global__ __launch_bounds__(256) void mx_quant_tokens_kernel(const uint16_t *__restrict__ src, long ld,
                                                               long nsrc, const int *__restrict__ rows,
@@ -134,7 +152,10 @@ __global__ __launch_bounds__(256) void mx_quant_tokens_kernel(const uint16_t *__
                                                               const int *__restrict__ poff, int E,
                                                               long pitch, uint8_t *__restrict__ q,
                                                               uint8_t *__restrict__ sc) {
-    __shared__ __attribute__((aligned(16))) uint16_t tile[32 * WQ_PITCH];
+    // the staged 32 x 256 input block, and at the end the 256 x 128 codes
+    __shared__ __attribute__((aligned(16))) uint8_t lds[256 * TQ_OPITCH];
+    static_assert(32 * WQ_PITCH * 2 <= 256 * TQ_OPITCH, "the input block fits the code buffer");
+    uint16_t *tile = reinterpret_cast<uint16_t *>(lds);
     __shared__ int s_row[128];
     const int t = threadIdx.x;
     const int c0 = blockIdx.x * WQ_TN;
@@ -157,22 +178,21 @@ __global__ __launch_bounds__(256) void mx_quant_tokens_kernel(const uint16_t *__
         }
         s_row[t] = r;
     }
+    __syncthreads();
+    u32x4_t pf[4];
+    tq_fetch(src, ld, s_row, 0, c0, t, pf);
     uint32_t codes[32];
     uint32_t scw = 0;
 #pragma unroll
     for (int sb = 0; sb < 4; ++sb) {
-        __syncthreads();                        // s_row written / tile free
-        // 32 rows x 256 columns: 1024 chunks of 8 bf16, 4 per thread, coalesced
+        if (sb > 0) __syncthreads();            // the previous block's column reads are done
 #pragma unroll
         for (int it = 0; it < 4; ++it) {
             const int ch = it * 256 + t;
-            const int r = ch / 32, c = 8 * (ch % 32);
-            const int row = s_row[32 * sb + r];
-            u32x4_t v = u32x4_t{0, 0, 0, 0};
-            if (row >= 0) v = ld_u32x4(src + (long)row * ld + c0 + c);
-            st_u32x4(tile + r * WQ_PITCH + c, v);
+            st_u32x4(tile + (ch / 32) * WQ_PITCH + 8 * (ch % 32), pf[it]);
         }
         __syncthreads();
+        if (sb < 3) tq_fetch(src, ld, s_row, sb + 1, c0, t, pf);
         float v[32];
         float amax = 0.f;
 #pragma unroll
@@ -192,10 +212,18 @@ __global__ __launch_bounds__(256) void mx_quant_tokens_kernel(const uint16_t *__
         }
         scw |= (uint32_t)(s + 127) << (8 * sb);
     }
-    uint8_t *dst = q + (long)(c0 + t) * pitch + p0;
+    __syncthreads();                            // every column read of the last block is done
 #pragma unroll
     for (int w = 0; w < 8; ++w)
-        st_u32x4(dst + 16 * w, u32x4_t{codes[4 * w], codes[4 * w + 1], codes[4 * w + 2], codes[4 * w + 3]});
+        st_u32x4(lds + t * TQ_OPITCH + 16 * w,
+                 u32x4_t{codes[4 * w], codes[4 * w + 1], codes[4 * w + 2], codes[4 * w + 3]});
+    __syncthreads();
+    // pass i: thread t writes bytes 16 (t % 8) .. + 15 of column 32 i + t / 8
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int cr = 32 * i + (t >> 3), chunk = t & 7;
+        st_u32x4(q + (long)(c0 + cr) * pitch + p0 + 16 * chunk, ld_u32x4(lds + cr * TQ_OPITCH + 16 * chunk));
+    }
     *reinterpret_cast<uint32_t *>(sc + (long)(c0 + t) * (pitch / 32) + p0 / 32) = scw;
 }
 
