@@ -13,7 +13,7 @@
 //   mx_quant_rows:    rows of a K-contiguous bf16 matrix (tokens of X); each
 //                     lane takes 8 elements, 4 lanes share a block.
 //   mx_quant_weights: [E][K][N] bf16 weights -> K-contiguous [E][N][K] codes
-//                     and [E][N][K/32] scales (a 32 x 256 tile transposed
+//                     and [E][N][K/32] scales (128 x 256 tiles transposed
 //                     through LDS), the operand layout of the fp8 GEMMs.
 //   mx_quant_tokens:  the weight-gradient operands, which contract over an
 //                     expert's tokens: rows of the expert's plan region in
@@ -63,43 +63,6 @@ __global__ __launch_bounds__(256) void mx_quant_rows_kernel(const uint16_t *__re
 constexpr int WQ_TN = 256;            // output rows (weight columns) per block
 constexpr int WQ_PITCH = WQ_TN + 8;   // LDS pitch in bf16 (16-byte rows)
 
-// Grid (N / 256, K / 32, E).  Block: 256 threads, thread t owns weight column
-// n0 + t for the 32 k rows of this block.
-__global__ __launch_bounds__(256) void mx_quant_weights_kernel(const uint16_t *__restrict__ W, int K,
-                                                               int N, uint8_t *__restrict__ q,
-                                                               uint8_t *__restrict__ sc) {
-    __shared__ __attribute__((aligned(16))) uint16_t tile[32 * WQ_PITCH];
-    const int t = threadIdx.x;
-    const int n0 = blockIdx.x * WQ_TN, k0 = blockIdx.y * 32, e = blockIdx.z;
-    const uint16_t *src = W + ((long)e * K + k0) * N + n0;
-    // 32 rows x 256 columns: 1024 chunks of 8 bf16, 4 per thread, coalesced
-#pragma unroll
-    for (int it = 0; it < 4; ++it) {
-        const int ch = it * 256 + t;
-        const int r = ch / 32, c = 8 * (ch % 32);
-        st_u32x4(tile + r * WQ_PITCH + c, ld_u32x4(src + (long)r * N + c));
-    }
-    __syncthreads();
-    float v[32];
-    float amax = 0.f;
-#pragma unroll
-    for (int r = 0; r < 32; ++r) {
-        v[r] = bf2f(tile[r * WQ_PITCH + t]);
-        amax = fmaxf(amax, fabsf(v[r]));
-    }
-    const int s = mx_shared_exp(amax);
-    const long n = n0 + t;
-    uint8_t *dst = q + ((long)e * N + n) * K + k0;
-#pragma unroll
-    for (int h = 0; h < 4; ++h) {
-        float part[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) part[j] = v[8 * h + j];
-        *reinterpret_cast<u32x2_t *>(dst + 8 * h) = e4m3_pack8(part, s);
-    }
-    sc[((long)e * N + n) * (K / 32) + k0 / 32] = (uint8_t)(s + 127);
-}
-
 // Padded expert regions: poff[e] = sum over e' < e of count(e') rounded up
 // to 128; poff[E] = the padded total.  One wave, a scan per 64 experts.
 __global__ __launch_bounds__(64) void mx_pad_offsets_kernel(const int *__restrict__ offsets, int E,
@@ -122,16 +85,18 @@ __global__ __launch_bounds__(64) void mx_pad_offsets_kernel(const int *__restric
     if (lane == 0) poff[E] = cum;
 }
 
-// Grid (C / 256, max_pos / 128).  Block: 256 threads; thread t owns column
-// c0 + t of the 128 padded positions [p0, p0 + 128) of one expert: four
-// 32-position blocks, each staged through LDS (32 rows x 256 columns; the
-// next block's rows are loaded into registers meanwhile).  The codes stay in
+// Quantisation along the rows of a bf16 matrix, 128 rows x 256 columns per
+// workgroup: thread t owns column c0 + t and quantises its four 32-row MX
+// blocks.  Each block is staged through LDS (32 rows x 256 columns; the next
+// block's rows are loaded into registers meanwhile).  The codes stay in
 // registers until all four blocks are done; then they go through LDS once
 // more, so that every store instruction writes whole 128-byte row segments
-// (8 columns per wave instruction) instead of 16 bytes in 64 rows.
+// (8 columns per wave instruction) instead of 16 bytes in each of 64 rows.
 constexpr int TQ_OPITCH = 144;   // LDS bytes per column of codes (+16: conflict-free 16-byte writes)
+constexpr int TQ_LDS = 256 * TQ_OPITCH;
+static_assert(32 * WQ_PITCH * 2 <= TQ_LDS, "the input block fits the code buffer");
 
-// Rows 32 sb .. 32 sb + 31 of the block's 128 positions (r < 0: zeros), 8
+// Rows 32 sb .. 32 sb + 31 of the 128 (s_row: source row, < 0 for zeros), 8
 // bf16 columns per chunk, 4 chunks per thread.
 DEV void tq_fetch(const uint16_t *__restrict__ src, long ld, const int *s_row, int sb, int c0, int t,
                   u32x4_t *v) {
@@ -145,39 +110,13 @@ DEV void tq_fetch(const uint16_t *__restrict__ src, long ld, const int *s_row, i
     }
 }
 
-template <bool GATHER>
-__global__ __launch_bounds__(256) void mx_quant_tokens_kernel(const uint16_t *__restrict__ src, long ld,
-                                                              long nsrc, const int *__restrict__ rows,
-                                                              const int *__restrict__ offsets,
-                                                              const int *__restrict__ poff, int E,
-                                                              long pitch, uint8_t *__restrict__ q,
-                                                              uint8_t *__restrict__ sc) {
-    // the staged 32 x 256 input block, and at the end the 256 x 128 codes
-    __shared__ __attribute__((aligned(16))) uint8_t lds[256 * TQ_OPITCH];
-    static_assert(32 * WQ_PITCH * 2 <= 256 * TQ_OPITCH, "the input block fits the code buffer");
+// The 128 source rows are s_row[0..127] (written before the call, visible
+// after its first barrier).  Column c's 128 codes go to q + c * pitch (c
+// counted from c0) and its 4 scales to the 4 bytes at sc + c * spitch.
+DEV void quant_cols128(const uint16_t *__restrict__ src, long ld, const int *s_row, int c0, int t,
+                       uint8_t *lds, uint8_t *__restrict__ q, long pitch, uint8_t *__restrict__ sc,
+                       long spitch) {
     uint16_t *tile = reinterpret_cast<uint16_t *>(lds);
-    __shared__ int s_row[128];
-    const int t = threadIdx.x;
-    const int c0 = blockIdx.x * WQ_TN;
-    const int p0 = blockIdx.y * 128;
-    if (p0 >= poff[E]) return;                 // past the padded total (uniform)
-    // the expert whose padded region holds p0: the last e with poff[e] <= p0
-    int lo = 0, hi = E - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (poff[mid] <= p0) lo = mid;
-        else hi = mid - 1;
-    }
-    const int base = offsets[lo], cnt = offsets[lo + 1] - base;
-    if (t < 128) {
-        const int local = p0 - poff[lo] + t;
-        int r = -1;                             // padding: zeros
-        if (local < cnt) {
-            r = GATHER ? rows[base + local] : base + local;
-            r = r < 0 ? 0 : (r >= nsrc ? (int)nsrc - 1 : r);   // a malformed plan stays in bounds
-        }
-        s_row[t] = r;
-    }
     __syncthreads();
     u32x4_t pf[4];
     tq_fetch(src, ld, s_row, 0, c0, t, pf);
@@ -222,9 +161,61 @@ __global__ __launch_bounds__(256) void mx_quant_tokens_kernel(const uint16_t *__
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const int cr = 32 * i + (t >> 3), chunk = t & 7;
-        st_u32x4(q + (long)(c0 + cr) * pitch + p0 + 16 * chunk, ld_u32x4(lds + cr * TQ_OPITCH + 16 * chunk));
+        st_u32x4(q + (long)cr * pitch + 16 * chunk, ld_u32x4(lds + cr * TQ_OPITCH + 16 * chunk));
     }
-    *reinterpret_cast<uint32_t *>(sc + (long)(c0 + t) * (pitch / 32) + p0 / 32) = scw;
+    *reinterpret_cast<uint32_t *>(sc + (long)t * spitch) = scw;
+}
+
+// Grid (N / 256, K / 128, E): W [E][K][N] -> K-contiguous codes [E][N][K] and
+// scales [E][N][K / 32], the operand layout of the fp8 GEMMs.
+__global__ __launch_bounds__(256) void mx_quant_weights_kernel(const uint16_t *__restrict__ W, int K,
+                                                               int N, uint8_t *__restrict__ q,
+                                                               uint8_t *__restrict__ sc) {
+    __shared__ __attribute__((aligned(16))) uint8_t lds[TQ_LDS];
+    __shared__ int s_row[128];
+    const int t = threadIdx.x;
+    const int c0 = blockIdx.x * WQ_TN, k0 = blockIdx.y * 128, e = blockIdx.z;
+    if (t < 128) s_row[t] = k0 + t;
+    const long col0 = (long)e * N + c0;
+    quant_cols128(W + (long)e * K * N, N, s_row, c0, t, lds, q + col0 * K + k0, K,
+                  sc + col0 * (K / 32) + k0 / 32, K / 32);
+}
+
+// Grid (C / 256, max_pos / 128): the 128 padded positions [p0, p0 + 128) of
+// one expert, rows of its plan region (gathered through `rows` when GATHER)
+// or zeros past its count.
+template <bool GATHER>
+__global__ __launch_bounds__(256) void mx_quant_tokens_kernel(const uint16_t *__restrict__ src, long ld,
+                                                              long nsrc, const int *__restrict__ rows,
+                                                              const int *__restrict__ offsets,
+                                                              const int *__restrict__ poff, int E,
+                                                              long pitch, uint8_t *__restrict__ q,
+                                                              uint8_t *__restrict__ sc) {
+    __shared__ __attribute__((aligned(16))) uint8_t lds[TQ_LDS];
+    __shared__ int s_row[128];
+    const int t = threadIdx.x;
+    const int c0 = blockIdx.x * WQ_TN;
+    const int p0 = blockIdx.y * 128;
+    if (p0 >= poff[E]) return;                 // past the padded total (uniform)
+    // the expert whose padded region holds p0: the last e with poff[e] <= p0
+    int lo = 0, hi = E - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (poff[mid] <= p0) lo = mid;
+        else hi = mid - 1;
+    }
+    const int base = offsets[lo], cnt = offsets[lo + 1] - base;
+    if (t < 128) {
+        const int local = p0 - poff[lo] + t;
+        int r = -1;                             // padding: zeros
+        if (local < cnt) {
+            r = GATHER ? rows[base + local] : base + local;
+            r = r < 0 ? 0 : (r >= nsrc ? (int)nsrc - 1 : r);   // a malformed plan stays in bounds
+        }
+        s_row[t] = r;
+    }
+    quant_cols128(src, ld, s_row, c0, t, lds, q + (long)c0 * pitch + p0, pitch,
+                  sc + (long)c0 * (pitch / 32) + p0 / 32, pitch / 32);
 }
 
 }  // namespace
@@ -241,7 +232,7 @@ hipError_t launch_mx_quant_rows(const uint16_t *X, long rows, int K, uint8_t *q,
 hipError_t launch_mx_quant_weights(const uint16_t *W, int E, int K, int N, uint8_t *q, uint8_t *sc,
                                    hipStream_t st) {
     if (E <= 0) return hipSuccess;
-    mx_quant_weights_kernel<<<dim3(N / WQ_TN, K / 32, E), dim3(256), 0, st>>>(W, K, N, q, sc);
+    mx_quant_weights_kernel<<<dim3(N / WQ_TN, K / 128, E), dim3(256), 0, st>>>(W, K, N, q, sc);
     return hipGetLastError();
 }
 
