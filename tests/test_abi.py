@@ -61,6 +61,8 @@ def test_workspace_sizes(name):
         assert off % 256 == 0 and off + nb <= bwd
     off, nb = B.moe_workspace_region(sh, True, B.WS_HW)
     assert nb == R * w.f * 2 and off >= fwd                  # backward only
+    with pytest.raises(B.MoeError):
+        B.moe_workspace_region(sh, False, B.WS_HW)
 
 
 def test_workspace_zero_for_bad_shapes():
