@@ -168,11 +168,47 @@ def test_mx_backward_edge_shapes(w):
 @pytest.mark.parametrize("w", EDGE + [
     Workload("mx_wgrad_block_edges", T=160, d=512, E=5, k=3, f=256, f_s=256, bias_std=1.0,
              backward=True),
+    Workload("mx_sixteen_experts", T=333, d=768, E=16, k=5, f=256, f_s=256, backward=True),
 ], ids=lambda w: w.name)
 def test_mx_wgrad_edge_shapes(w):
     """MXFP8 weight gradients: one token per expert, every expert holding
     every token, empty experts, several tiles each way, ragged counts."""
     mx_backward_parity(w, seed=34, wgrad=True)
+
+
+def test_mx_wgrad_block_aligned_counts():
+    """Routes forced so that the experts hold exactly 128, 32, 96, 0 and 256
+    rows: regions with no padding, a single 32-block, a partial 128-span, an
+    empty expert and two full spans.  The weights are the restricted softmax
+    of the GPU's logits over the forced sets."""
+    w = Workload("mx_aligned_train", T=256, d=256, E=5, k=2, f=256, f_s=256, backward=True)
+    inp = make_inputs(w, 36)
+    say(f"[gpu] mx train {w.name} forced counts 128/32/96/0/256, mxfp8 wgrad")
+    L = DeviceLayer(w, inp, mx=True, mx_wgrad=True)
+    idx = np.empty((w.T, w.k), np.int32)
+    idx[:, 1] = 4
+    idx[:128, 0], idx[128:160, 0], idx[160:, 0] = 0, 1, 2
+    L.route()
+    torch.cuda.synchronize()
+    wts = O.gate_weights(to_np(L.logits), idx).astype(np.float32)
+    L.topk_idx.copy_(torch.from_numpy(idx))
+    L.topk_w.copy_(torch.from_numpy(wts))
+    L.plan()
+    L.forward_mx()
+    L.backward_mx()
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(L.counts), [128, 32, 96, 0, 256])
+    check_token_codes(L, inp, w, idx, range(w.E))
+    g = M.moe_backward_mx(inp["X"], inp["W_r"], weights_dict(inp), idx, wts.astype(np.float64),
+                          inp["dY"], wgrad_mx=True)
+    for n in ("dX", "dZ", "dW_r", "dWg_s", "dWu_s", "dWd_s"):
+        assert_close(n, to_np(getattr(L, n)), g[n])
+    for i, n in enumerate(("dW_gate", "dW_up", "dW_down")):
+        tf = np.stack([teacher_forced_wgrad(L, inp, w, idx, e)[i] for e in range(w.E)])
+        assert_close(f"{n} (the GPU's dA, dB, w h)", to_np(getattr(L, n)), tf)
+        assert_close_fro(n, to_np(getattr(L, n)), g[n])
+    assert torch.count_nonzero(L.dW_gate[3]) == 0 and torch.count_nonzero(L.dW_down[3]) == 0
+    assert L.error_word() == 0
 
 
 def test_mx_wgrad_changes_only_weight_gradients():
