@@ -256,6 +256,40 @@ def test_mx_backward_determinism(wgrad):
 
 
 @pytest.mark.parametrize("wgrad", [False, True], ids=["bf16_wgrad", "mxfp8_wgrad"])
+def test_mx_training_graph_replay(wgrad):
+    """route + plan + the MXFP8 forward and backward captured in one HIP
+    graph.  Before each replay every output and the whole workspace are
+    overwritten by eager fills; every replay equals the eager step bitwise."""
+    w = Workload("mx_graph_train", T=500, d=512, E=6, k=2, f=512, f_s=256, bias_std=0.5,
+                 backward=True)
+    L, _ = mx_train_layer(w, 37, wgrad)
+    names = ("logits", "topk_idx", "topk_w", "counts", "offsets", "perm", "route_pos", "Y", "dX",
+             "dW_gate", "dW_up", "dW_down", "dW_r", "dZ", "dWg_s", "dWu_s", "dWd_s")
+    eager = {n: getattr(L, n).clone() for n in names}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        L.step_mx()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        L.step_mx()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for n in names:
+            getattr(L, n).fill_(-7 if getattr(L, n).dtype == torch.int32 else 3.0)
+        L.ws.fill_(0xA5)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for n in names:
+            assert torch.equal(getattr(L, n), eager[n]), (rep, n)
+    assert L.error_word() == 0
+    say("  graph replays bitwise equal to eager")
+
+
+@pytest.mark.parametrize("wgrad", [False, True], ids=["bf16_wgrad", "mxfp8_wgrad"])
 def test_mx_training_step_full_size_sampled(wgrad):
     """The training workload in MXFP8: the backward weight codes of two
     experts bit-exact (with the MXFP8 weight gradients also X^T and dY^T of
