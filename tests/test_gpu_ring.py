@@ -123,6 +123,7 @@ def test_ring_determinism_and_graph_replay():
     for rep in range(3):
         for n in names:
             getattr(ring, n).fill_(-7 if getattr(ring, n).dtype == torch.int32 else 3.0)
+        ring.ws.fill_(0xA5)
         torch.cuda.synchronize()
         graph.replay()
         torch.cuda.synchronize()

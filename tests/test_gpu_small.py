@@ -183,6 +183,7 @@ def test_graph_capture_replays_match_eager():
     for rep in range(3):
         for n in names:                     # eager work between replays: clobber every output
             getattr(L, n).fill_(-7 if getattr(L, n).dtype == torch.int32 else 3.0)
+        L.ws.fill_(0xA5)                    # and the workspace: nothing carries over between steps
         torch.cuda.synchronize()
         graph.replay()
         torch.cuda.synchronize()
