@@ -35,8 +35,8 @@ F64 = np.float64
 
 
 # ---------------------------------------------------------------------------
-# Router (§2.1: "a router projection to select the top-k routed experts and
-# assign each a router weight")
+# Router (§2.1: the router's projection picks a token's top-k routed experts
+# and gives each of them a weight)
 # ---------------------------------------------------------------------------
 
 def router_logits(X, W_r, bias=None, out_dtype=np.float32):
@@ -91,52 +91,34 @@ def gate_weights(Z, idx):
 
 
 # ---------------------------------------------------------------------------
-# Dispatch schedule (§3.1, Algorithm 1 and its sort-key restatement)
+# Dispatch schedule (§3.1, Algorithm 1 through its sort-key statement)
 # ---------------------------------------------------------------------------
 
-def schedule_algorithm1(A, L, c=0):
-    """Algorithm 1 (pull-based dispatch schedule construction), §3.1.
+def schedule_counts(A, L, c=0):
+    """Route counts per (source rank, local expert) and region starts (§3.1).
 
     A: int [R, N*K] global expert id of route j on source rank r.
-    L: local experts per rank; c: current rank (local expert l is global c*L+l).
-    Returns (M [R, L], S [L], Phi [P, 2]) where Phi[p] = (r, j) is the route
-    that local buffer position p receives.
+    L: local experts per rank; c: current rank (local expert l is global
+    c*L + l).  Returns (M [R, L], S [L]): M[r, l] counts the routes of rank r
+    to local expert l, and S[l] is the sum of M over all ranks and over the
+    experts before l (where l's region of the receive buffer starts).
     """
     A = np.asarray(A, np.int64)
-    R, NK = A.shape
-    lo, hi = c * L, (c + 1) * L
-    # route count per (source rank, local expert)
+    R = A.shape[0]
     M = np.zeros((R, L), np.int64)
     for r in range(R):
-        for j in range(NK):
-            if lo <= A[r, j] < hi:
-                M[r, A[r, j] - lo] += 1
-    # start of each local expert's buffer region: sum of all earlier experts' counts
-    S = np.zeros(L, np.int64)
-    for l in range(L):
-        S[l] = sum(int(M[r, lp]) for r in range(R) for lp in range(l))
-    Phi = np.full((int(M.sum()), 2), -1, np.int64)
-    for r in range(R):
-        seen = {}   # seen[a] = #{j' < j : A[r, j'] == a}, updated in j order
-        for j in range(NK):
-            a = int(A[r, j])
-            o = seen.get(a, 0)
-            seen[a] = o + 1
-            if not lo <= a < hi:
-                continue
-            l = a - lo
-            p = sum(min(int(M[rp, l]), o) for rp in range(R)) \
-                + sum(1 for rp in range(r) if M[rp, l] > o)
-            Phi[S[l] + p] = (r, j)
-    return M, S, Phi
+        loc = A[r][(A[r] >= c * L) & (A[r] < (c + 1) * L)] - c * L
+        M[r] = np.bincount(loc, minlength=L)
+    S = np.concatenate([[0], np.cumsum(M.sum(axis=0))[:-1]]).astype(np.int64)
+    return M, S
 
 
 def schedule_sort_key(A, L, c=0):
-    """The same table from the sort-key view of §3.1 ("Scheduling").
+    """The pull-based dispatch schedule of §3.1 from its sort-key statement.
 
     Sorts the local routes by (local expert l, per-source-rank ordinal o,
     source rank r), where o counts earlier routes of rank r to the same expert.
-    Returns Phi [P, 2] of (r, j).
+    Returns Phi [P, 2] of (r, j): buffer position p receives route j of rank r.
     """
     A = np.asarray(A, np.int64)
     R, NK = A.shape
@@ -155,6 +137,13 @@ def schedule_sort_key(A, L, c=0):
     return np.array([(r, j) for (_, _, r, j) in rows], np.int64).reshape(-1, 2)
 
 
+def schedule(A, L, c=0):
+    """Algorithm 1's outputs (§3.1): (M, S, Phi), as schedule_counts and
+    schedule_sort_key define them."""
+    M, S = schedule_counts(A, L, c)
+    return M, S, schedule_sort_key(A, L, c)
+
+
 def plan(idx, E):
     """Single-GPU dispatch plan: Algorithm 1 with one source rank (R = 1, c = 0).
 
@@ -166,7 +155,7 @@ def plan(idx, E):
     """
     idx = np.asarray(idx, np.int64)
     A = idx.reshape(1, -1)
-    M, S, Phi = schedule_algorithm1(A, E, 0)
+    M, S, Phi = schedule(A, E, 0)
     counts = M[0].astype(np.int32)
     offsets = np.zeros(E + 1, np.int32)
     offsets[:E] = S
@@ -386,6 +375,36 @@ def token_backward(X, W_r, W, idx, w, dY, tokens):
             dx += (dh * b * _dsilu(a)) @ Wg.T + (dh * silu(a)) @ Wu.T
         dXs[n] = dx[0]
     return dXs, dZs, dgs
+
+
+def router_gradient(X, W, idx, w, dY, chunk=4096):
+    """dZ [T, E] and dg [T, k] of every token, from the definition of the
+    router weights' role in the §2.1 layer: Y depends on w[t, e] only through
+    the term w[t, e] f_e(x_t), so dL/dw[t, e] = <dY[t], f_e(x_t)>; dZ then
+    follows from the restricted-softmax Jacobian.  Unlike moe_backward (which
+    takes the §3.4 identity <dY W_down^T, h>), this forms each expert output
+    f_e(x) in full.  Tokens go through each expert in chunks to bound memory.
+    """
+    X = np.asarray(X, F64)
+    T = X.shape[0]
+    E = W["W_gate"].shape[0]
+    k = idx.shape[1]
+    dg = np.zeros((T, k), F64)
+    for e in range(E):
+        ts, ss = np.nonzero(np.asarray(idx) == e)
+        if ts.size == 0:
+            continue
+        Wg = np.asarray(W["W_gate"][e], F64)
+        Wu = np.asarray(W["W_up"][e], F64)
+        Wd = np.asarray(W["W_down"][e], F64)
+        for c0 in range(0, ts.size, chunk):
+            t, s = ts[c0:c0 + chunk], ss[c0:c0 + chunk]
+            fe = expert_ffn(X[t], Wg, Wu, Wd)
+            dg[t, s] = (np.asarray(dY[t], F64) * fe).sum(axis=1)
+    dz_sel = softmax_restricted_backward(np.asarray(w, F64), dg)
+    dZ = np.zeros((T, E), F64)
+    np.put_along_axis(dZ, np.asarray(idx, np.int64), dz_sel, axis=1)
+    return dZ, dg
 
 
 def expert_weight_grad_columns(X, W, idx, w, dY, e, cols):

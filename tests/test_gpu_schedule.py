@@ -1,8 +1,9 @@
 """GPU parity of the multi-rank dispatch schedule (§3.1, Algorithm 1).
 
 Integer outputs, so the bar is bit-exactness: M, S and every schedule row
-against the literal Algorithm 1 of the oracle (and its sort-key statement),
-at the full route-table sizes and on the degenerate cases.
+against the oracle's schedule (counts from their definition, rows from the
+sort-key statement, pinned on the CPU to Algorithm 1's position formula), at
+the full route-table sizes and on the degenerate cases.
 """
 import numpy as np
 import pytest
@@ -40,19 +41,16 @@ def run_schedule(A, L, c, phi_rows=None):
     return to_np(M).reshape(R, L), to_np(S), to_np(phi), err
 
 
-def check_exact(A, L, c, literal=True):
+def check_exact(A, L, c):
     R, NK = A.shape
     M, S, phi, err = run_schedule(A, L, c)
-    Mo, So, Phio = O.schedule_algorithm1(A, L, c) if literal else (None, None, None)
-    Pk = O.schedule_sort_key(A, L, c)
+    Mo, So, Pk = O.schedule(A, L, c)
     P = int(S[L])
     assert err == 0, err
-    if literal:
-        assert np.array_equal(M, Mo), "M"
-        assert np.array_equal(S[:L], So), "S"
-        assert np.array_equal(phi[:P], Phio), "phi vs Algorithm 1"
+    assert np.array_equal(M, Mo), "M"
+    assert np.array_equal(S[:L], So), "S"
     assert P == len(Pk)
-    assert np.array_equal(phi[:P], Pk), "phi vs sort key"
+    assert np.array_equal(phi[:P], Pk), "phi"
     assert np.all(phi[P:] == SENTINEL), "rows past P written"
     return M, S, phi[:P]
 
@@ -63,7 +61,7 @@ def test_schedule_full_size_exact(name):
     A = make_route_table(t, seed=11)
     for c in sorted({0, t.R // 2 + 1, t.R - 1}):
         say(f"  {name} R={t.R} N={t.N} K={t.K} L={t.L} c={c}")
-        M, S, phi = check_exact(A, t.L, c, literal=(c == t.R - 1))
+        M, S, phi = check_exact(A, t.L, c)
         # every local route appears exactly once
         loc = np.argwhere((A >= c * t.L) & (A < (c + 1) * t.L))
         assert len(loc) == len(phi)
@@ -85,7 +83,7 @@ def test_schedule_shapes_every_rank(R, N, K, L):
     A = make_route_table(t, seed=R + N)
     ranks = range(R) if R <= 8 else (0, 1, R // 2, R - 1)
     for c in ranks:
-        check_exact(A, L, c, literal=R * N * K <= 50000)
+        check_exact(A, L, c)
 
 
 def test_schedule_single_hot_expert_round_robin():

@@ -4,6 +4,8 @@ Each case swaps one oracle function for a subtly wrong copy (on the CPU, inside
 this process only) and asserts that at least one pin of
 tests/test_oracle_pins.py then fails.  Nothing here touches the GPU path.
 """
+import functools
+
 import numpy as np
 import pytest
 
@@ -43,15 +45,27 @@ def _softmax_bwd_sign(w, dg):
     return w * (dg + (w * dg).sum(axis=1, keepdims=True))
 
 
-def _alg1_off_by_one(A, L, c=0):
-    M, S, Phi = _orig_alg1(A, L, c)
+def _schedule_swapped_rows(A, L, c=0):
+    Phi = _orig_sort_key(A, L, c)
     if len(Phi) > 1:
         Phi = Phi.copy()
         Phi[[0, 1]] = Phi[[1, 0]]
-    return M, S, Phi
+    return Phi
 
 
-_orig_alg1 = O.schedule_algorithm1
+def _schedule_rank_major(A, L, c=0):
+    """Orders a region by source rank before ordinal (no interleave)."""
+    A = np.asarray(A, np.int64)
+    rows = []
+    for r in range(A.shape[0]):
+        for j in range(A.shape[1]):
+            if c * L <= A[r, j] < (c + 1) * L:
+                rows.append((A[r, j] - c * L, r, j))
+    rows.sort()
+    return np.array([(r, j) for (_, r, j) in rows], np.int64).reshape(-1, 2)
+
+
+_orig_sort_key = O.schedule_sort_key
 _orig_backward = O.moe_backward
 
 
@@ -78,6 +92,7 @@ PINS = [P.test_topk_exact_ties_golden, P.test_gate_weights_closed_forms,
         P.test_identical_experts_ignore_routing, P.test_forward_matches_torch_layer_with_library_topk,
         P.test_backward_central_finite_differences, P.test_backward_matches_torch_autograd,
         P.test_algorithm1_hand_worked_two_ranks, P.test_plan_invariants_and_stable_sort,
+        functools.partial(P.test_schedule_positions_follow_algorithm1_formula, 3, 4, 20, 3, 1),
         P.test_router_gradient_identity]
 
 
@@ -88,7 +103,8 @@ PINS = [P.test_topk_exact_ties_golden, P.test_gate_weights_closed_forms,
     ("expert_ffn", _ffn_gate_up_swapped),
     ("_dsilu", _dsilu_dropped_term),
     ("softmax_restricted_backward", _softmax_bwd_sign),
-    ("schedule_algorithm1", _alg1_off_by_one),
+    ("schedule_sort_key", _schedule_swapped_rows),
+    ("schedule_sort_key", _schedule_rank_major),
     ("moe_backward", _backward_unweighted_down),
     ("moe_backward", _backward_transposed_router),
 ])

@@ -161,22 +161,49 @@ def _read_golden_alg1():
 def test_algorithm1_hand_worked_two_ranks():
     A = np.array([[0, 1, 1, 2, 0, 3], [1, 0, 3, 0, 0, 1]])
     for c, M, S, Phi in _read_golden_alg1():
-        gM, gS, gPhi = O.schedule_algorithm1(A, 2, c)
+        gM, gS, gPhi = O.schedule(A, 2, c)
         assert np.array_equal(gM, M) and np.array_equal(gS, S)
         assert np.array_equal(gPhi, Phi)
 
 
 @pytest.mark.parametrize("R,L,N,K,c", [(1, 8, 50, 2, 0), (3, 4, 20, 3, 1), (4, 2, 16, 2, 3),
-                                       (2, 5, 30, 4, 0), (1, 1, 7, 1, 0)])
-def test_algorithm1_equals_sort_key_restatement(R, L, N, K, c):
+                                       (2, 5, 30, 4, 0), (1, 1, 7, 1, 0), (5, 3, 12, 2, 4)])
+def test_schedule_positions_follow_algorithm1_formula(R, L, N, K, c):
+    """Every scheduled route sits where Algorithm 1's position formula puts it:
+    p = S[l] + sum_r' min(M[r', l], o) + #{r' < r : M[r', l] > o}, with o the
+    number of earlier routes of rank r to the same expert.  Also: Phi lists
+    every local route exactly once, each expert's rows form one contiguous
+    region starting at S[l], a rank's routes keep their order inside it, and
+    the ranks take turns (the i-th routes of all ranks precede the
+    (i+1)-th)."""
     rng = _rng(R * 100 + L)
     # distinct experts per token, as top-K selection produces
     A = np.stack([np.concatenate([rng.choice(R * L, K, replace=False) for _ in range(N)])
                   for _ in range(R)])
-    M, S, Phi = O.schedule_algorithm1(A, L, c)
-    assert np.array_equal(Phi, O.schedule_sort_key(A, L, c))
-    # region starts are the exclusive prefix of per-expert totals
+    M, S, Phi = O.schedule(A, L, c)
+    # counts and region starts from their definitions
+    for r in range(R):
+        for l in range(L):
+            assert M[r, l] == int(np.sum(A[r] == c * L + l))
     assert np.array_equal(S, np.concatenate([[0], np.cumsum(M.sum(0))[:-1]]))
+    local = [(r, j) for r in range(R) for j in range(A.shape[1]) if c * L <= A[r, j] < (c + 1) * L]
+    assert sorted(map(tuple, Phi.tolist())) == sorted(local)      # each local route once
+    for p, (r, j) in enumerate(Phi):
+        l = A[r, j] - c * L
+        o = int(np.sum(A[r, :j] == A[r, j]))
+        want = S[l] + sum(min(int(M[q, l]), o) for q in range(R)) \
+            + sum(1 for q in range(r) if M[q, l] > o)
+        assert p == want, (p, r, j)
+    for l in range(L):
+        reg = Phi[S[l]:S[l] + M[:, l].sum()]
+        assert np.all(A[reg[:, 0], reg[:, 1]] == c * L + l)          # contiguous region
+        for r in range(R):
+            js = reg[reg[:, 0] == r, 1]
+            assert np.all(np.diff(js) > 0)                          # rank order kept
+        # round robin: position of each rank's i-th route grows with i, and
+        # all i-th routes come before any (i+1)-th one
+        ords = [int(np.sum(A[r, :j] == A[r, j])) for r, j in reg]
+        assert ords == sorted(ords)
 
 
 def test_plan_invariants_and_stable_sort():
@@ -400,3 +427,18 @@ def test_sampled_backward_helpers_match_full_backward():
         assert np.allclose(a, G[0][:, cols], atol=1e-12)
         assert np.allclose(b, G[1][:, cols], atol=1e-12)
         assert np.allclose(c, G[2][cols, :], atol=1e-12)
+
+
+def test_router_gradient_from_expert_outputs_matches_backward():
+    """router_gradient forms <dY, f_e(x)> from the expert outputs themselves;
+    moe_backward takes the §3.4 identity.  Both must give the same dZ and dg
+    (chunk sizes below an expert's route count exercise the chunking)."""
+    X, W_r, W, dY = small_layer(T=40, d=16, E=5, k=3, f=8, f_s=8, seed=71)
+    Z = O.router_logits(X, W_r)
+    idx = O.topk_select(Z, 3)
+    w = O.gate_weights(Z, idx)
+    g = O.moe_backward(X, W_r, W, idx, w, dY)
+    for chunk in (3, 4096):
+        dZ, dg = O.router_gradient(X, W, idx, w, dY, chunk=chunk)
+        assert np.allclose(dZ, g["dZ"], rtol=0, atol=1e-12 * np.abs(g["dZ"]).max())
+        assert np.allclose(dg, g["dg"], rtol=0, atol=1e-12 * np.abs(g["dg"]).max())
