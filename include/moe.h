@@ -135,7 +135,15 @@ typedef enum {
     MOE_WS_DYTS = 24,   /* E8M0 [d, P/32]                                   */
     /* Backward (either layout): */
     MOE_WS_HW = 25,     /* bf16 [T*k, f]  gate weight times silu(A) * B     */
-    MOE_WS_COUNT = 26
+    /* MXFP8 only (moe_mx_workspace_region).  Values a quantiser reads are
+     * kept at the precision they were produced in (fp32): */
+    MOE_WS_AF = 26,     /* fp32 [T*k, f]  routed gate pre-activation A,
+                           kept by moe_forward_mx (save_for_backward = 1)   */
+    MOE_WS_BF = 27,     /* fp32 [T*k, f]  routed up pre-activation B        */
+    MOE_WS_DAF = 28,    /* fp32 [T*k, f]  dA (moe_backward_mx, wgrad_mxfp8 = 1) */
+    MOE_WS_DBF = 29,    /* fp32 [T*k, f]  dB (same)                          */
+    MOE_WS_HWF = 30,    /* fp32 [T*k, f]  gate weight times h (same)         */
+    MOE_WS_COUNT = 31
 } moe_ws_tensor;
 
 /* MXFP8 routed-expert weights (§3.4 "MXFP8 Support"), written once by
@@ -250,7 +258,8 @@ moe_status moe_mx_quantize_weights(const moe_shape *shape, const moe_weights *we
  * followed by moe_backward_mx (with_backward = 1), or of the same with the
  * MXFP8 weight gradients (with_backward = 2; adds the token-axis operands,
  * (2 d + 3 f) P bytes of codes and 1/32 of that of scales, P as for
- * MOE_WS_POFF); 0 for an invalid or unsupported shape.  Pure host function. */
+ * MOE_WS_POFF, and their fp32 sources, 12 T k f bytes); 0 for an invalid or
+ * unsupported shape.  Pure host function. */
 size_t moe_mx_workspace_bytes(const moe_shape *shape, int with_backward);
 
 /* Byte offset and size of a region of the MXFP8 workspace: the MXFP8 regions
@@ -287,8 +296,10 @@ moe_status moe_mx_quantize_weights_bwd(const moe_shape *shape, const moe_weights
  *     fp32 in the up/gate epilogue, and Yexp is rounded to bf16;
  *   - `weights` supplies only the shared expert (its routed pointers are
  *     ignored and may be NULL);
- *   - save_for_backward = 1 keeps the routed pre-activations A, B (bf16,
- *     from the MXFP8 products) and the shared expert's for moe_backward_mx.
+ *   - save_for_backward = 1 keeps the routed pre-activations A, B in fp32
+ *     (the accumulators of the MXFP8 products; the backward's dA, dB
+ *     quantisation reads values computed from them) and the shared
+ *     expert's in bf16, for moe_backward_mx.
  * Y [T, d] bf16 out.  ws: at least moe_mx_workspace_bytes(shape,
  * save_for_backward) bytes. */
 moe_status moe_forward_mx(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
@@ -302,15 +313,17 @@ moe_status moe_forward_mx(const moe_shape *shape, const moe_bf16 *X, const moe_w
  * gated activation).  As moe_backward, except:
  *   - dY is quantised once per token along d, and dh' = Q(dY) Q(W_down)^T
  *     runs on the block-scaled matrix cores with the weights in `mx`;
- *   - the gated-activation backward in that GEMM's epilogue writes dA, dB
- *     in bf16 and also quantised along f, and dXperm = Q(dA) Q(W_gate)^T +
- *     Q(dB) Q(W_up)^T runs in MXFP8;
+ *   - the gated-activation backward in that GEMM's epilogue (on the fp32
+ *     A, B the forward kept) quantises dA, dB along f from their fp32
+ *     values, and dXperm = Q(dA) Q(W_gate)^T + Q(dB) Q(W_up)^T runs in MXFP8;
  *   - the weight gradients contract over each expert's ragged token set;
- *     with wgrad_mxfp8 = 0 they stay BF16 on X, dY and the bf16 dA, dB,
- *     w h; with wgrad_mxfp8 = 1 these operands are quantised along the
- *     token axis (blocks of 32 plan rows from each expert's first row; the
- *     quantisation the expert-grouped GEMMs need for a contraction over
- *     tokens) and dW_gate = Q_t(X_e)^T Q_t(dA_e), dW_up = Q_t(X_e)^T Q_t(dB_e),
+ *     with wgrad_mxfp8 = 0 they stay BF16 on X, dY and dA, dB, w h stored
+ *     in bf16 (MOE_WS_DA, MOE_WS_DB, MOE_WS_HW); with wgrad_mxfp8 = 1 dA,
+ *     dB, w h are stored in fp32 instead (MOE_WS_DAF .. MOE_WS_HWF) and
+ *     every operand is quantised along the token axis (blocks of 32 plan
+ *     rows from each expert's first row; the quantisation the
+ *     expert-grouped GEMMs need for a contraction over tokens), and
+ *     dW_gate = Q_t(X_e)^T Q_t(dA_e), dW_up = Q_t(X_e)^T Q_t(dB_e),
  *     dW_down = Q_t(w h)^T Q_t(dY_e) run on the block-scaled matrix cores;
  *   - the shared expert, the router gradient and dX's router term are those
  *     of moe_backward.

@@ -195,24 +195,18 @@ def mx_qdq_token_blocks(v):
     return mx_qdq(vp, 0)[:n]
 
 
-def bf16_round(v):
-    """Round to the nearest bfloat16 (8 significand bits), ties to even, via
-    float32 (the GPU rounds its fp32 results the same way)."""
-    b = np.asarray(v, np.float32).view(np.uint32).astype(np.uint64)
-    b = (b + 0x7FFF + ((b >> 16) & 1)) & 0xFFFF0000
-    return b.astype(np.uint32).view(np.float32).astype(F64)
-
-
-def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True, wgrad_mx=False):
+def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True, wgrad_mx=False, keep=False):
     """Backward of the layer with MXFP8 routed experts (teacher-forced on idx, w).
 
     Readings (§3.4 "MXFP8 Support" names MXFP8 training and fused activation
     quantisation; it does not say which backward products run in MXFP8):
 
     * the pre-activations a, b and the activation h come from the MXFP8
-      forward (X quantised along d, W_gate / W_up along d); a and b are kept
-      in bf16 between the passes, as the BF16 path keeps them, and the
-      backward works from those values (quant=True only);
+      forward (X quantised along d, W_gate / W_up along d) and enter the
+      backward at full precision, exactly as in the BF16 oracle: the method
+      quantises only GEMM operands, and it fuses each quantisation into the
+      kernel that produces the values, so a quantiser reads the producer's
+      own result, never a rounded copy of it (§3.4 "MXFP8 Support");
     * the two products that contract over a model dimension run in MXFP8:
       dh' = Q_d(dY) Q_d(W_down[e])^T (dY per token and W_down per row, blocks
       along d), and dX_e = Q_f(dA) Q_f(W_gate[e])^T + Q_f(dB) Q_f(W_up[e])^T
@@ -220,21 +214,27 @@ def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True, wgrad_mx=False):
       of [d, f], blocks along f);
     * the weight-gradient products contract over each expert's ragged token
       set and stay BF16: dW_gate = X_e^T dA, dW_up = X_e^T dB,
-      dW_down = (w h)^T dY_e, with the unquantised X, dY and the fp32 dA, dB
-      (the gradient passes straight through the quantiser);
+      dW_down = (w h)^T dY_e, with the unquantised X, dY and the
+      full-precision dA, dB (the gradient passes straight through the
+      quantiser);
     * the router-weight gradient, the softmax backward, dW_r, the shared expert
       (BF16) and dX's router term are those of the BF16 backward.
 
     With wgrad_mx (the opt-in MXFP8 weight gradients), the weight-gradient
     products run in MXFP8 too.  They contract over the expert's tokens, so
     each operand is quantised along the token axis, per expert
-    (mx_qdq_token_blocks): X and dY as given, and dA, dB, w h in bf16, as
-    they are stored between the two backward GEMM stages:
+    (mx_qdq_token_blocks): X and dY as given, and dA, dB, w h as the
+    gated-activation backward produces them (full precision, the same
+    reading as for a and b above):
       dW_gate = Q_t(X_e)^T Q_t(dA_e), dW_up = Q_t(X_e)^T Q_t(dB_e),
       dW_down = Q_t(w h)^T Q_t(dY_e).
 
     quant=False replaces every quantise-dequantise by the identity, which must
     reproduce moe_oracle.moe_backward.
+
+    keep=True also returns, under "routes", each expert's pre-activations a,
+    b, the gradients dA, dB and the weighted activation w h, one row per
+    route of the expert in ascending route id (the plan order).
     """
     qdq = mx_qdq if quant else (lambda v, axis: np.asarray(v, F64))
     X = np.asarray(X, F64)
@@ -249,17 +249,17 @@ def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True, wgrad_mx=False):
     dWu = np.zeros((E, d, f), F64)
     dWd = np.zeros((E, f, d), F64)
     dg = np.zeros((T, k), F64)
+    routes = []
     for e in range(E):
         ts, ss = np.nonzero(np.asarray(idx) == e)
         if ts.size == 0:
+            routes.append(None)
             continue
         Wg = np.asarray(W["W_gate"][e], F64)
         Wu = np.asarray(W["W_up"][e], F64)
         Wd = np.asarray(W["W_down"][e], F64)
         a = Xh[ts] @ qdq(Wg, 0)                # forward: blocks of W_gate[e] [d, f] along d
         b = Xh[ts] @ qdq(Wu, 0)
-        if quant:                              # kept in bf16 for the backward
-            a, b = bf16_round(a), bf16_round(b)
         h = O.silu(a) * b
         we = np.asarray(w, F64)[ts, ss][:, None]
         dhp = dYh[ts] @ qdq(Wd, 1).T           # W_down[e] [f, d], blocks along d
@@ -267,11 +267,13 @@ def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True, wgrad_mx=False):
         dh = we * dhp
         dA = dh * b * O._dsilu(a)
         dB = dh * O.silu(a)
+        if keep:
+            routes.append(dict(a=a, b=b, dA=dA, dB=dB, wh=we * h))
         if quant and wgrad_mx:
             xt = mx_qdq_token_blocks(X[ts])
-            dWg[e] = xt.T @ mx_qdq_token_blocks(bf16_round(dA))
-            dWu[e] = xt.T @ mx_qdq_token_blocks(bf16_round(dB))
-            dWd[e] = mx_qdq_token_blocks(bf16_round(we * h)).T @ mx_qdq_token_blocks(dY[ts])
+            dWg[e] = xt.T @ mx_qdq_token_blocks(dA)
+            dWu[e] = xt.T @ mx_qdq_token_blocks(dB)
+            dWd[e] = mx_qdq_token_blocks(we * h).T @ mx_qdq_token_blocks(dY[ts])
         else:
             dWg[e] = X[ts].T @ dA
             dWu[e] = X[ts].T @ dB
@@ -284,6 +286,8 @@ def moe_backward_mx(X, W_r, W, idx, w, dY, quant=True, wgrad_mx=False):
     dX += dZ @ np.asarray(W_r, F64).T
     out = dict(dX=dX, dW_gate=dWg, dW_up=dWu, dW_down=dWd, dW_r=dW_r, dZ=dZ, dg=dg,
                dWg_s=None, dWu_s=None, dWd_s=None)
+    if keep:
+        out["routes"] = routes
     if W.get("Wg_s") is not None:             # the shared expert stays BF16
         Wg = np.asarray(W["Wg_s"], F64)
         Wu = np.asarray(W["Wu_s"], F64)
@@ -333,8 +337,8 @@ def mx_token_backward(X, W_r, W, idx, w, dY, tokens):
             if e not in cache:
                 cache[e] = _mx_expert_weights(W, e)
             q = cache[e]
-            a = bf16_round(xq @ q["g_fwd"])
-            b = bf16_round(xq @ q["u_fwd"])
+            a = xq @ q["g_fwd"]
+            b = xq @ q["u_fwd"]
             dhp = q["d_bwd"] @ dyq
             dg[n, s] = dhp @ (O.silu(a) * b)
             dh = w[t, s] * dhp
@@ -354,10 +358,12 @@ def mx_token_backward(X, W_r, W, idx, w, dY, tokens):
     return dX, dZ, dg
 
 
-def mx_expert_weight_grad_columns(X, W, idx, w, dY, e, cols, wgrad_mx=False):
+def mx_expert_weight_grad_columns(X, W, idx, w, dY, e, cols, wgrad_mx=False, keep=False):
     """dW_gate[e][:, cols], dW_up[e][:, cols] and dW_down[e][cols, :] of
     moe_backward_mx (token-axis blocks are per column, so the selected
-    columns need only their own operand columns)."""
+    columns need only their own operand columns).  keep=True also returns the
+    expert's operand columns dA[:, cols], dB[:, cols], (w h)[:, cols] in plan
+    order, as a fourth element (a dict)."""
     X = np.asarray(X, F64)
     dY = np.asarray(dY, F64)
     ts, ss = np.nonzero(np.asarray(idx) == e)
@@ -365,8 +371,8 @@ def mx_expert_weight_grad_columns(X, W, idx, w, dY, e, cols, wgrad_mx=False):
     Wu = np.asarray(W["W_up"][e], F64)
     Wd = np.asarray(W["W_down"][e], F64)
     xq = mx_qdq(X[ts], 1)
-    a = bf16_round(xq @ mx_qdq(Wg, 0)[:, cols])
-    b = bf16_round(xq @ mx_qdq(Wu, 0)[:, cols])
+    a = xq @ mx_qdq(Wg, 0)[:, cols]
+    b = xq @ mx_qdq(Wu, 0)[:, cols]
     dhp = mx_qdq(dY[ts], 1) @ mx_qdq(Wd, 1)[cols, :].T
     we = np.asarray(w, F64)[ts, ss][:, None]
     dh = we * dhp
@@ -376,6 +382,9 @@ def mx_expert_weight_grad_columns(X, W, idx, w, dY, e, cols, wgrad_mx=False):
     if wgrad_mx:
         qt = mx_qdq_token_blocks
         xt = qt(X[ts])
-        return (xt.T @ qt(bf16_round(dA)), xt.T @ qt(bf16_round(dB)),
-                qt(bf16_round(we * h)).T @ qt(dY[ts]))
-    return X[ts].T @ dA, X[ts].T @ dB, (we * h).T @ dY[ts]
+        out = (xt.T @ qt(dA), xt.T @ qt(dB), qt(we * h).T @ qt(dY[ts]))
+    else:
+        out = (X[ts].T @ dA, X[ts].T @ dB, (we * h).T @ dY[ts])
+    if keep:
+        return out + (dict(dA=dA, dB=dB, wh=we * h),)
+    return out

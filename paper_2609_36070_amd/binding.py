@@ -24,6 +24,7 @@ WS_XQ, WS_XS, WS_HQ, WS_HS = range(10, 14)
 WS_DYQ, WS_DYS, WS_DAQ, WS_DAS, WS_DBQ, WS_DBS = range(14, 20)
 WS_POFF, WS_XTQ, WS_XTS, WS_DYTQ, WS_DYTS = range(20, 25)
 WS_HW = 25
+WS_AF, WS_BF, WS_DAF, WS_DBF, WS_HWF = range(26, 31)
 
 EXPORTS = ("moe_workspace_bytes", "moe_workspace_region", "moe_route", "moe_plan",
            "moe_schedule_workspace_bytes", "moe_schedule", "moe_dispatch", "moe_forward",

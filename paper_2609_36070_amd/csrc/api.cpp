@@ -30,10 +30,12 @@ struct Layout {
     size_t xq, xs, hq, hsc;   // MXFP8 forward: quantised X and H (over the backward regions)
     size_t mx_total;
     size_t dyq, dys, daq, das, dbq, dbs;   // MXFP8 backward: quantised dY, dA, dB
+    size_t a32, b32;                       // MXFP8: the fp32 pre-activations kept for the backward
     size_t mxb_total;
     // MXFP8 weight gradients: padded expert offsets and the token-axis codes
     // and scales of X, dY, dA, dB and w h, [C][tpad] and [C][tpad / 32]
     size_t poff, xt, xts, dyt, dyts, dat, dats, dbt, dbts, hwt, hwts;
+    size_t da32, db32, hw32;   // their fp32 sources dA, dB, w h (plan order)
     size_t mxw_total;
     long tpad;                 // their row pitch: the padded token positions' bound
     long act_rows;             // rows of the per-route activation buffers
@@ -101,6 +103,8 @@ Layout make_layout(const moe_shape &s, long ring_rows = -1) {
     L.das = take(R * f / 32);
     L.dbq = take(R * f);
     L.dbs = take(R * f / 32);
+    L.a32 = take(R * f * 4);
+    L.b32 = take(R * f * 4);
     L.mxb_total = o;
     // each expert's rows padded to 128 positions: at most R + 127 E in all
     L.tpad = (long)((R + 128 * E + 127) / 128 * 128);
@@ -116,6 +120,9 @@ Layout make_layout(const moe_shape &s, long ring_rows = -1) {
     L.dbts = take(f * P / 32);
     L.hwt = take(f * P);
     L.hwts = take(f * P / 32);
+    L.da32 = take(R * f * 4);
+    L.db32 = take(R * f * 4);
+    L.hw32 = take(R * f * 4);
     L.mxw_total = o;
     return L;
 }
@@ -847,6 +854,11 @@ moe_status moe_mx_workspace_region(const moe_shape *shape, moe_ws_tensor which, 
         case MOE_WS_XTS: *offset = L.xts; *bytes = d * (size_t)L.tpad / 32; break;
         case MOE_WS_DYTQ: *offset = L.dyt; *bytes = d * (size_t)L.tpad; break;
         case MOE_WS_DYTS: *offset = L.dyts; *bytes = d * (size_t)L.tpad / 32; break;
+        case MOE_WS_AF: *offset = L.a32; *bytes = R * f * 4; break;
+        case MOE_WS_BF: *offset = L.b32; *bytes = R * f * 4; break;
+        case MOE_WS_DAF: *offset = L.da32; *bytes = R * f * 4; break;
+        case MOE_WS_DBF: *offset = L.db32; *bytes = R * f * 4; break;
+        case MOE_WS_HWF: *offset = L.hw32; *bytes = R * f * 4; break;
         default: return moe_workspace_region(shape, 1, which, offset, bytes);
     }
     return MOE_OK;
@@ -883,6 +895,7 @@ moe_status moe_forward_mx(const moe_shape *shape, const moe_bf16 *X, const moe_w
     if (!ptr_ok(ws)) return MOE_EINVAL;
     const Layout L = make_layout(*shape);
     if (ws_bytes < L.mx_total) return MOE_ENOSPACE;
+    if (save_for_backward && ws_bytes < L.mxb_total) return MOE_ENOSPACE;
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int T = (int)shape->T, d = (int)shape->d, E = (int)shape->E, k = (int)shape->k;
     const int f = (int)shape->f, fs = (int)shape->f_shared;
@@ -904,7 +917,7 @@ moe_status moe_forward_mx(const moe_shape *shape, const moe_bf16 *X, const moe_w
         g.B = mx->Wg_q; g.Bs = mx->Wg_s; g.B2 = mx->Wu_q; g.Bs2 = mx->Wu_s;
         g.K = d; g.N = f; g.offsets = plan->offsets; g.E = E;
         g.C = hq; g.Cs = hs;
-        if (save_for_backward) { g.Sa = at<uint16_t>(ws, L.A); g.Sb = at<uint16_t>(ws, L.B); }
+        if (save_for_backward) { g.Sa = at<float>(ws, L.a32); g.Sb = at<float>(ws, L.b32); }
         g.a_bytes = (uint32_t)((long)(T > 0 ? T : 1) * d);
         g.as_bytes = (uint32_t)((long)(T > 0 ? T : 1) * d / 32);
         g.b_bytes = (uint32_t)((long)E * f * d);
@@ -994,8 +1007,12 @@ moe_status moe_backward_mx(const moe_shape *shape, const moe_bf16 *dY, const moe
         g.B = mx->Wd_q; g.Bs = mx->Wd_s;
         g.K = d; g.N = f; g.offsets = plan->offsets; g.E = E;
         g.C = daq; g.Cs = das; g.C2 = dbq; g.Cs2 = dbs;
-        g.Cb = at<uint16_t>(ws, L.dA); g.Cb2 = at<uint16_t>(ws, L.dB); g.Cb3 = at<uint16_t>(ws, L.Hw);
-        g.E1 = at<uint16_t>(ws, L.A); g.E2 = at<uint16_t>(ws, L.B);
+        if (wgrad_mxfp8) {   // the token-axis quantisers read dA, dB, w h at fp32
+            g.Cf1 = at<float>(ws, L.da32); g.Cf2 = at<float>(ws, L.db32); g.Cf3 = at<float>(ws, L.hw32);
+        } else {
+            g.Cb = at<uint16_t>(ws, L.dA); g.Cb2 = at<uint16_t>(ws, L.dB); g.Cb3 = at<uint16_t>(ws, L.Hw);
+        }
+        g.E1 = at<float>(ws, L.a32); g.E2 = at<float>(ws, L.b32);
         g.rowscale = at<float>(ws, L.wperm);
         g.dgpart = at<float>(ws, L.dgpart); g.dg_ld = L.dg_parts;
         g.a_bytes = (uint32_t)(Tn * d);
@@ -1031,12 +1048,12 @@ moe_status moe_backward_mx(const moe_shape *shape, const moe_bf16 *dY, const moe
                                        at<uint8_t>(ws, L.xt), at<uint8_t>(ws, L.xts), s));
         MOE_TRY(launch_mx_quant_tokens(dY, d, T, rowidx, plan->offsets, poff, E, d, P, P,
                                        at<uint8_t>(ws, L.dyt), at<uint8_t>(ws, L.dyts), s));
-        MOE_TRY(launch_mx_quant_tokens(at<uint16_t>(ws, L.dA), f, R, nullptr, plan->offsets, poff, E,
-                                       f, P, P, at<uint8_t>(ws, L.dat), at<uint8_t>(ws, L.dats), s));
-        MOE_TRY(launch_mx_quant_tokens(at<uint16_t>(ws, L.dB), f, R, nullptr, plan->offsets, poff, E,
-                                       f, P, P, at<uint8_t>(ws, L.dbt), at<uint8_t>(ws, L.dbts), s));
-        MOE_TRY(launch_mx_quant_tokens(at<uint16_t>(ws, L.Hw), f, R, nullptr, plan->offsets, poff, E,
-                                       f, P, P, at<uint8_t>(ws, L.hwt), at<uint8_t>(ws, L.hwts), s));
+        MOE_TRY(launch_mx_quant_tokens_f32(at<float>(ws, L.da32), f, R, plan->offsets, poff, E, f, P,
+                                           P, at<uint8_t>(ws, L.dat), at<uint8_t>(ws, L.dats), s));
+        MOE_TRY(launch_mx_quant_tokens_f32(at<float>(ws, L.db32), f, R, plan->offsets, poff, E, f, P,
+                                           P, at<uint8_t>(ws, L.dbt), at<uint8_t>(ws, L.dbts), s));
+        MOE_TRY(launch_mx_quant_tokens_f32(at<float>(ws, L.hw32), f, R, plan->offsets, poff, E, f, P,
+                                           P, at<uint8_t>(ws, L.hwt), at<uint8_t>(ws, L.hwts), s));
         auto wg = [&](size_t a, size_t as, int M, size_t b, size_t bs, int N, float *out) {
             MxGemmArgs g;
             g.A = at<uint8_t>(ws, a); g.As = at<uint8_t>(ws, as); g.a_nrows = M;

@@ -39,6 +39,16 @@ DEV int shfl_xor_i(int v, int m) { return __shfl_xor(v, m, 64); }
 DEV u32x4_t ld_u32x4(const void *p) { return *reinterpret_cast<const u32x4_t *>(p); }
 DEV void st_u32x4(void *p, u32x4_t v) { *reinterpret_cast<u32x4_t *>(p) = v; }
 DEV u32x2_t ld_u32x2(const void *p) { return *reinterpret_cast<const u32x2_t *>(p); }
+// 8 consecutive floats (two 16-byte accesses)
+DEV f32x8 ld_f32x8(const float *p) {
+    const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(p);
+    const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(p + 4);
+    return f32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+}
+DEV void st_f32x8(float *p, const f32x8 &v) {
+    *reinterpret_cast<f32x4_t *>(p) = f32x4_t{v[0], v[1], v[2], v[3]};
+    *reinterpret_cast<f32x4_t *>(p + 4) = f32x4_t{v[4], v[5], v[6], v[7]};
+}
 
 // 8 floats -> 8 bf16 (round to nearest even) packed in 16 bytes
 DEV u32x4_t pack_bf8(const f32x8 &v) {

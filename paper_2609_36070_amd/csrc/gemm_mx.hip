@@ -4,12 +4,14 @@
 //
 //   MX_UP    g = Xq[tok(p)] . Wg_q[e][n], u = Xq[tok(p)] . Wu_q[e][n];
 //            H = silu(g) * u, quantised to MXFP8 along f (the activation
-//            quantisation fused into the gated activation) -> Hq, Hs
+//            quantisation fused into the gated activation) -> Hq, Hs; g and
+//            u kept in fp32 for the backward on request
 //   MX_DOWN  Yexp = Hq[p] . Wd_q[e][n] -> bf16
 //   MX_DGRAD dh' = dYq[tok(p)] . Wd_qd[e][n] (W_down rows quantised along d),
-//            then the gated-activation backward on the saved A, B: dg partials
-//            <dh', h>, dA = w dh' B silu'(A), dB = w dh' silu(A), Hw = w h;
-//            dA and dB go out in bf16 (for the weight gradients) and
+//            then the gated-activation backward on the saved fp32 A, B: dg
+//            partials <dh', h>, dA = w dh' B silu'(A), dB = w dh' silu(A),
+//            Hw = w h; dA, dB and Hw go out for the weight gradients (bf16,
+//            or fp32 when the weight gradients quantise them) and dA, dB
 //            quantised to MXFP8 along f (for the dX product)
 //   MX_DX    dXperm = dAq[p] . Wg_qf[e][n] + dBq[p] . Wu_qf[e][n] (one K loop
 //            over both halves; W_gate / W_up rows quantised along f) -> bf16
@@ -376,9 +378,11 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
                         *reinterpret_cast<u32x2_t *>(g.C + (long)p * g.N + fcol0 + c) =
                             e4m3_pack8(hv, s);
                         if ((lane & 3) == 0) g.Cs[(long)p * hs_row + fcol0 / 32] = (uint8_t)(s + 127);
-                        if (g.Sa) {   // pre-activations for the backward
-                            st_u32x4(g.Sa + (long)p * g.N + fcol0 + c, pack_bf8(a));
-                            st_u32x4(g.Sb + (long)p * g.N + fcol0 + c, pack_bf8(b));
+                        if (g.Sa) {   // pre-activations for the backward, fp32
+                            float *sa = g.Sa + (long)p * g.N + fcol0 + c;
+                            float *sb = g.Sb + (long)p * g.N + fcol0 + c;
+                            st_f32x8(sa, a);
+                            st_f32x8(sb, b);
                         }
                     }
                 }
@@ -400,14 +404,14 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
         // round trips overlap the passes in between instead of each pass
         // waiting for its own.  Rows past the region's end read its last row.
         constexpr int NP = 32 / RPP, NU = TM * NP, PF = 4;
-        u32x4_t qa[PF], qb[PF];
+        f32x8 qa[PF], qb[PF];
         float qw[PF];
-        auto fetch = [&](int u, u32x4_t &a, u32x4_t &b, float &w) {
+        auto fetch = [&](int u, f32x8 &a, f32x8 &b, float &w) {
             const int row = lane / LPR + RPP * (u % NP), c = 8 * (lane % LPR);
             const int pl = min(row0 + wm * WM + 32 * (u / NP) + row, row_end - 1);
             const long o = (long)pl * g.N + n0 + wn * WN + c;
-            a = ld_u32x4(g.E1 + o);
-            b = ld_u32x4(g.E2 + o);
+            a = ld_f32x8(g.E1 + o);
+            b = ld_f32x8(g.E2 + o);
             w = g.rowscale[pl];
         };
 #pragma unroll
@@ -421,7 +425,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
 #pragma unroll 1
             for (int t = 0; t < NP; ++t) {
                 const int u = i * NP + t;
-                const u32x4_t av = qa[0], bv = qb[0];
+                const f32x8 av = qa[0], bv = qb[0];
                 const float wv = qw[0];
 #pragma unroll
                 for (int q = 0; q + 1 < PF; ++q) { qa[q] = qa[q + 1]; qb[q] = qb[q + 1]; qw[q] = qw[q + 1]; }
@@ -437,8 +441,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
                 float prod = 0.f, amax_a = 0.f, amax_b = 0.f;
 #pragma unroll
                 for (int k = 0; k < 8; ++k) {
-                    const float a = (k & 1) ? bf_hi(av[k >> 1]) : bf_lo(av[k >> 1]);
-                    const float b = (k & 1) ? bf_hi(bv[k >> 1]) : bf_lo(bv[k >> 1]);
+                    const float a = av[k], b = bv[k];
                     const float sg = 1.0f / (1.0f + expf(-a));
                     const float sl = a * sg;
                     const float h = sl * b;
@@ -456,9 +459,15 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
                 amax_b = fmaxf(amax_b, shfl_xor_f(amax_b, 2));
                 const int sa = mx_shared_exp(amax_a), sb = mx_shared_exp(amax_b);
                 if (p < row_end) {
-                    st_u32x4(g.Cb + o, pack_bf8(dav));
-                    st_u32x4(g.Cb2 + o, pack_bf8(dbv));
-                    st_u32x4(g.Cb3 + o, pack_bf8(hw));
+                    if (g.Cf1) {   // fp32 for the token-axis quantisers
+                        st_f32x8(g.Cf1 + o, dav);
+                        st_f32x8(g.Cf2 + o, dbv);
+                        st_f32x8(g.Cf3 + o, hw);
+                    } else {
+                        st_u32x4(g.Cb + o, pack_bf8(dav));
+                        st_u32x4(g.Cb2 + o, pack_bf8(dbv));
+                        st_u32x4(g.Cb3 + o, pack_bf8(hw));
+                    }
                     *reinterpret_cast<u32x2_t *>(g.C + o) = e4m3_pack8(dav, sa);
                     *reinterpret_cast<u32x2_t *>(g.C2 + o) = e4m3_pack8(dbv, sb);
                     if ((lane & 3) == 0) {

@@ -104,10 +104,13 @@ struct MxGemmArgs {
     uint16_t *Cb = nullptr;            // MX_DOWN, MX_DX: bf16 [rows][N]; MX_DGRAD: dA bf16
     uint16_t *Cb2 = nullptr;           // MX_DGRAD: dB bf16
     uint16_t *Cb3 = nullptr;           // MX_DGRAD: w * h bf16
-    uint16_t *Sa = nullptr;            // MX_UP: keep the gate / up pre-activations (bf16)
-    uint16_t *Sb = nullptr;
-    const uint16_t *E1 = nullptr;      // MX_DGRAD: saved pre-activations A, B (bf16)
-    const uint16_t *E2 = nullptr;
+    float *Cf1 = nullptr;              // MX_DGRAD: dA, dB, w * h in fp32 instead of bf16
+    float *Cf2 = nullptr;              //   (the token-axis quantisers of the MXFP8 weight
+    float *Cf3 = nullptr;              //   gradients read them)
+    float *Sa = nullptr;               // MX_UP: keep the gate / up pre-activations (fp32)
+    float *Sb = nullptr;
+    const float *E1 = nullptr;         // MX_DGRAD: saved pre-activations A, B (fp32)
+    const float *E2 = nullptr;
     const float *rowscale = nullptr;   // MX_DGRAD: router weight per row
     float *dgpart = nullptr;           // MX_DGRAD: <dh', h> partial per row and n-tile
     int dg_ld = 0;
@@ -134,6 +137,10 @@ hipError_t launch_mx_pad_offsets(const int *offsets, int E, int *poff, hipStream
 hipError_t launch_mx_quant_tokens(const uint16_t *src, long ld, long nsrc, const int *rows,
                                   const int *offsets, const int *poff, int E, int C, long pitch,
                                   long max_pos, uint8_t *q, uint8_t *sc, hipStream_t st);
+// The same for an fp32 source in plan order (no gather).
+hipError_t launch_mx_quant_tokens_f32(const float *src, long ld, long nsrc, const int *offsets,
+                                      const int *poff, int E, int C, long pitch, long max_pos,
+                                      uint8_t *q, uint8_t *sc, hipStream_t st);
 hipError_t launch_mx_quant_rows(const uint16_t *X, long rows, int K, uint8_t *q, uint8_t *sc,
                                 hipStream_t st);
 hipError_t launch_mx_quant_weights(const uint16_t *W, int E, int K, int N, uint8_t *q, uint8_t *sc,

@@ -19,7 +19,9 @@
 //                     expert's tokens: rows of the expert's plan region in
 //                     32-row blocks from its first row, written transposed
 //                     (token-contiguous) at the expert's region padded to
-//                     128 positions, the K step of the fp8 GEMM.
+//                     128 positions, the K step of the fp8 GEMM.  The source
+//                     is bf16 (X, dY, gathered by token) or fp32 (dA, dB and
+//                     w h as the gated-activation backward produced them).
 #include "common.h"
 #include "kernels.h"
 #include "mx_common.h"
@@ -96,14 +98,31 @@ constexpr int TQ_OPITCH = 144;   // LDS bytes per column of codes (+16: conflict
 constexpr int TQ_LDS = 256 * TQ_OPITCH;
 static_assert(32 * WQ_PITCH * 2 <= TQ_LDS, "the input block fits the code buffer");
 
-// Rows 32 sb .. 32 sb + 31 of the 128 (s_row: source row, < 0 for zeros), 8
-// bf16 columns per chunk, 4 chunks per thread.
-DEV void tq_fetch(const uint16_t *__restrict__ src, long ld, const int *s_row, int sb, int c0, int t,
+// Element formats of the column quantiser's source: PER elements per 16-byte
+// chunk, CH chunks per thread per 32-row block, LDS pitch in elements.
+template <typename S> struct TqFmt;
+template <> struct TqFmt<uint16_t> {
+    static constexpr int PER = 8, CH = 4, PITCH = WQ_PITCH;
+    static DEV float val(uint16_t v) { return bf2f(v); }
+};
+template <> struct TqFmt<float> {
+    static constexpr int PER = 4, CH = 8, PITCH = 256 + 4;
+    static DEV float val(float v) { return v; }
+};
+static_assert(32 * TqFmt<uint16_t>::PITCH * 2 <= TQ_LDS, "a bf16 input block fits the code buffer");
+static_assert(32 * TqFmt<float>::PITCH * 4 <= TQ_LDS, "an fp32 input block fits the code buffer");
+
+// Rows 32 sb .. 32 sb + 31 of the 128 (s_row: source row, < 0 for zeros),
+// one 16-byte chunk of the 256 columns per load, CH loads per thread.
+template <typename S>
+DEV void tq_fetch(const S *__restrict__ src, long ld, const int *s_row, int sb, int c0, int t,
                   u32x4_t *v) {
+    using F = TqFmt<S>;
+    constexpr int RC = 256 / F::PER;   // chunks per row
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
+    for (int it = 0; it < F::CH; ++it) {
         const int ch = it * 256 + t;
-        const int r = ch / 32, c = 8 * (ch % 32);
+        const int r = ch / RC, c = F::PER * (ch % RC);
         const int row = s_row[32 * sb + r];
         v[it] = u32x4_t{0, 0, 0, 0};
         if (row >= 0) v[it] = ld_u32x4(src + (long)row * ld + c0 + c);
@@ -113,12 +132,15 @@ DEV void tq_fetch(const uint16_t *__restrict__ src, long ld, const int *s_row, i
 // The 128 source rows are s_row[0..127] (written before the call, visible
 // after its first barrier).  Column c's 128 codes go to q + c * pitch (c
 // counted from c0) and its 4 scales to the 4 bytes at sc + c * spitch.
-DEV void quant_cols128(const uint16_t *__restrict__ src, long ld, const int *s_row, int c0, int t,
+template <typename S>
+DEV void quant_cols128(const S *__restrict__ src, long ld, const int *s_row, int c0, int t,
                        uint8_t *lds, uint8_t *__restrict__ q, long pitch, uint8_t *__restrict__ sc,
                        long spitch) {
-    uint16_t *tile = reinterpret_cast<uint16_t *>(lds);
+    using F = TqFmt<S>;
+    constexpr int RC = 256 / F::PER;
+    S *tile = reinterpret_cast<S *>(lds);
     __syncthreads();
-    u32x4_t pf[4];
+    u32x4_t pf[F::CH];
     tq_fetch(src, ld, s_row, 0, c0, t, pf);
     uint32_t codes[32];
     uint32_t scw = 0;
@@ -126,9 +148,9 @@ DEV void quant_cols128(const uint16_t *__restrict__ src, long ld, const int *s_r
     for (int sb = 0; sb < 4; ++sb) {
         if (sb > 0) __syncthreads();            // the previous block's column reads are done
 #pragma unroll
-        for (int it = 0; it < 4; ++it) {
+        for (int it = 0; it < F::CH; ++it) {
             const int ch = it * 256 + t;
-            st_u32x4(tile + (ch / 32) * WQ_PITCH + 8 * (ch % 32), pf[it]);
+            st_u32x4(tile + (ch / RC) * F::PITCH + F::PER * (ch % RC), pf[it]);
         }
         __syncthreads();
         if (sb < 3) tq_fetch(src, ld, s_row, sb + 1, c0, t, pf);
@@ -136,7 +158,7 @@ DEV void quant_cols128(const uint16_t *__restrict__ src, long ld, const int *s_r
         float amax = 0.f;
 #pragma unroll
         for (int r = 0; r < 32; ++r) {
-            v[r] = bf2f(tile[r * WQ_PITCH + t]);
+            v[r] = F::val(tile[r * F::PITCH + t]);
             amax = fmaxf(amax, fabsf(v[r]));
         }
         const int s = mx_shared_exp(amax);
@@ -184,8 +206,8 @@ __global__ __launch_bounds__(256) void mx_quant_weights_kernel(const uint16_t *_
 // Grid (C / 256, max_pos / 128): the 128 padded positions [p0, p0 + 128) of
 // one expert, rows of its plan region (gathered through `rows` when GATHER)
 // or zeros past its count.
-template <bool GATHER>
-__global__ __launch_bounds__(256) void mx_quant_tokens_kernel(const uint16_t *__restrict__ src, long ld,
+template <bool GATHER, typename S>
+__global__ __launch_bounds__(256) void mx_quant_tokens_kernel(const S *__restrict__ src, long ld,
                                                               long nsrc, const int *__restrict__ rows,
                                                               const int *__restrict__ offsets,
                                                               const int *__restrict__ poff, int E,
@@ -247,8 +269,17 @@ hipError_t launch_mx_quant_tokens(const uint16_t *src, long ld, long nsrc, const
     if (max_pos <= 0 || C <= 0 || E <= 0 || nsrc <= 0) return hipSuccess;
     const dim3 grid((unsigned)(C / WQ_TN), (unsigned)(max_pos / 128));
     if (rows)
-        mx_quant_tokens_kernel<true><<<grid, dim3(256), 0, st>>>(src, ld, nsrc, rows, offsets, poff, E, pitch, q, sc);
+        mx_quant_tokens_kernel<true, uint16_t><<<grid, dim3(256), 0, st>>>(src, ld, nsrc, rows, offsets, poff, E, pitch, q, sc);
     else
-        mx_quant_tokens_kernel<false><<<grid, dim3(256), 0, st>>>(src, ld, nsrc, rows, offsets, poff, E, pitch, q, sc);
+        mx_quant_tokens_kernel<false, uint16_t><<<grid, dim3(256), 0, st>>>(src, ld, nsrc, rows, offsets, poff, E, pitch, q, sc);
+    return hipGetLastError();
+}
+
+hipError_t launch_mx_quant_tokens_f32(const float *src, long ld, long nsrc, const int *offsets,
+                                      const int *poff, int E, int C, long pitch, long max_pos,
+                                      uint8_t *q, uint8_t *sc, hipStream_t st) {
+    if (max_pos <= 0 || C <= 0 || E <= 0 || nsrc <= 0) return hipSuccess;
+    const dim3 grid((unsigned)(C / WQ_TN), (unsigned)(max_pos / 128));
+    mx_quant_tokens_kernel<false, float><<<grid, dim3(256), 0, st>>>(src, ld, nsrc, nullptr, offsets, poff, E, pitch, q, sc);
     return hipGetLastError();
 }

@@ -49,8 +49,6 @@ def _variant(X, W_r, W, idx, w, dY, quant=True, dy_axis=1, wd_axis=1, da_axis=1,
         fq = qdq if forward_quantised else (lambda v, axis: v)
         a = Xh[ts] @ fq(Wg, 0)
         b = Xh[ts] @ fq(Wu, 0)
-        if quant:
-            a, b = M.bf16_round(a), M.bf16_round(b)
         h = O.silu(a) * b
         we = np.asarray(w, F64)[ts, ss][:, None]
         dhp = dYh[ts] @ qdq(Wd, wd_axis).T

@@ -40,15 +40,14 @@ def _variant(X, W_r, W, idx, w, dY, quant=True, wgrad_mx=False, grid="expert", x
     for e in range(E):
         ts, ss = np.nonzero(np.asarray(idx) == e)
         Wg, Wu, Wd = (np.asarray(W[key][e], F64) for key in ("W_gate", "W_up", "W_down"))
-        a = M.bf16_round(Xh[ts] @ M.mx_qdq(Wg, 0))
-        b = M.bf16_round(Xh[ts] @ M.mx_qdq(Wu, 0))
+        a = Xh[ts] @ M.mx_qdq(Wg, 0)
+        b = Xh[ts] @ M.mx_qdq(Wu, 0)
         h = O.silu(a) * b
         we = np.asarray(w, F64)[ts, ss][:, None]
         dh = we * (dYh[ts] @ M.mx_qdq(Wd, 1).T)
         dA = dh * b * O._dsilu(a)
         dB = dh * O.silu(a)
-        parts.append(dict(x=X[ts], dy=dY[ts], da=M.bf16_round(dA), db=M.bf16_round(dB),
-                          wh=M.bf16_round(we * h)))
+        parts.append(dict(x=X[ts], dy=dY[ts], da=dA, db=dB, wh=we * h))
 
     def tq(name, axis=0, on=True):
         """The operand `name` of every expert after its weight-gradient quantiser."""
