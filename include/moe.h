@@ -214,6 +214,27 @@ moe_status moe_plan(const moe_shape *shape, const int32_t *topk_idx,
                     const moe_plan_bufs *plan, void *ws, size_t ws_bytes,
                     moe_stream stream);
 
+/* The dispatch plan of moe_plan for callers that cannot allocate device
+ * memory or pass a workspace (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation).  Same inputs and plan outputs as
+ * moe_plan; its scratch (per-chunk histograms, bases and flags) lives in a
+ * device array of MOE_PLAN_NOALLOC_SCRATCH_BYTES that the library holds on
+ * each GPU it runs on until the process ends.  The call allocates nothing
+ * (no hipMalloc, hipFree or allocating library routine).
+ *   error_word [1] int32 out (device): 1 if some expert id lies outside
+ *              [0, E) (that route is left unplaced, as in moe_plan), else 0.
+ * The plan needs 8 * ceil(T*k / 1024) * E bytes of scratch (each of its
+ * regions rounded up to 256 bytes) plus 4 * ceil(T*k / 1024): shapes needing
+ * more than MOE_PLAN_NOALLOC_SCRATCH_BYTES return MOE_EUNSUPPORTED before
+ * anything is launched (at E = 256 that admits T*k up to about 2 million
+ * routes).  All calls on one GPU share its array: calls that overlap on one
+ * GPU (on different streams, or from different threads) race and must be
+ * serialised by the caller.  Other errors as moe_plan; MOE_EHIP also when
+ * the array's device address cannot be obtained. */
+#define MOE_PLAN_NOALLOC_SCRATCH_BYTES (4u << 20)
+moe_status moe_plan_noalloc(const moe_shape *shape, const int32_t *topk_idx,
+                            const moe_plan_bufs *plan, int32_t *error_word, moe_stream stream);
+
 /* Pull-based dispatch schedule for R source ranks (§3.1, Algorithm 1, and
  * its sort-key statement in "Scheduling").  Each of R ranks holds N tokens
  * with K routes each; A is the all-gathered route table and the schedule is

@@ -31,7 +31,9 @@ EXPORTS = ("moe_workspace_bytes", "moe_workspace_region", "moe_route", "moe_plan
            "moe_backward", "moe_mx_quantize_weights", "moe_mx_workspace_bytes",
            "moe_mx_workspace_region", "moe_forward_mx", "moe_ring_workspace_bytes",
            "moe_forward_ring", "moe_backward_ring", "moe_forward_fused",
-           "moe_mx_quantize_weights_bwd", "moe_backward_mx", "moe_status_string", "moe_version")
+           "moe_mx_quantize_weights_bwd", "moe_backward_mx", "moe_plan_noalloc", "moe_status_string",
+           "moe_version")
+PLAN_NOALLOC_SCRATCH_BYTES = 4 << 20
 
 
 class MoeShape(ctypes.Structure):
@@ -95,6 +97,7 @@ def lib():
         L.moe_workspace_region.argtypes = [P(MoeShape), c_int, c_int, P(c_size_t), P(c_size_t)]
         L.moe_route.argtypes = [P(MoeShape)] + [c_void_p] * 7 + [c_size_t, c_void_p]
         L.moe_plan.argtypes = [P(MoeShape), c_void_p, P(MoePlanBufs), c_void_p, c_size_t, c_void_p]
+        L.moe_plan_noalloc.argtypes = [P(MoeShape), c_void_p, P(MoePlanBufs), c_void_p, c_void_p]
         L.moe_dispatch.argtypes = [P(MoeShape), c_void_p, P(MoePlanBufs), c_void_p, c_void_p]
         L.moe_schedule_workspace_bytes.argtypes = [ctypes.c_int64] * 3
         L.moe_schedule_workspace_bytes.restype = c_size_t
@@ -221,6 +224,13 @@ def moe_plan(shape, topk_idx, plan: MoePlanBufs, ws, ws_bytes=None, stream=None,
     st = lib().moe_plan(ctypes.byref(shape), _p(topk_idx), ctypes.byref(plan), _p(ws), nbytes,
                         _stream(stream))
     return _check("moe_plan", st, raise_on_error)
+
+
+def moe_plan_noalloc(shape, topk_idx, plan: MoePlanBufs, error_word, stream=None,
+                     raise_on_error=True):
+    st = lib().moe_plan_noalloc(ctypes.byref(shape), _p(topk_idx), ctypes.byref(plan),
+                                _p(error_word), _stream(stream))
+    return _check("moe_plan_noalloc", st, raise_on_error)
 
 
 def moe_schedule_workspace_bytes(R: int, NK: int, L: int) -> int:

@@ -5,6 +5,7 @@
 
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 
 #include "../../include/moe.h"
 #include "kernels.h"
@@ -206,6 +207,38 @@ SchedLayout schedule_layout(int64_t R, int64_t NK, int64_t L) {
 
 template <typename T>
 T *at(void *ws, size_t off) { return reinterpret_cast<T *>(static_cast<char *>(ws) + off); }
+
+// Plan scratch of moe_plan_noalloc: a device array the library owns, one
+// copy per GPU, held until the process ends.  In host code `scratch` is only
+// a stand-in for the symbol: its device address comes from
+// hipGetSymbolAddress, taken once per device with that device current, and
+// only that address is ever handed to a kernel.
+constexpr size_t NOALLOC_SCRATCH_BYTES = size_t(MOE_PLAN_NOALLOC_SCRATCH_BYTES);
+static __device__ __align__(256) uint8_t scratch[NOALLOC_SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex scratch_mu;
+void *scratch_ptr[MAX_DEVICES] = {};
+
+// The current device's copy of `scratch` (nullptr if its address cannot be had).
+void *device_scratch() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) return nullptr;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (!scratch_ptr[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+        scratch_ptr[dev] = p;
+    }
+    return scratch_ptr[dev];
+}
+
+// Bytes of plan scratch for R routes over E experts (per-chunk histograms,
+// their scanned bases and flags, each region 256-byte aligned).
+size_t plan_scratch_bytes(long R, long E) {
+    const size_t nb = (size_t)plan_nblocks(R);
+    return 2 * up(nb * (size_t)E * 4) + up(nb * 4 > 0 ? nb * 4 : 1);
+}
 
 // MXFP8 path: every fp8 operand is addressed with 32-bit offsets.
 moe_status check_mx_shape(const moe_shape *s) {
@@ -554,6 +587,29 @@ moe_status moe_plan(const moe_shape *shape, const int32_t *topk_idx, const moe_p
     MOE_TRY(launch_plan(topk_idx, R, (int)shape->E, plan->counts, plan->offsets, plan->perm,
                         plan->route_pos, at<int>(ws, L.blockcounts), at<int>(ws, L.blockbase),
                         at<int>(ws, L.blockflags), at<int>(ws, L.err), s));
+    return MOE_OK;
+}
+
+moe_status moe_plan_noalloc(const moe_shape *shape, const int32_t *topk_idx,
+                            const moe_plan_bufs *plan, int32_t *error_word, moe_stream stream) {
+    moe_status st = check_shape(shape);
+    if (st != MOE_OK) return st;
+    if (!ptr_ok(topk_idx) || !ptr_ok(error_word)) return MOE_EINVAL;
+    if ((st = check_plan(plan)) != MOE_OK) return st;
+    const long R = (long)(shape->T * shape->k);
+    const size_t need = plan_scratch_bytes(R, shape->E);
+    if (need > NOALLOC_SCRATCH_BYTES) return MOE_EUNSUPPORTED;
+    uint8_t *sp = static_cast<uint8_t *>(device_scratch());
+    if (!sp) return MOE_EHIP;
+    const size_t nb = (size_t)plan_nblocks(R);
+    const size_t cnt_bytes = up(nb * (size_t)shape->E * 4);
+    int *blockcounts = reinterpret_cast<int *>(sp);
+    int *blockbase = reinterpret_cast<int *>(sp + cnt_bytes);
+    int *blockflags = reinterpret_cast<int *>(sp + 2 * cnt_bytes);
+    // every scratch word is written before it is read, so nothing is cleared
+    MOE_TRY(launch_plan(topk_idx, (int)R, (int)shape->E, plan->counts, plan->offsets, plan->perm,
+                        plan->route_pos, blockcounts, blockbase, blockflags, error_word,
+                        static_cast<hipStream_t>(stream)));
     return MOE_OK;
 }
 

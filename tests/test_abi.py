@@ -317,3 +317,22 @@ def test_oracle_is_not_imported_by_the_package():
         if fn.endswith(".py"):
             src = open(os.path.join(pkg_dir, fn)).read()
             assert "import oracle" not in src and "from oracle" not in src, fn
+
+
+def test_plan_noalloc_validation():
+    """Rejected on the host before any HIP call: bad pointers, and shapes whose
+    plan scratch exceeds the library-held array."""
+    sh = B.make_shape(1000, 256, 8, 2, 256, 0)
+    pb = B.MoePlanBufs(FAKE, FAKE, FAKE, FAKE)
+    L = B.lib()
+    assert L.moe_plan_noalloc(ctypes.byref(sh), None, ctypes.byref(pb), FAKE, None) == B.MOE_EINVAL
+    assert L.moe_plan_noalloc(ctypes.byref(sh), FAKE, ctypes.byref(pb), None, None) == B.MOE_EINVAL
+    assert L.moe_plan_noalloc(ctypes.byref(sh), FAKE, ctypes.byref(pb), MISALIGNED, None) == B.MOE_EINVAL
+    bad = B.MoePlanBufs(FAKE, None, FAKE, FAKE)
+    assert L.moe_plan_noalloc(ctypes.byref(sh), FAKE, ctypes.byref(bad), FAKE, None) == B.MOE_EINVAL
+    big = B.make_shape(300000, 256, 256, 8, 256, 0)     # ~4.8 MB of scratch needed
+    assert L.moe_plan_noalloc(ctypes.byref(big), FAKE, ctypes.byref(pb), FAKE, None) == B.MOE_EUNSUPPORTED
+    ok = B.make_shape(200000, 256, 256, 8, 256, 0)      # ~3.2 MB: admitted (not run here)
+    assert 8 * -(-200000 * 8 // 1024) * 256 + 4 * -(-200000 * 8 // 1024) <= B.PLAN_NOALLOC_SCRATCH_BYTES
+    del ok
+
