@@ -22,8 +22,12 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "MoE layer fwd+bwd TFLOP/s and tokens/s on 1 MI355X; % of bf16 MFMA peak"
-PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, AMD's published figure (2.4 GHz)
+PEAK_BF16_TFLOPS_ALT = 2300.0  # the ~2.3 PFLOP/s dense bf16 figure the benchmark spec quotes
 PEAK_HBM_GBS = 8000.0
+# configurations measured forward-only beside the training step (the paper
+# benchmarks its layer at several shapes, §4.1)
+FORWARD_CONFIGS = ("tiny", "many_experts", "hot_expert", "large_shared")
 
 
 def log(*a):
@@ -343,15 +347,253 @@ def ring_timing(H, stream, w, inputs, L_full, steps, warmup):
     return out
 
 
+def hbm_bytes(w):
+    """Algorithmic HBM bytes per launch of the memory-bound kernels (each
+    tensor read or written once)."""
+    T, d, E, k, R = w.T, w.d, w.E, w.k, w.T * w.k
+    sh = 1 if w.f_s else 0
+    out = {
+        # X, W_r read; logits, top-k ids and weights written
+        "route": 2 * T * d + 2 * d * E + 4 * T * E + 8 * T * k,
+        # Yexp rows, Ysh read; Y written; route positions and weights read
+        "combine": 2 * R * d + 2 * T * d * sh + 2 * T * d + 8 * R,
+    }
+    if w.backward:
+        # dXperm rows, dXsh, dZ, W_r read; dX written; route positions read
+        out["reverse_combine"] = 2 * R * d + 2 * T * d * sh + 4 * T * E + 2 * d * E + 2 * T * d + 4 * R
+        # X and dZ read, dW_r written
+        out["dw_router"] = 2 * T * d + 4 * T * E + 4 * d * E
+    return out
+
+
+def copy_ceiling(H, stream, mib=2048, reps=5):
+    """A plain device-to-device copy on this GPU: the practical HBM ceiling
+    (bytes read + bytes written per second), median of `reps` copies."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    # copies back to back between one pair of events: the GPU stays busy, so
+    # no host-side launch latency enters the time
+    a, b = H.create(), H.create()
+    H.record(a, stream)
+    for _ in range(reps):
+        dst.copy_(src)
+    H.record(b, stream)
+    H.sync(b)
+    ms = H.ms(a, b) / reps
+    H.destroy(a)
+    H.destroy(b)
+    del src, dst
+    torch.cuda.synchronize()
+    return {"bytes": 2 * mib * (1 << 20), "ms": round(ms, 4),
+            "GB/s": round(2 * mib * (1 << 20) / (ms * 1e-3) / 1e9, 1)}
+
+
+def route_time(H, stream, L, reps=20):
+    """moe_route alone, `reps` calls back to back between one pair of events
+    (a lone call between events is padded by the events' own gaps)."""
+    a, b = H.create(), H.create()
+    L.route()
+    H.record(a, stream)
+    for _ in range(reps):
+        L.route()
+    H.record(b, stream)
+    H.sync(b)
+    ms = H.ms(a, b) / reps
+    H.destroy(a)
+    H.destroy(b)
+    return ms
+
+
+def hbm_report(w, stages, copy_gbs):
+    """GB/s of the memory-bound kernels from their stage times."""
+    names = {"route": "route", "combine": "fwd.combine", "reverse_combine": "bwd.reverse_combine",
+             "dw_router": "bwd.dw_router"}
+    out = {}
+    for k, nb in hbm_bytes(w).items():
+        ms = stages.get(names[k])
+        if not ms:
+            continue
+        gbs = nb / (ms * 1e-3) / 1e9
+        out[k] = {"bytes": nb, "ms": round(ms, 4), "GB/s": round(gbs, 1),
+                  "frac_of_8TBs": round(gbs / PEAK_HBM_GBS, 3),
+                  "frac_of_copy": round(gbs / copy_gbs, 3) if copy_gbs else None}
+    if "plan" in stages:
+        out["plan"] = {"us": round(1e3 * stages["plan"], 2), "bound": "latency"}
+    return out
+
+
+def expert_roofline_ms(w, counts):
+    """Sum over experts of max(FLOPs / peak, bytes / HBM) for the routed
+    up/gate and down GEMMs of a forward: FLOPs 6 M_e d f; bytes the expert's
+    three bf16 weight matrices plus its rows (X read, H written and read,
+    Yexp written).  Small experts are bound by reading their weights."""
+    d, f = w.d, w.f
+    t = 0.0
+    for m in counts:
+        m = int(m)
+        if m == 0:
+            continue
+        fl = 6.0 * m * d * f
+        by = 6.0 * d * f + m * (2.0 * d + 4.0 * f + 2.0 * d)
+        t += max(fl / (PEAK_BF16_TFLOPS * 1e12), by / (PEAK_HBM_GBS * 1e9))
+    return 1e3 * t
+
+
+def forward_config_timing(H, stream, name, steps, warmup, copy_gbs, inputs=None):
+    """route + plan + forward of one forward configuration: per-stage times
+    (from steps with events at every stage boundary), then `steps` timed
+    passes with events only around each pass; median and mean."""
+    import numpy as np
+    import torch
+    from paper_2609_36070_amd import binding as B
+    from paper_2609_36070_amd.layer import DeviceLayer
+    from paper_2609_36070_amd.workloads import WORKLOADS, make_inputs
+    w = WORKLOADS[name]
+    if inputs is None:
+        inputs = make_inputs(w, seed=0)
+    L = DeviceLayer(w, inputs, with_backward=False)
+    for _ in range(warmup):
+        L.route()
+        L.plan()
+        L.forward()
+    torch.cuda.synchronize()
+    nf = len(B.FWD_STAGES) + 1
+    stages = {}
+    route_ms = route_time(H, stream, L)
+    nstage = 3
+    for _ in range(nstage):
+        e0, e1 = H.create(), H.create()
+        ev = [H.create() for _ in range(nf)]
+        fe = B.MoeStageEvents()
+        for i, e in enumerate(ev):
+            fe.ev[i] = e
+        H.record(e0, stream)
+        L.route()
+        H.record(e1, stream)
+        L.plan()
+        L.forward(events=fe)
+        H.sync(ev[-1])
+        stages["route"] = stages.get("route", 0.0) + H.ms(e0, e1) / nstage
+        stages["plan"] = stages.get("plan", 0.0) + H.ms(e1, ev[0]) / nstage
+        for i, st in enumerate(B.FWD_STAGES):
+            stages["fwd." + st] = stages.get("fwd." + st, 0.0) + H.ms(ev[i], ev[i + 1]) / nstage
+        for e in [e0, e1] + ev:
+            H.destroy(e)
+    marks = [(H.create(), H.create()) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in marks:
+        H.record(a, stream)
+        L.route()
+        L.plan()
+        L.forward()
+        H.record(b, stream)
+    H.sync(marks[-1][1])
+    times = sorted(H.ms(a, b) for a, b in marks)
+    for a, b in marks:
+        H.destroy(a)
+        H.destroy(b)
+    med = times[len(times) // 2]
+    mean = sum(times) / len(times)
+    fl = w.fwd_flops()
+    fwd_fl, _ = stage_flops(w)
+    counts = L.counts.cpu().numpy()
+    out = {"workload": name, "T": w.T, "d": w.d, "E": w.E, "k": w.k, "f": w.f, "f_shared": w.f_s,
+           "passes": "fwd", "step": "route+plan+forward", "steps": steps,
+           "ms_median": round(med, 4), "ms_mean": round(mean, 4),
+           "tflops": round(fl / (med * 1e-3) / 1e12, 2),
+           "tokens_per_s": round(w.T / (med * 1e-3), 1),
+           "frac_of_bf16_peak": round(fl / (med * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+           "frac_of_2300": round(fl / (med * 1e-3) / 1e12 / PEAK_BF16_TFLOPS_ALT, 4),
+           "expert_load": {"min": int(counts.min()), "mean": round(float(counts.mean()), 1),
+                           "max": int(counts.max())},
+           "stages": {}}
+    for st, ms in stages.items():
+        out["stages"][st] = {"ms": round(ms, 4)}
+        key = st.split(".", 1)[-1]
+        if st.startswith("fwd.") and key in fwd_fl and ms > 0 and fwd_fl[key][0] > 0:
+            out["stages"][st]["tflops"] = round(fwd_fl[key][0] / (ms * 1e-3) / 1e12, 1)
+    gemm_ms = sum(stages.get("fwd." + k, 0.0) for k in ("up_routed", "down_routed"))
+    roof = expert_roofline_ms(w, counts)
+    out["routed_expert_gemms"] = {"ms": round(gemm_ms, 4), "roofline_ms": round(roof, 4),
+                                  "frac_of_roofline": round(roof / gemm_ms, 4) if gemm_ms else None}
+    out["hbm"] = hbm_report(w, dict(stages, route=route_ms), copy_gbs)
+    del L
+    torch.cuda.synchronize()
+    return out
+
+
+def graph_step_timing(H, stream, L, reps):
+    """The whole step captured in one HIP graph and replayed `reps` times,
+    with an event pair around each replay; median and mean of the replays."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        L.step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        L.step()
+    torch.cuda.synchronize()
+    graph.replay()
+    torch.cuda.synchronize()
+    marks = [(H.create(), H.create()) for _ in range(reps)]
+    for a, b in marks:
+        H.record(a, stream)
+        graph.replay()
+        H.record(b, stream)
+    H.sync(marks[-1][1])
+    times = sorted(H.ms(a, b) for a, b in marks)
+    for a, b in marks:
+        H.destroy(a)
+        H.destroy(b)
+    del graph
+    torch.cuda.synchronize()
+    return {"replays": reps, "ms_median": round(times[len(times) // 2], 4),
+            "ms_mean": round(sum(times) / len(times), 4), "ms_min": round(times[0], 4)}
+
+
+def host_info():
+    """CPU model, usable cores and the BLAS numpy calls into."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = None
+    try:
+        from threadpoolctl import threadpool_info
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                blas = f"{i.get('internal_api')} {i.get('version')} ({i.get('num_threads')} threads)"
+                break
+    except Exception:  # pragma: no cover
+        pass
+    return {"cpu_model": model, "affinity_cores": len(os.sched_getaffinity(0)), "blas": blas}
+
+
 def cpu_baseline(w, inputs, sample_tokens):
     """Time the CPU oracle on the first `sample_tokens` tokens of the workload."""
     import numpy as np
     from oracle import moe_oracle as O
+    info = host_info()
+    cores = info["affinity_cores"]
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        used = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+        if used:
+            cores = min(cores, max(used))   # the BLAS threads the oracle's products ran on
     except Exception:  # pragma: no cover
-        cores = len(os.sched_getaffinity(0))
+        pass
     n = min(sample_tokens, w.T)
     X = inputs["X"][:n]
     W = {key: inputs.get(key) for key in ("W_gate", "W_up", "W_down", "Wg_s", "Wu_s", "Wd_s")}
@@ -369,7 +611,8 @@ def cpu_baseline(w, inputs, sample_tokens):
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
             "sample": f"first {n} of {w.T} tokens, all {w.k} routes each, full weights; "
                       f"route+plan+forward{'+backward' if w.backward else ''} in fp64 numpy; "
-                      f"{dt:.1f} s"}
+                      f"{dt:.1f} s",
+            "seconds": round(dt, 2), "tokens_per_s": round(n / dt, 1), **info}
 
 
 def main():
@@ -390,6 +633,8 @@ def main():
     ap.add_argument("--ring-only", type=int, default=0, metavar="ROWS",
                     help="time only steps in bounded-memory execution with a ring of ROWS rows "
                          "(for kernel traces of that mode); prints its own JSON line")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the forward-only configurations measured beside the step")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (the reference "
                          "kernel for scaling HBM byte counters)")
@@ -537,7 +782,8 @@ def main():
     roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic(dom, w.name),
-                "avg_launch_ms": round(avg_ms, 4), "flops_per_launch": fl}
+                "avg_launch_ms": round(avg_ms, 4), "flops_per_launch": fl,
+                "frac_of_2300": round(achieved / PEAK_BF16_TFLOPS_ALT, 4)}
 
     step_flops = w.fwd_flops() + (w.bwd_flops() if w.backward else 0.0)
     value = step_flops / (ms_step * 1e-3) / 1e12
@@ -551,6 +797,28 @@ def main():
             stage_report[name]["tflops"] = round(fl / (ms * 1e-3) / 1e12, 1) if ms > 0 else None
     for name, v in stage_report.items():
         log(f"   {name:28s} {v['ms']:9.4f} ms  {v.get('tflops', '')}")
+
+    copy = copy_ceiling(H, stream)
+    log(f"[bench] device-to-device copy: {copy['GB/s']} GB/s (read + write)")
+    hbm = hbm_report(w, dict(stages, route=route_time(H, stream, L)), copy["GB/s"])
+    for name, v in hbm.items():
+        log(f"   hbm {name:18s} {v}")
+
+    graph = graph_step_timing(H, stream, L, max(5, args.steps))
+    log(f"[bench] graph-replayed step: median {graph['ms_median']:.3f} ms over {graph['replays']} replays")
+
+    configs = None
+    if not args.no_configs:
+        configs = {}
+        for cname in FORWARD_CONFIGS:
+            t_c = time.perf_counter()
+            same = cname == "large_shared" and w.name == "large_shared_train"
+            c = forward_config_timing(H, stream, cname, max(5, args.steps), 2, copy["GB/s"],
+                                      inputs=inputs if same else None)
+            configs[cname] = c
+            log(f"[bench] config {cname}: {c['ms_median']:.3f} ms median, {c['tflops']} TFLOP/s, "
+                f"{c['tokens_per_s']:.0f} tok/s, routed GEMMs {c['routed_expert_gemms']} "
+                f"({time.perf_counter() - t_c:.1f} s)")
 
     mxf = None
     if not args.no_mx and w.name in ("large_shared", "large_shared_train"):
@@ -613,9 +881,14 @@ def main():
                    "step": "route+plan+forward" + ("+backward" if w.backward else "")},
         "tokens_per_s": round(w.T / (ms_step * 1e-3), 1),
         "frac_of_bf16_peak": round(value / PEAK_BF16_TFLOPS, 4),
+        "frac_of_2300": round(value / PEAK_BF16_TFLOPS_ALT, 4),
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "graph_replay": graph,
+        "hbm_copy": copy,
+        "hbm_kernels": hbm,
         "stages": stage_report,
+        "forward_configs": configs,
         "schedule": sched,
         "mxfp8_forward": mxf,
         "mxfp8_training_step": mxt,

@@ -45,3 +45,27 @@ def test_traffic_record_is_reported_only_for_the_current_sources(monkeypatch):
     monkeypatch.setattr(bench, "source_sha256", lambda: "0" * 64)
     assert bench.measured_traffic(rec["kernel"], rec["workload"]) is None
     assert bench.measured_traffic("no such kernel", rec["workload"]) is None
+
+
+def test_hbm_bytes_follow_the_per_kernel_formulas():
+    """Route 2Td + 2dE + 4TE + 8Tk and combine 2Rd + 2Td (shared) + 2Td + 8R
+    (236.6 MB and 2.35 GB at the large-shared layer)."""
+    w = WORKLOADS["large_shared_train"]
+    b = bench.hbm_bytes(w)
+    assert b["route"] == 236_568_576
+    assert b["combine"] == 2_349_858_816
+    assert b["dw_router"] == 2 * w.T * w.d + 4 * w.T * w.E + 4 * w.d * w.E
+    assert "reverse_combine" in b
+    assert "reverse_combine" not in bench.hbm_bytes(WORKLOADS["large_shared"])
+
+
+def test_expert_roofline_closed_forms():
+    """Large experts are bound by their FLOPs, tiny ones by their weights,
+    empty ones cost nothing."""
+    w = WORKLOADS["many_experts"]
+    big = 10 ** 6
+    t = bench.expert_roofline_ms(w, [big])
+    assert t == pytest.approx(1e3 * 6.0 * big * w.d * w.f / (bench.PEAK_BF16_TFLOPS * 1e12))
+    t1 = bench.expert_roofline_ms(w, [1])
+    assert t1 == pytest.approx(1e3 * (6.0 * w.d * w.f + 4.0 * w.d + 4.0 * w.f) / (bench.PEAK_HBM_GBS * 1e9))
+    assert bench.expert_roofline_ms(w, [0, 0]) == 0.0
