@@ -66,6 +66,16 @@ class HipEvents:
         self.h.hipEventDestroy(e)
 
 
+def dense_routing(w):
+    """Every token routes to every local expert (k == E): the library folds
+    the combine into the down GEMM (its stage "down_routed" then also holds
+    the shared down product, and "down_shared" and "combine" are empty) and
+    the reverse combine into one dX GEMM over every expert, the shared expert
+    and the router term (stage "dx_shared"; "dx_routed" and
+    "reverse_combine" are empty)."""
+    return w.k == w.E
+
+
 def stage_flops(w):
     """Algorithmic FLOPs of each timed stage and launches per stage."""
     R, d, f, fs, T = w.T * w.k, w.d, w.f, w.f_s, w.T
@@ -75,6 +85,11 @@ def stage_flops(w):
            "wgrad_gate_up": (4.0 * R * d * f, 2), "wgrad_down": (2.0 * R * f * d, 1),
            "dgrad_shared": (2.0 * T * d * fs, 1), "dx_shared": (4.0 * T * fs * d, 1),
            "wgrad_shared": (6.0 * T * d * fs, 3)}
+    if dense_routing(w):
+        fwd["down_routed"] = (2.0 * (R * f + T * fs) * d, 1)
+        fwd["down_shared"] = (0.0, 0)
+        bwd["dx_shared"] = (4.0 * (R * f + T * fs) * d, 1)
+        bwd["dx_routed"] = (0.0, 0)
     return fwd, bwd
 
 
@@ -413,9 +428,10 @@ def hbm_report(w, stages, copy_gbs):
     names = {"route": "route", "combine": "fwd.combine", "reverse_combine": "bwd.reverse_combine",
              "dw_router": "bwd.dw_router"}
     out = {}
+    folded = ("combine", "reverse_combine") if dense_routing(w) else ()
     for k, nb in hbm_bytes(w).items():
         ms = stages.get(names[k])
-        if not ms:
+        if not ms or k in folded:       # dense routing folds the combines into GEMMs
             continue
         gbs = nb / (ms * 1e-3) / 1e9
         out[k] = {"bytes": nb, "ms": round(ms, 4), "GB/s": round(gbs, 1),
@@ -516,6 +532,8 @@ def forward_config_timing(H, stream, name, steps, warmup, copy_gbs, inputs=None)
         key = st.split(".", 1)[-1]
         if st.startswith("fwd.") and key in fwd_fl and ms > 0 and fwd_fl[key][0] > 0:
             out["stages"][st]["tflops"] = round(fwd_fl[key][0] / (ms * 1e-3) / 1e12, 1)
+    # routed expert GEMMs (with dense routing the folded down GEMM also holds
+    # the shared expert's down product: its share of the time is left in)
     gemm_ms = sum(stages.get("fwd." + k, 0.0) for k in ("up_routed", "down_routed"))
     roof = expert_roofline_ms(w, counts)
     out["routed_expert_gemms"] = {"ms": round(gemm_ms, 4), "roofline_ms": round(roof, 4),
@@ -748,17 +766,22 @@ def main():
     # kernels that run as exactly one instance per launch shape: (phase, first
     # stage, end stage, launches, FLOPs per launch)
     fi, bi = B.FWD_STAGES.index, B.BWD_STAGES.index
+    dense = dense_routing(w)
     kern = {
         "gemm up/gate+SwiGLU (routed)": ("fwd", fi("up_routed"), fi("up_routed") + 1, 1,
                                          fwd_fl["up_routed"][0]),
-        "gemm down (routed)": ("fwd", fi("down_routed"), fi("down_routed") + 1, 1,
-                               fwd_fl["down_routed"][0]),
+        ("gemm down + combine (all experts)" if dense else "gemm down (routed)"):
+            ("fwd", fi("down_routed"), fi("down_routed") + 1, 1, fwd_fl["down_routed"][0]),
     }
     if w.backward:
         kern["gemm dgrad+SwiGLU bwd (routed)"] = ("bwd", bi("dgrad_routed"), bi("dgrad_routed") + 1, 1,
                                                   bwd_fl["dgrad_routed"][0])
-        kern["gemm dX (routed)"] = ("bwd", bi("dx_routed"), bi("dx_routed") + 1, 1,
-                                    bwd_fl["dx_routed"][0])
+        if dense:
+            kern["gemm dX + reverse combine (all experts)"] = ("bwd", bi("dx_shared"), bi("dx_shared") + 1,
+                                                               1, bwd_fl["dx_shared"][0])
+        else:
+            kern["gemm dX (routed)"] = ("bwd", bi("dx_routed"), bi("dx_routed") + 1, 1,
+                                        bwd_fl["dx_routed"][0])
         kern["gemm weight grad (routed)"] = ("bwd", bi("wgrad_gate_up"), bi("wgrad_down") + 1, 3,
                                              2.0 * w.T * w.k * w.d * w.f)
 

@@ -97,7 +97,11 @@ typedef struct {
     float *dWd_s;    /* [f_shared, d], NULL iff f_shared == 0 */
 } moe_grads;
 
-/* Named regions of the workspace, for inspection after a synchronisation. */
+/* Named regions of the workspace, for inspection after a synchronisation.
+ * With dense routing (k == E: every token routes to every local expert)
+ * moe_forward and moe_forward_fused keep w * h in MOE_WS_H and write neither
+ * MOE_WS_YEXP nor MOE_WS_YSH, and moe_backward does not write MOE_WS_DXPERM:
+ * the combines are folded into the down and dX products (see moe_forward). */
 typedef enum {
     MOE_WS_ERROR = 0,   /* int32[1], reset by moe_plan.  Bit 0: moe_plan
                            saw an expert id outside [0, E) (such routes are
@@ -371,7 +375,14 @@ moe_status moe_dispatch(const moe_shape *shape, const moe_bf16 *X,
  *   X [T, d], weights, topk_idx/topk_w from moe_route, plan from moe_plan.
  *   Y [T, d] bf16 out: Ysh[t] + sum over the token's experts in ascending
  *   id of w * f_e(x_t), accumulated in fp32 and rounded once.
- *   save_for_backward: keep A and B (gate/up pre-activations) in ws. */
+ *   save_for_backward: keep A and B (gate/up pre-activations) in ws.
+ * Dense routing (k == E; each token's k ids are then 0 .. E-1): the token's
+ * route to expert e is plan row offsets[e] + t, so the combine is one
+ * contraction over the experts' intermediate columns in ascending expert id
+ * followed by the shared expert's: Y[t] = sum_e (w h_e[t]) W_down[e] +
+ * h_s[t] Wd_s in one fp32 accumulator (w h rounded to bf16), rounded once.
+ * The same holds for dX in moe_backward (routed terms in ascending expert
+ * id, then the shared expert, then dZ[t] W_r^T, one fp32 accumulator). */
 moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weights *weights,
                        const int32_t *topk_idx, const float *topk_w,
                        const moe_plan_bufs *plan, moe_bf16 *Y, int save_for_backward,

@@ -26,7 +26,7 @@ struct Layout {
     size_t acc, coff;          // ring only: fp32 per-token accumulator, window regions
     size_t A, B, H, Yexp, As, Bs, Hs, Ysh;
     size_t fwd_total;
-    size_t dA, dB, Hw, dgpart, dg, dZ, dXperm, dAs, dBs, dXsh, dwr_part;
+    size_t dA, dB, Hw, dgpart, dg, dZ, dXperm, dAs, dBs, dXsh, dwr_part, dzs, wrs;
     size_t bwd_total;
     size_t xq, xs, hq, hsc;   // MXFP8 forward: quantised X and H (over the backward regions)
     size_t mx_total;
@@ -90,6 +90,8 @@ Layout make_layout(const moe_shape &s, long ring_rows = -1) {
     L.dBs = take(T * fs * 2);
     L.dXsh = take(T * d * 2);
     L.dwr_part = take((size_t)dwr_nchunks((long)T) * d * E * 4);
+    L.dzs = take(T * 64 * 2);   // dense routing: router-term rows of dX
+    L.wrs = take(d * 64 * 2);
     L.bwd_total = o;
     o = L.fwd_total;
     L.xq = take(T * d);
@@ -430,46 +432,48 @@ GemmArgs wgrad_args(const moe_shape &sh, const Layout &L, void *ws, const moe_bf
     return g;
 }
 
-// Shared-expert backward: dAs/dBs, dXsh and its three weight gradients.
-// Marks stages 7 and 8 of the stage events between its GEMMs.
-hipError_t shared_backward(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *dY,
-                           const moe_bf16 *X, const moe_weights *w, const moe_grads *gr,
-                           const StageMarks &mk, hipStream_t s) {
+// Shared-expert backward, in three parts: dAs/dBs (the gated-activation
+// backward on the saved As, Bs), dXsh, and the three weight gradients.
+hipError_t shared_dgrad(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *dY,
+                        const moe_weights *w, hipStream_t s) {
+    const int T = (int)sh.T, d = (int)sh.d, fs = (int)sh.f_shared;
+    GemmArgs g;
+    g.zeros = at<uint16_t>(ws, L.zeros);
+    g.A = dY; g.lda = d; g.a_nrows = T > 0 ? T : 1; g.M = T;
+    g.B = w->Wd_s; g.ldb = d;
+    g.N = fs; g.K = d;
+    g.E1 = at<uint16_t>(ws, L.As); g.E2 = at<uint16_t>(ws, L.Bs); g.ldc = fs;
+    g.C = at<uint16_t>(ws, L.dAs); g.C2 = at<uint16_t>(ws, L.dBs);
+    return launch_gemm_bwd_dgrad(g, T, 1, s);
+}
+
+hipError_t shared_dx(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w,
+                     hipStream_t s) {
+    const int T = (int)sh.T, d = (int)sh.d, fs = (int)sh.f_shared;
+    GemmArgs g;
+    g.zeros = at<uint16_t>(ws, L.zeros);
+    g.A = at<uint16_t>(ws, L.dAs); g.A2 = at<uint16_t>(ws, L.dBs); g.lda = fs;
+    g.a_nrows = T > 0 ? T : 1; g.M = T;
+    g.B = w->Wg_s; g.B2 = w->Wu_s; g.ldb = fs;
+    g.N = d; g.K = fs;
+    g.C = at<uint16_t>(ws, L.dXsh); g.ldc = d;
+    return launch_gemm_bwd_dx(g, T, 1, s);
+}
+
+hipError_t shared_wgrads(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *dY,
+                         const moe_bf16 *X, const moe_grads *gr, hipStream_t s) {
     const int T = (int)sh.T, d = (int)sh.d, fs = (int)sh.f_shared;
     const int Tn = T > 0 ? T : 1;
-    uint16_t *dAs = at<uint16_t>(ws, L.dAs), *dBs = at<uint16_t>(ws, L.dBs);
-    uint16_t *dXsh = at<uint16_t>(ws, L.dXsh);
     hipError_t e;
     {
         GemmArgs g;
         g.zeros = at<uint16_t>(ws, L.zeros);
-        g.A = dY; g.lda = d; g.a_nrows = Tn; g.M = T;
-        g.B = w->Wd_s; g.ldb = d;
-        g.N = fs; g.K = d;
-        g.E1 = at<uint16_t>(ws, L.As); g.E2 = at<uint16_t>(ws, L.Bs); g.ldc = fs;
-        g.C = dAs; g.C2 = dBs;
-        if ((e = launch_gemm_bwd_dgrad(g, T, 1, s)) != hipSuccess) return e;
-    }
-    if ((e = mk.mark(7)) != hipSuccess) return e;
-    {
-        GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
-        g.A = dAs; g.A2 = dBs; g.lda = fs; g.a_nrows = Tn; g.M = T;
-        g.B = w->Wg_s; g.B2 = w->Wu_s; g.ldb = fs;
-        g.N = d; g.K = fs;
-        g.C = dXsh; g.ldc = d;
-        if ((e = launch_gemm_bwd_dx(g, T, 1, s)) != hipSuccess) return e;
-    }
-    if ((e = mk.mark(8)) != hipSuccess) return e;
-    {
-        GemmArgs g;
-        g.zeros = at<uint16_t>(ws, L.zeros);
         g.A = X; g.lda = d; g.a_nrows = Tn;
-        g.B = dAs; g.ldb = fs; g.b_nrows = Tn;
+        g.B = at<uint16_t>(ws, L.dAs); g.ldb = fs; g.b_nrows = Tn;
         g.M = d; g.N = fs; g.K = T;
         g.Cf = gr->dWg_s; g.ldc = fs;
         if ((e = launch_gemm_wgrad(g, 1, s)) != hipSuccess) return e;
-        g.B = dBs; g.Cf = gr->dWu_s;
+        g.B = at<uint16_t>(ws, L.dBs); g.Cf = gr->dWu_s;
         if ((e = launch_gemm_wgrad(g, 1, s)) != hipSuccess) return e;
     }
     GemmArgs g;
@@ -479,6 +483,71 @@ hipError_t shared_backward(const moe_shape &sh, const Layout &L, void *ws, const
     g.M = fs; g.N = d; g.K = T;
     g.Cf = gr->dWd_s; g.ldc = d;
     return launch_gemm_wgrad(g, 1, s);
+}
+
+// The whole shared-expert backward.  Marks stages 7 and 8 of the stage
+// events between its GEMMs.
+hipError_t shared_backward(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *dY,
+                           const moe_bf16 *X, const moe_weights *w, const moe_grads *gr,
+                           const StageMarks &mk, hipStream_t s) {
+    hipError_t e;
+    if ((e = shared_dgrad(sh, L, ws, dY, w, s)) != hipSuccess) return e;
+    if ((e = mk.mark(7)) != hipSuccess) return e;
+    if ((e = shared_dx(sh, L, ws, w, s)) != hipSuccess) return e;
+    if ((e = mk.mark(8)) != hipSuccess) return e;
+    return shared_wgrads(sh, L, ws, dY, X, gr, s);
+}
+
+// Dense routing (k == E): every token routes to every local expert, so its
+// route to expert e sits at row offsets[e] + t of the plan, and the combine
+// (sum over the token's experts in ascending id, plus the shared expert) is a
+// contraction over the experts' concatenated intermediate columns.  The down
+// product then writes Y directly from fp32, with no per-route output and no
+// combine pass; the dX product likewise writes dX with the shared expert's
+// and the router's terms.
+bool dense_routing(const moe_shape &sh) { return sh.k == sh.E; }
+
+// Y = sum_e (w h)_e W_down[e] + Hs Wd_s over K segments (H holds w h).
+GemmArgs down_cmb_args(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w,
+                       const int *offsets, moe_bf16 *Y) {
+    const int T = (int)sh.T, d = (int)sh.d, f = (int)sh.f, fs = (int)sh.f_shared;
+    const long R = (long)T * sh.k;
+    GemmArgs g;
+    g.zeros = at<uint16_t>(ws, L.zeros);
+    g.A = at<uint16_t>(ws, L.H); g.lda = f; g.a_nrows = R > 0 ? (int)R : 1;
+    g.B = w->W_down; g.ldb = d; g.b_estride = (long)f * d;
+    g.M = T; g.N = d;
+    g.seg_offsets = offsets; g.nseg = (int)sh.E; g.segK = f;
+    if (fs > 0) {
+        g.segK_s = fs;
+        g.As = at<uint16_t>(ws, L.Hs); g.lda_s = fs;
+        g.Bs = w->Wd_s; g.ldb_s = d;
+    }
+    g.C = Y; g.ldc = d;
+    return g;
+}
+
+// dX = sum_e (dA W_gate[e]^T + dB W_up[e]^T) + dAs Wg_s^T + dBs Wu_s^T +
+// dZ W_r^T over K segments (the router term from the split rows).
+GemmArgs dx_cmb_args(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w,
+                     const int *offsets, moe_bf16 *dX) {
+    const int T = (int)sh.T, d = (int)sh.d, f = (int)sh.f, fs = (int)sh.f_shared;
+    const long R = (long)T * sh.k;
+    GemmArgs g;
+    g.zeros = at<uint16_t>(ws, L.zeros);
+    g.A = at<uint16_t>(ws, L.dA); g.A2 = at<uint16_t>(ws, L.dB); g.lda = f;
+    g.a_nrows = R > 0 ? (int)R : 1;
+    g.B = w->W_gate; g.B2 = w->W_up; g.ldb = f; g.b_estride = (long)d * f;
+    g.M = T; g.N = d;
+    g.seg_offsets = offsets; g.nseg = (int)sh.E; g.segK = f;
+    if (fs > 0) {
+        g.segK_s = fs;
+        g.As = at<uint16_t>(ws, L.dAs); g.As2 = at<uint16_t>(ws, L.dBs); g.lda_s = fs;
+        g.Bs = w->Wg_s; g.Bs2 = w->Wu_s; g.ldb_s = fs;
+    }
+    g.Ar = at<uint16_t>(ws, L.dzs); g.Br = at<uint16_t>(ws, L.wrs);
+    g.C = dX; g.ldc = d;
+    return g;
 }
 
 moe_status check_backward_args(const moe_shape *shape, const moe_bf16 *dY, const moe_bf16 *X,
@@ -666,6 +735,21 @@ moe_status moe_forward(const moe_shape *shape, const moe_bf16 *X, const moe_weig
     MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, at<int>(ws, L.rowidx),
                         at<float>(ws, L.wperm), at<uint16_t>(ws, L.zeros), s));
     MOE_TRY(mk.mark(1));
+    if (dense_routing(*shape)) {
+        // H keeps w h; the down product adds every expert and the shared
+        // expert into Y (stages 4 and 5 are empty)
+        GemmArgs gu = up_args(*shape, L, ws, X, weights, all, true, save_for_backward != 0);
+        gu.rowscale = at<float>(ws, L.wperm);
+        MOE_TRY(launch_gemm_fwd_up(gu, all.count(), E, s));
+        MOE_TRY(mk.mark(2));
+        if (fs > 0) MOE_TRY(shared_up(*shape, L, ws, X, weights, save_for_backward != 0, s));
+        MOE_TRY(mk.mark(3));
+        MOE_TRY(launch_gemm_fwd_down_cmb(down_cmb_args(*shape, L, ws, weights, plan->offsets, Y), s));
+        MOE_TRY(mk.mark(4));
+        MOE_TRY(mk.mark(5));
+        MOE_TRY(mk.mark(6));
+        return MOE_OK;
+    }
     MOE_TRY(routed_up(*shape, L, ws, X, weights, all, true, save_for_backward != 0, s));
     MOE_TRY(mk.mark(2));
     if (fs > 0) MOE_TRY(shared_up(*shape, L, ws, X, weights, save_for_backward != 0, s));
@@ -701,10 +785,14 @@ moe_status moe_forward_fused(const moe_shape *shape, const moe_bf16 *X, const mo
     MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, at<int>(ws, L.rowidx),
                         at<float>(ws, L.wperm), at<uint16_t>(ws, L.zeros), s));
     const GemmArgs none;
-    MOE_TRY(launch_fused_forward(shared ? shared_up_args(*shape, L, ws, X, weights, save) : none,
-                                 up_args(*shape, L, ws, X, weights, all, true, save),
-                                 shared ? shared_down_args(*shape, L, ws, weights) : none,
-                                 down_args(*shape, L, ws, weights, all), shared, T, R, E,
+    const bool dense = dense_routing(*shape);
+    GemmArgs gu = up_args(*shape, L, ws, X, weights, all, true, save);
+    if (dense) gu.rowscale = at<float>(ws, L.wperm);
+    MOE_TRY(launch_fused_forward(shared ? shared_up_args(*shape, L, ws, X, weights, save) : none, gu,
+                                 shared && !dense ? shared_down_args(*shape, L, ws, weights) : none,
+                                 dense ? down_cmb_args(*shape, L, ws, weights, plan->offsets, Y)
+                                       : down_args(*shape, L, ws, weights, all),
+                                 shared, dense, T, R, E,
                                  at<uint16_t>(ws, L.Yexp), at<uint16_t>(ws, L.Ysh), topk_w,
                                  plan->route_pos, topk_idx, plan->offsets, d, k, Y,
                                  at<int>(ws, L.fused), at<int>(ws, L.err), s));
@@ -734,6 +822,30 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
     MOE_TRY(mk.mark(2));
     MOE_TRY(launch_softmax_bwd(at<float>(ws, L.dgpart), L.dg_parts, plan->route_pos, topk_w, topk_idx,
                                T, k, E, at<float>(ws, L.dg), dZ, s));
+    if (dense_routing(*shape)) {
+        // dX in one product over every expert, the shared expert and the
+        // router term (stage 3, the routed dX, and stage 10, the reverse
+        // combine, are empty; stage 7 is the whole dX)
+        const bool shared = shape->f_shared > 0;
+        MOE_TRY(launch_router_split(dZ, W_r, T, d, E, at<uint16_t>(ws, L.dzs), at<uint16_t>(ws, L.wrs), s));
+        MOE_TRY(mk.mark(3));
+        MOE_TRY(mk.mark(4));
+        MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, 0), E, s));
+        MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, 1), E, s));
+        MOE_TRY(mk.mark(5));
+        MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, 2), E, s));
+        MOE_TRY(mk.mark(6));
+        if (shared) MOE_TRY(shared_dgrad(*shape, L, ws, dY, weights, s));
+        MOE_TRY(mk.mark(7));
+        MOE_TRY(launch_gemm_bwd_dx_cmb(dx_cmb_args(*shape, L, ws, weights, plan->offsets, dX), s));
+        MOE_TRY(mk.mark(8));
+        if (shared) MOE_TRY(shared_wgrads(*shape, L, ws, dY, X, grads, s));
+        MOE_TRY(mk.mark(9));
+        MOE_TRY(launch_dwr(X, dZ, T, d, E, at<float>(ws, L.dwr_part), grads->dW_r, s));
+        MOE_TRY(mk.mark(10));
+        MOE_TRY(mk.mark(11));
+        return MOE_OK;
+    }
     MOE_TRY(mk.mark(3));
     MOE_TRY(routed_dx(*shape, L, ws, weights, all, s));
     MOE_TRY(mk.mark(4));

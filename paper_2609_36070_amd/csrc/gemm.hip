@@ -71,15 +71,18 @@ constexpr int LD_PER_OP = (BK / 2) / NWAVES;  // 1 KB direct loads per operand p
 constexpr int LOADS_PER_K = 2 * LD_PER_OP; // direct-load instructions per thread per K step
 static_assert(WN == 64 || WN == 128, "gate/up column pairs and the epilogue need 64- or 128-column wave tiles");
 
-enum Mode { FWD_UP = 0, FWD_DOWN = 1, BWD_DGRAD = 2, BWD_DX = 3, WGRAD = 4 };
+enum Mode { FWD_UP = 0, FWD_DOWN = 1, BWD_DGRAD = 2, BWD_DX = 3, WGRAD = 4, FWD_DOWN_CMB = 5,
+            BWD_DX_CMB = 6 };
 
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 
 template <int MODE>
 struct Traits {
     static constexpr bool A_COL = (MODE == WGRAD);                       // A stored [K][M]
-    static constexpr bool B_COL = (MODE == FWD_UP || MODE == FWD_DOWN || MODE == WGRAD);
+    static constexpr bool B_COL = (MODE == FWD_UP || MODE == FWD_DOWN || MODE == WGRAD ||
+                                   MODE == FWD_DOWN_CMB);
     static constexpr bool GROUPED_ROWS = (MODE != WGRAD);
+    static constexpr bool CMB = (MODE == FWD_DOWN_CMB || MODE == BWD_DX_CMB);   // K segments
 };
 
 // Row tiles: 16-byte chunk c of row r lives at chunk c ^ ((r >> 2) & 3)
@@ -147,6 +150,8 @@ __shared__ __attribute__((aligned(16))) uint16_t lds_b0[TILE_ELEMS];
 __shared__ __attribute__((aligned(16))) uint16_t lds_a1[TILE_ELEMS];
 __shared__ __attribute__((aligned(16))) uint16_t lds_b1[TILE_ELEMS];
 __shared__ int s_info[2];
+// fused forward: first m-tile slot of every expert in the grouped raster
+__shared__ int s_tilebase[257];
 
 // One output tile of product MODE: workgroup vb of a grid of nvb (a multiple
 // of 8, so vb % 8 is the XCD the tile runs on).
@@ -255,7 +260,18 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
         }
         klen = g.K;
         slot = mt;
-        if (g.dep) wait_count(g.dep + mt, g.dep_need, g.err);
+        if constexpr (Tr::CMB) {
+            // fused dense forward: this token tile needs the up/gate tile of
+            // its tokens in every expert, and the shared expert's
+            if (g.dep) {
+                if (tid < g.nseg)
+                    poll_count(g.dep + min(s_tilebase[tid] + mt, g.dep_slots - 1), g.dep_need, g.err);
+                else if (tid == g.nseg && g.dep2) poll_count(g.dep2 + mt, g.dep_need2, g.err);
+                __syncthreads();
+            }
+        } else {
+            if (g.dep) wait_count(g.dep + mt, g.dep_need, g.err);
+        }
     } else {
         const int ntn = g.N / BN, ntm = g.M / BM;
         int cm = 0;   // (expert, m-tile) pair
@@ -292,7 +308,14 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
 #pragma unroll
     for (int i = 0; i < LD_PER_OP; ++i) lds_off[i] = (LD_PER_OP * wave + i) * 512;   // bf16 elements (1 KB)
 
-    if constexpr (!Tr::A_COL) {
+    // dense-routing products: element offsets of each load inside its
+    // segment's operand, for the three row pitches a segment can have (routed,
+    // shared, router); the segment only adds its base and K offset.  Every
+    // operand here holds fewer than 2^31 elements.
+    // token / output row of each load, its chunk, and (B col tiles) its column
+    uint32_t cm_t[LD_PER_OP], cm_c[LD_PER_OP], cm_b[LD_PER_OP];   // filled once col_of exists
+    if constexpr (Tr::CMB) {
+    } else if constexpr (!Tr::A_COL) {
 #pragma unroll
         for (int i = 0; i < LD_PER_OP; ++i) {
             const int r = ROWS_PER_LD * (LD_PER_OP * wave + i) + lane / (BK / 8);
@@ -307,7 +330,9 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
     } else {
         a_col_off = m0;
     }
-    if constexpr (!Tr::B_COL) {
+    if constexpr (Tr::CMB) {
+        // set above
+    } else if constexpr (!Tr::B_COL) {
 #pragma unroll
         for (int i = 0; i < LD_PER_OP; ++i) {
             const int r = ROWS_PER_LD * (LD_PER_OP * wave + i) + lane / (BK / 8);
@@ -328,7 +353,72 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
         return 16 * b + 8 * (slot & 1);
     };
 
-    const int nk = (MODE == BWD_DX) ? 2 * (g.K / BK) : (klen + BK - 1) / BK;
+    // dense routing: steps per routed segment, routed steps (E segments, two
+    // per expert for dX), shared steps, and the router step of dX
+    constexpr int CM_H = (MODE == BWD_DX_CMB) ? 2 : 1;
+    const int cm_sr = Tr::CMB ? g.segK / BK : 1;
+    const int cm_nr = Tr::CMB ? g.nseg * CM_H * cm_sr : 0;
+    const int cm_ss = Tr::CMB ? g.segK_s / BK : 1;
+    const int cm_ns = (Tr::CMB && g.segK_s > 0) ? CM_H * cm_ss : 0;
+    const int cm_nrt = (MODE == BWD_DX_CMB && g.Ar) ? 1 : 0;
+    if constexpr (Tr::CMB) {
+#pragma unroll
+        for (int i = 0; i < LD_PER_OP; ++i) {
+            const int r = ROWS_PER_LD * (LD_PER_OP * wave + i) + lane / (BK / 8);
+            // rows past the last token load the last token; they are never stored
+            cm_t[i] = (uint32_t)min(row0 + r, row_end - 1);
+            cm_c[i] = 8u * (uint32_t)row_swz(r, lane % (BK / 8));
+            if constexpr (Tr::B_COL) {
+                // the routed and shared down weights share the row pitch d
+                const int kr = 2 * (LD_PER_OP * wave + i) + (lane >> 5);
+                cm_b[i] = (uint32_t)(kr * g.ldb + n0 + col_of(kr));
+            } else {
+                cm_b[i] = (uint32_t)(n0 + r);
+            }
+        }
+    }
+    // segment sg: routed (expert sg / CM_H, half sg % CM_H), then shared
+    // (half), then the router step; bases at the segment's first K step
+    struct CmbSeg {
+        const uint16_t *ab, *bb;
+        uint32_t lda, ldb;
+        int len;
+    };
+    const int cm_nsr = Tr::CMB ? g.nseg * CM_H : 0;
+    const int cm_nsegs = cm_nsr + (cm_ns ? CM_H : 0) + cm_nrt;
+    auto cmb_enter = [&](int sg) {
+        CmbSeg c;
+        if (sg < cm_nsr) {
+            const int ex = sg / CM_H, half = sg - ex * CM_H;
+            // the tokens' rows in expert ex's region; an offset that a
+            // malformed plan would push past the buffer is clamped into it
+            const int off = min(max(uniform(g.seg_offsets[ex]), 0), g.a_nrows - g.M);
+            c.ab = (half ? g.A2 : g.A) + (long)off * g.lda;
+            c.bb = (half ? g.B2 : g.B) + (long)ex * g.b_estride;
+            c.lda = (uint32_t)g.lda;
+            c.ldb = (uint32_t)g.ldb;
+            c.len = cm_sr;
+        } else if (sg < cm_nsr + (cm_ns ? CM_H : 0)) {
+            const int half = sg - cm_nsr;
+            c.ab = half ? g.As2 : g.As;
+            c.bb = half ? g.Bs2 : g.Bs;
+            c.lda = (uint32_t)g.lda_s;
+            c.ldb = (uint32_t)g.ldb_s;
+            c.len = cm_ss;
+        } else {
+            c.ab = g.Ar;
+            c.bb = g.Br;
+            c.lda = 64u;
+            c.ldb = 64u;
+            c.len = 1;
+        }
+        return c;
+    };
+    int cs_sg = 0, cs_st = 0;
+    CmbSeg cs{};
+    if constexpr (Tr::CMB) cs = cmb_enter(0);
+    const int nk = Tr::CMB ? cm_nr + cm_ns + cm_nrt
+                 : (MODE == BWD_DX) ? 2 * (g.K / BK) : (klen + BK - 1) / BK;
     const int nk_half = g.K / BK;
 
     // Forward col tiles: this lane's source for each of its loads at K step
@@ -356,6 +446,25 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
         // this K step needs first (scalar loads, one wait), then issue the
         // direct loads.  A wave's k rows are consecutive plan positions, so
         // inside the expert's range they take one 4-index load per 4 rows.
+        if constexpr (Tr::CMB) {
+            // steps run in order: the current segment's bases advance by one
+            // K step per call, and a new segment is entered when one ends
+            const int kl = cs_st * BK;
+#pragma unroll
+            for (int i = 0; i < LD_PER_OP; ++i) {
+                // row offsets in 32 bits (token < 2^24, pitch < 2^21)
+                load_lds16(cs.ab + kl + (cm_t[i] * cs.lda + cm_c[i]), la + lds_off[i]);
+                if constexpr (Tr::B_COL)
+                    load_lds16(cs.bb + (long)kl * cs.ldb + cm_b[i], lb + lds_off[i]);
+                else
+                    load_lds16(cs.bb + kl + (cm_b[i] * cs.ldb + cm_c[i]), lb + lds_off[i]);
+            }
+            if (++cs_st == cs.len) {
+                cs_st = 0;
+                if (++cs_sg < cm_nsegs) cs = cmb_enter(cs_sg);
+            }
+            return;
+        }
         int pa[LD_PER_OP], pb[LD_PER_OP];
         if constexpr (MODE == WGRAD) {
             int ia[2 * LD_PER_OP], ib[2 * LD_PER_OP];
@@ -439,6 +548,19 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
             }
         }
     };
+
+    // FWD_UP with dense routing: the gate weights of this lane's epilogue
+    // rows, loaded now so that their round trips are long over by then
+    float wrow[TM][2];
+    if constexpr (MODE == FWD_UP) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const int p = min(row0 + wm * WM + 32 * i + (lane >> 2) + 16 * t, row_end - 1);
+                wrow[i][t] = g.rowscale ? g.rowscale[p] : 1.0f;
+            }
+    }
 
     f32x16_t acc[TM][TN];
 #pragma unroll
@@ -535,7 +657,8 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
     };
     if constexpr (MODE == FWD_UP) {
         // staged columns 64 jp + 0..31 hold the gate, 64 jp + 32..63 the up
-        // projection of the same 32 f columns
+        // projection of the same 32 f columns.  With dense routing each row
+        // is scaled by its gate weight (loaded before the K loop).
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             stage(i);
@@ -548,9 +671,11 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
                     const int p = row0 + wm * WM + 32 * i + row;
                     const f32x8 a = read8(row, 64 * jp + c), b = read8(row, 64 * jp + 32 + c);
                     if (p < row_end) {
+                        // dense routing keeps w h for the folded combine
+                        const float ws = wrow[i][t];
                         f32x8 h;
 #pragma unroll
-                        for (int k = 0; k < 8; ++k) h[k] = silu_f(a[k]) * b[k];
+                        for (int k = 0; k < 8; ++k) h[k] = ws * (silu_f(a[k]) * b[k]);
                         const long o = (long)p * g.ldc + fcol0 + c;
                         if (g.C) st_nt(g.C + o, pack_bf8(h));
                         if (g.C2) {
@@ -561,7 +686,8 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
                 }
             }
         }
-    } else if constexpr (MODE == FWD_DOWN || MODE == BWD_DX) {
+    } else if constexpr (MODE == FWD_DOWN || MODE == BWD_DX || MODE == FWD_DOWN_CMB ||
+                         MODE == BWD_DX_CMB) {
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             stage(i);
@@ -749,6 +875,14 @@ hipError_t launch_gemm_bwd_dgrad(const GemmArgs &g, long rows, int groups, hipSt
 hipError_t launch_gemm_bwd_dx(const GemmArgs &g, long rows, int groups, hipStream_t st) {
     return launch_mode<BWD_DX>(g, mtiles(g, rows, groups), g.N / BN, st);
 }
+hipError_t launch_gemm_fwd_down_cmb(const GemmArgs &g, hipStream_t st) {
+    if (g.offsets) return hipErrorInvalidValue;   // token tiles are not grouped
+    return launch_mode<FWD_DOWN_CMB>(g, (g.M + BM - 1) / BM, g.N / BN, st);
+}
+hipError_t launch_gemm_bwd_dx_cmb(const GemmArgs &g, hipStream_t st) {
+    if (g.offsets) return hipErrorInvalidValue;
+    return launch_mode<BWD_DX_CMB>(g, (g.M + BM - 1) / BM, g.N / BN, st);
+}
 hipError_t launch_gemm_wgrad(const GemmArgs &g, int groups, hipStream_t st) {
     return launch_mode<WGRAD>(g, groups * (g.M / BM), g.N / BN, st,
                               wgrad_grid(groups, g.M / BM, g.N / BN));
@@ -816,7 +950,8 @@ namespace {
 constexpr int FUSED_TB = 16;   // tokens per combine item (k <= 16: <= 256 route checks)
 
 struct FusedFwd {
-    GemmArgs g[4];       // shared up, routed up, shared down, routed down
+    GemmArgs g[4];       // shared up, routed up, shared down, routed down (dense: folded down)
+    int dense;           // every token routes to every expert: no combine phase
     int grid[4];         // workgroups of each product's own launch (multiple of 8)
     int base[6];         // queue item index where each phase starts (5 phases)
     int *queue;          // [8] tickets
@@ -831,7 +966,6 @@ struct FusedFwd {
 };
 
 __shared__ int s_ticket;
-__shared__ int s_tilebase[257];
 __shared__ int s_cpos[FUSED_TB * 16];     // combine item: route positions (-1: none)
 __shared__ float s_cwt[FUSED_TB * 16];    // and gate weights, [token][slot]
 
@@ -960,6 +1094,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void fused_forward_kernel(FusedFwd fa)
         if (P == 0) gemm_tile<FWD_UP, false, true>(fa.g[0], fa.g[0].a_rows, fa.g[0].b_rows, vb, fa.grid[0]);
         else if (P == 1) gemm_tile<FWD_UP, true, true>(fa.g[1], fa.g[1].a_rows, fa.g[1].b_rows, vb, fa.grid[1]);
         else if (P == 2) gemm_tile<FWD_DOWN, false, true>(fa.g[2], fa.g[2].a_rows, fa.g[2].b_rows, vb, fa.grid[2]);
+        else if (P == 3 && fa.dense) gemm_tile<FWD_DOWN_CMB, false, true>(fa.g[3], nullptr, nullptr, vb, fa.grid[3]);
         else if (P == 3) gemm_tile<FWD_DOWN, true, true>(fa.g[3], fa.g[3].a_rows, fa.g[3].b_rows, vb, fa.grid[3]);
         else fused_combine(fa, vb);
         __syncthreads();   // LDS of this item is free for the next
@@ -995,7 +1130,7 @@ int fused_counter_ints(long T, long R, int E) {
 }
 
 hipError_t launch_fused_forward(const GemmArgs &up_s, const GemmArgs &up_r, const GemmArgs &down_s,
-                                const GemmArgs &down_r, bool shared, long T, long R, int E,
+                                const GemmArgs &down_r, bool shared, bool dense, long T, long R, int E,
                                 const uint16_t *Yexp, const uint16_t *Ysh, const float *topk_w,
                                 const int *route_pos, const int *topk_idx, const int *offsets, int d,
                                 int k, uint16_t *Y, int *counters, int *err, hipStream_t st) {
@@ -1010,19 +1145,31 @@ hipError_t launch_fused_forward(const GemmArgs &up_s, const GemmArgs &up_r, cons
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
 
+    if (dense && (down_r.offsets || down_r.nseg != E || E > 256)) return hipErrorInvalidValue;
     FusedFwd fa{};
+    fa.dense = dense ? 1 : 0;
     fa.g[0] = up_s; fa.g[1] = up_r; fa.g[2] = down_s; fa.g[3] = down_r;
     const int ntn_up_s = shared ? up_s.N / (BN / 2) : 0, ntn_up_r = up_r.N / (BN / 2);
-    const int ntn_dn_s = shared ? down_s.N / BN : 0, ntn_dn_r = down_r.N / BN;
+    const int ntn_dn_s = (shared && !dense) ? down_s.N / BN : 0, ntn_dn_r = down_r.N / BN;
     fa.g[0].tiles_m = shared ? (int)tm_s : 0;
     fa.g[1].tiles_m = (int)tm_r;
-    fa.g[2].tiles_m = shared ? (int)tm_s : 0;
-    fa.g[3].tiles_m = (int)tm_r;
+    fa.g[2].tiles_m = (shared && !dense) ? (int)tm_s : 0;
+    // dense: the folded down product runs over token tiles
+    fa.g[3].tiles_m = dense ? (int)tm_s : (int)tm_r;
     const long tiles[4] = {(long)fa.g[0].tiles_m * ntn_up_s, (long)tm_r * ntn_up_r,
-                           (long)fa.g[2].tiles_m * ntn_dn_s, (long)tm_r * ntn_dn_r};
+                           (long)fa.g[2].tiles_m * ntn_dn_s, (long)fa.g[3].tiles_m * ntn_dn_r};
     fa.g[0].sig = up_done_s; fa.g[1].sig = up_done_r;
     fa.g[2].dep = up_done_s; fa.g[2].dep_need = ntn_up_s; fa.g[2].sig = down_done_s;
-    fa.g[3].dep = up_done_r; fa.g[3].dep_need = ntn_up_r; fa.g[3].sig = down_done_r;
+    fa.g[3].dep = up_done_r; fa.g[3].dep_need = ntn_up_r;
+    if (dense) {
+        // a token tile waits for its up/gate tile in every expert and in the
+        // shared expert; nothing waits for it
+        fa.g[3].dep2 = shared ? up_done_s : nullptr;
+        fa.g[3].dep_need2 = ntn_up_s;
+        fa.g[3].dep_slots = (int)tm_r;
+    } else {
+        fa.g[3].sig = down_done_r;
+    }
     for (int i = 0; i < 4; ++i) fa.g[i].err = err;
     long at = 0;
     const int ntns[4] = {ntn_up_s, ntn_up_r, ntn_dn_s, ntn_dn_r};
@@ -1031,7 +1178,7 @@ hipError_t launch_fused_forward(const GemmArgs &up_s, const GemmArgs &up_r, cons
         fa.base[i] = (int)at;
         at += fa.grid[i] / 8;
     }
-    const long nblk = (T + FUSED_TB - 1) / FUSED_TB;
+    const long nblk = dense ? 0 : (T + FUSED_TB - 1) / FUSED_TB;
     fa.base[4] = (int)at;
     at += (nblk + 7) / 8;
     fa.base[5] = (int)at;

@@ -47,6 +47,22 @@ struct GemmArgs {
     int dep_need = 0;
     int *sig = nullptr;
     int *err = nullptr;                // bit 1 set when a wait gave up
+    // Dense routing (every token routes to every one of the E experts): the
+    // K loop of a token tile runs over segments.  Routed segment e reads the
+    // plan rows of the tile's tokens in expert e's region (seg_offsets[e] +
+    // token) through A (and A2), against expert e's B (and B2); then the
+    // shared expert's segments (As / Bs, As2 / Bs2, width segK_s); BWD_DX_CMB
+    // ends with one 64-wide step of the router term (Ar, Br rows of 64).
+    const int *seg_offsets = nullptr;  // the plan's offsets [E+1]
+    int nseg = 0, segK = 0, segK_s = 0;
+    const uint16_t *As = nullptr, *As2 = nullptr, *Bs = nullptr, *Bs2 = nullptr;
+    long lda_s = 0, ldb_s = 0;
+    const uint16_t *Ar = nullptr, *Br = nullptr;
+    // fused dense forward: a token tile also waits for dep2[m-tile] >= dep_need2
+    // (the shared expert's up/gate tiles); dep is then indexed per expert
+    const int *dep2 = nullptr;
+    int dep_need2 = 0;
+    int dep_slots = 0;                 // counters in dep (per-expert indices are clamped to it)
 };
 
 int gemm_tile_m();
@@ -56,6 +72,17 @@ hipError_t launch_gemm_fwd_down(const GemmArgs &g, long rows, int groups, hipStr
 hipError_t launch_gemm_bwd_dgrad(const GemmArgs &g, long rows, int groups, hipStream_t st);
 hipError_t launch_gemm_bwd_dx(const GemmArgs &g, long rows, int groups, hipStream_t st);
 hipError_t launch_gemm_wgrad(const GemmArgs &g, int groups, hipStream_t st);
+// Dense routing (k == E): Y = sum over experts of (w h) W_down[e], plus the
+// shared expert, over one token tile's K segments (the combine folded into the
+// down product); dX likewise with dA W_gate^T + dB W_up^T per expert, the
+// shared expert and the router term.  g.M = T, g.N = d.
+hipError_t launch_gemm_fwd_down_cmb(const GemmArgs &g, hipStream_t st);
+hipError_t launch_gemm_bwd_dx_cmb(const GemmArgs &g, hipStream_t st);
+// Rows of 64 bf16 for the router term of the dense dX product: for dZ (fp32
+// [T][E]) the high and low bf16 parts of each value in columns e and 32 + e;
+// for W_r (bf16 [d][E]) the value in both.  E <= 32; other columns zero.
+hipError_t launch_router_split(const float *dZ, const uint16_t *W_r, int T, int d, int E,
+                               uint16_t *dz_split, uint16_t *wr_split, hipStream_t st);
 // Up to 4 grouped weight-gradient products (same groups), optionally with one
 // grouped up/gate product over `up_rows` plan rows, in one launch.
 // Fused persistent forward: shared up/gate, routed up/gate, shared down,
@@ -63,8 +90,10 @@ hipError_t launch_gemm_wgrad(const GemmArgs &g, int groups, hipStream_t st);
 // holds fused_counter_ints(...) ints; the launcher clears them first.  A
 // wait that gives up sets bit 1 of *err.
 int fused_counter_ints(long T, long R, int E);
+// With dense routing (down_r's mode is the folded down product: dense =
+// true) there is no combine phase: down_r's token tiles write Y.
 hipError_t launch_fused_forward(const GemmArgs &up_s, const GemmArgs &up_r, const GemmArgs &down_s,
-                                const GemmArgs &down_r, bool shared, long T, long R, int E,
+                                const GemmArgs &down_r, bool shared, bool dense, long T, long R, int E,
                                 const uint16_t *Yexp, const uint16_t *Ysh, const float *topk_w,
                                 const int *route_pos, const int *topk_idx, const int *offsets, int d,
                                 int k, uint16_t *Y, int *counters, int *err, hipStream_t st);

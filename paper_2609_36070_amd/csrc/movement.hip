@@ -521,6 +521,50 @@ __global__ __launch_bounds__(256) void dwr_reduce_kernel(const float *__restrict
 
 inline unsigned rows_grid(long rows) { return (unsigned)(rows < 16384 ? (rows > 0 ? rows : 1) : 16384); }
 
+// Rows of 64 bf16 for the router term of the dense dX product: row t < T
+// holds the high and low bf16 parts of dZ[t][e] (hi = RNE(v), lo = RNE(v - hi),
+// so hi + lo carries about 16 significant bits) in columns e and 32 + e; row
+// T + n holds W_r[n][e] in both.  Multiplying the two row sets over the 64
+// columns gives sum_e dZ[t][e] W_r[n][e] (hi W + lo W).  One thread per row.
+__global__ __launch_bounds__(256) void router_split_kernel(const float *__restrict__ dZ,
+                                                           const uint16_t *__restrict__ Wr, int T,
+                                                           int d, int E, uint16_t *__restrict__ dzs,
+                                                           uint16_t *__restrict__ wrs) {
+    const long i = (long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (long)T + d) return;
+    uint32_t w[32];
+#pragma unroll
+    for (int q = 0; q < 32; ++q) w[q] = 0u;
+    uint16_t *dst;
+    if (i < T) {
+#pragma unroll
+        for (int e = 0; e < 32; ++e) {
+            if (e < E) {
+                const float v = dZ[i * E + e];
+                const uint16_t hi = f2bf(v);
+                const uint16_t lo = f2bf(v - bf2f(hi));
+                w[e >> 1] |= (uint32_t)hi << (16 * (e & 1));
+                w[16 + (e >> 1)] |= (uint32_t)lo << (16 * (e & 1));
+            }
+        }
+        dst = dzs + i * 64;
+    } else {
+        const long n = i - T;
+#pragma unroll
+        for (int e = 0; e < 32; ++e) {
+            if (e < E) {
+                const uint32_t v = Wr[n * E + e];
+                w[e >> 1] |= v << (16 * (e & 1));
+                w[16 + (e >> 1)] |= v << (16 * (e & 1));
+            }
+        }
+        dst = wrs + n * 64;
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+        st_u32x4(dst + 8 * q, u32x4_t{w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]});
+}
+
 }  // namespace
 
 int dwr_nchunks(long T) { return (int)((T + DWR_TC - 1) / DWR_TC); }
@@ -601,5 +645,15 @@ hipError_t launch_dwr(const uint16_t *X, const float *dZ, int T, int d, int E, f
         dwr_partial_kernel<<<grid, dim3(256), 0, st>>>(X, dZ, T, d, E, part);
     }
     dwr_reduce_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st>>>(part, nch, n, dWr);
+    return hipGetLastError();
+}
+
+hipError_t launch_router_split(const float *dZ, const uint16_t *W_r, int T, int d, int E,
+                               uint16_t *dz_split, uint16_t *wr_split, hipStream_t st) {
+    if (E > 32) return hipErrorInvalidValue;
+    const long n = (long)T + d;
+    if (n <= 0) return hipSuccess;
+    router_split_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st>>>(dZ, W_r, T, d, E,
+                                                                                  dz_split, wr_split);
     return hipGetLastError();
 }

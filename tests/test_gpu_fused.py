@@ -22,15 +22,18 @@ RAGGED_TRAIN = Workload("ragged_train", T=1000, d=512, E=6, k=2, f=512, f_s=256,
 
 
 def regions(L, w):
+    """The forward's outputs; with dense routing (k == E) the combine is folded
+    into the down product, so Yexp and Ysh are not written."""
     R = w.T * w.k
     out = {"Y": L.Y.clone(),
-           "H": L.ws_tensor(B.WS_H, torch.bfloat16, (R, w.f)).clone(),
-           "Yexp": L.ws_tensor(B.WS_YEXP, torch.bfloat16, (R, w.d)).clone()}
+           "H": L.ws_tensor(B.WS_H, torch.bfloat16, (R, w.f)).clone()}
+    if w.k != w.E:
+        out["Yexp"] = L.ws_tensor(B.WS_YEXP, torch.bfloat16, (R, w.d)).clone()
+        if w.f_s:
+            out["Ysh"] = L.ws_tensor(B.WS_YSH, torch.bfloat16, (w.T, w.d)).clone()
     if L.with_backward:
         out["A"] = L.ws_tensor(B.WS_A, torch.bfloat16, (R, w.f)).clone()
         out["B"] = L.ws_tensor(B.WS_B, torch.bfloat16, (R, w.f)).clone()
-    if w.f_s:
-        out["Ysh"] = L.ws_tensor(B.WS_YSH, torch.bfloat16, (w.T, w.d)).clone()
     return out
 
 
@@ -59,8 +62,11 @@ def assert_bitwise(ref, got):
     say("  bitwise equal to moe_forward: " + ", ".join(ref))
 
 
-def test_fused_ragged_training_layer():
-    w = RAGGED_TRAIN
+@pytest.mark.parametrize("w", [RAGGED_TRAIN,
+                               Workload("dense_shared_train", T=700, d=512, E=4, k=4, f=512,
+                                        f_s=256, bias_std=0.5, backward=True)],
+                         ids=lambda w: w.name)
+def test_fused_training_layer(w):
     L, inp, ref, got = run_both(w, 21)
     assert_bitwise(ref, got)
     Zo, idx_g = check_route_and_plan(L, inp, w)
@@ -82,6 +88,7 @@ def test_fused_ragged_training_layer():
     Workload("many_tiles", T=700, d=768, E=3, k=2, f=768),
     Workload("no_shared_k16", T=600, d=256, E=32, k=16, f=256, bias_std=0.5),
     Workload("max_experts", T=2000, d=256, E=256, k=4, f=256, f_s=512, bias_std=1.0),
+    Workload("dense_shared", T=555, d=768, E=6, k=6, f=256, f_s=512, bias_std=0.5),
 ], ids=lambda w: w.name)
 def test_fused_edge_shapes(w):
     L, inp, ref, got = run_both(w, 22)

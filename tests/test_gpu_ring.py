@@ -4,9 +4,10 @@ reverse macrobatch order and the ring-aware forward replay in the backward).
 Every case is checked twice: against the oracle to the usual per-tensor bar,
 and against the one-pass path on the same inputs.  What the windows cannot
 change must not change at all: routing, the plan, dZ and dW_r are compared
-bitwise, and with a single window every output is.  With several windows Y,
-dX and the routed weight gradients differ from the one-pass results only by
-fp32 summation order.
+bitwise, and with a single window every output is (but Y and dX when every
+token routes to every expert: the one-pass path then folds the combines into
+its GEMMs).  With several windows Y, dX and the routed weight gradients
+differ from the one-pass results only by summation order.
 """
 import numpy as np
 import pytest
@@ -43,11 +44,21 @@ def run_pair(w, ring_rows, seed):
 
 def compare_to_one_pass(full, ring, w, ring_rows):
     one_window = ring_rows >= w.T * w.k
+    # with dense routing (k == E) the one-pass path folds the combine into
+    # the down product and the reverse combine into the dX product: Y and dX
+    # then differ from the ring's by rounding order, whatever the windows
+    dense = w.k == w.E
     names = EXACT + SUMMED + (SHARED if w.f_s else ())
     for n in names:
         a, b = getattr(full, n), getattr(ring, n)
-        if n in EXACT or n in SHARED or one_window:
+        if n in EXACT or n in SHARED or (one_window and not (dense and n in ("Y", "dX"))):
             assert torch.equal(a, b), f"{n} differs from the one-pass result"
+        elif dense and n in ("Y", "dX"):
+            # bf16 outputs rounded once on each side from fp32 sums of
+            # differently rounded terms (w * bf16 f_e(x) against bf16(w h)
+            # f_e's down product): a few elements land one bf16 step apart,
+            # up to 2^-7 of the largest value's binade
+            assert_close(f"{n} (ring vs one-pass)", to_np(b), to_np(a), rel=1.6e-2)
         else:
             assert_close(f"{n} (ring vs one-pass)", to_np(b), to_np(a), rel=4e-3)
     say("  exact: " + ", ".join(n for n in names if torch.equal(getattr(full, n), getattr(ring, n))))

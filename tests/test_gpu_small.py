@@ -26,13 +26,21 @@ def forward_parity(w, seed=0):
     fw = O.moe_forward(inp["X"], weights_dict(inp), idx_g, w_orc)
     R = w.T * w.k
     assert_close("Y", to_np(L.Y), fw["Y"])
-    assert_close("H", to_np(L.ws_tensor(B.WS_H, torch.bfloat16, (R, w.f))), fw["H"])
-    assert_close("Yexp", to_np(L.ws_tensor(B.WS_YEXP, torch.bfloat16, (R, w.d))), fw["Yexp"])
+    H = to_np(L.ws_tensor(B.WS_H, torch.bfloat16, (R, w.f)))
+    if w.k == w.E:
+        # dense routing: H holds w h (the combine is folded into the down
+        # product, so there is no Yexp and no Ysh)
+        perm = O.plan(idx_g, w.E)[2]
+        w_pos = w_orc.reshape(-1)[perm][:, None]
+        assert_close("w H", H, w_pos * fw["H"])
+    else:
+        assert_close("H", H, fw["H"])
+        assert_close("Yexp", to_np(L.ws_tensor(B.WS_YEXP, torch.bfloat16, (R, w.d))), fw["Yexp"])
+        if w.f_s:
+            assert_close("Ysh", to_np(L.ws_tensor(B.WS_YSH, torch.bfloat16, (w.T, w.d))), fw["Ysh"])
     if w.backward:
         assert_close("A", to_np(L.ws_tensor(B.WS_A, torch.bfloat16, (R, w.f))), fw["A"])
         assert_close("B", to_np(L.ws_tensor(B.WS_B, torch.bfloat16, (R, w.f))), fw["B"])
-    if w.f_s:
-        assert_close("Ysh", to_np(L.ws_tensor(B.WS_YSH, torch.bfloat16, (w.T, w.d))), fw["Ysh"])
     return L, inp, Zo, idx_g, w_orc
 
 
@@ -74,6 +82,12 @@ def test_ragged_forward_backward():
     Workload("sixteen_experts", T=333, d=768, E=16, k=5, f=256, f_s=256, bias_std=0.5,
              backward=True),
     Workload("eight_experts_wide", T=77, d=1280, E=8, k=2, f=256, bias_std=0.5, backward=True),
+    # dense routing (k == E) with a shared expert: the combines fold into the
+    # down and dX products; a partial token tile, several column tiles, a
+    # shared width that differs from the routed one, and one expert
+    Workload("dense_shared", T=555, d=768, E=6, k=6, f=256, f_s=512, bias_std=0.5, backward=True),
+    Workload("dense_one_expert", T=260, d=512, E=1, k=1, f=512, f_s=256, backward=True),
+    Workload("dense_sixteen", T=130, d=256, E=16, k=16, f=256, backward=True),
 ], ids=lambda w: w.name)
 def test_edge_shapes(w):
     L, inp, Zo, idx_g, w_orc = forward_parity(w, seed=2)
