@@ -26,7 +26,9 @@ struct Layout {
     size_t acc, coff;          // ring only: fp32 per-token accumulator, window regions
     size_t A, B, H, Yexp, As, Bs, Hs, Ysh;
     size_t fwd_total;
-    size_t dA, dB, Hw, dgpart, dg, dZ, dXperm, dAs, dBs, dXsh, dwr_part, dzs, wrs;
+    size_t dA, dB, Hw, dgpart, dg, dZ, dXperm, dAs, dBs, dXsh, dwr_part, dzs, wrs, xtt;
+    size_t dytt;
+    long xt_ld;
     size_t bwd_total;
     size_t xq, xs, hq, hsc;   // MXFP8 forward: quantised X and H (over the backward regions)
     size_t mx_total;
@@ -92,6 +94,9 @@ Layout make_layout(const moe_shape &s, long ring_rows = -1) {
     L.dwr_part = take((size_t)dwr_nchunks((long)T) * d * E * 4);
     L.dzs = take(T * 64 * 2);   // dense routing: router-term rows of dX
     L.wrs = take(d * 64 * 2);
+    L.xt_ld = (long)((T + 63) / 64 * 64);
+    L.xtt = take(s.k == s.E ? d * (size_t)L.xt_ld * 2 : 0);   // dense routing: X^T [d][xt_ld]
+    L.dytt = take(s.k == s.E ? d * (size_t)L.xt_ld * 2 : 0);  // dense routing: dY^T likewise
     L.bwd_total = o;
     o = L.fwd_total;
     L.xq = take(T * d);
@@ -323,6 +328,12 @@ hipError_t shared_down(const moe_shape &sh, const Layout &L, void *ws, const moe
     return launch_gemm_fwd_down(shared_down_args(sh, L, ws, w), sh.T, 1, s);
 }
 
+// Dense routing (k == E): every token routes to every local expert (see
+// down_cmb_args).  Expert e's plan rows are then the tokens in order, so in
+// any window that starts at position 0 (its regions start where the plan's
+// do) a gathered row is the position minus the region's start.
+bool dense_routing(const moe_shape &sh) { return sh.k == sh.E; }
+
 // Positions [w0, w1) of the routed buffer, with the expert regions clipped
 // to it.  Per-route activation rows live at row p - w0 of their region, so
 // kernels keep indexing by the global position p through a shifted base.
@@ -386,6 +397,7 @@ hipError_t routed_dgrad(const moe_shape &sh, const Layout &L, void *ws, const mo
     g.N = f; g.K = d; g.offsets = win.offs; g.E = (int)sh.E;
     g.E1 = win.rows<uint16_t>(ws, L.A, f); g.E2 = win.rows<uint16_t>(ws, L.B, f); g.ldc = f;
     g.rowscale = at<float>(ws, L.wperm);
+    g.a_local = win.w0 == 0 && dense_routing(sh) ? 1 : 0;   // dY row = position - offsets[e]
     g.C = win.rows<uint16_t>(ws, L.dA, f); g.C2 = win.rows<uint16_t>(ws, L.dB, f);
     g.C3 = win.rows<uint16_t>(ws, L.Hw, f);
     g.dgpart = at<float>(ws, L.dgpart); g.dg_ld = L.dg_parts;
@@ -418,14 +430,17 @@ GemmArgs wgrad_args(const moe_shape &sh, const Layout &L, void *ws, const moe_bf
     g.zeros = at<uint16_t>(ws, L.zeros);
     g.offsets = win.offs; g.E = (int)sh.E;
     g.accumulate = accumulate ? 1 : 0;
+    const bool dense_rows = dense_routing(sh) && win.w0 == 0;   // rows = tokens in order
     if (which < 2) {
         g.A = X; g.lda = d; g.a_rows = at<int>(ws, L.rowidx); g.a_nrows = T > 0 ? T : 1;
+        g.a_local = dense_rows ? 1 : 0;
         g.B = win.rows<uint16_t>(ws, which == 0 ? L.dA : L.dB, f); g.ldb = f; g.b_nrows = win.span();
         g.M = d; g.N = f;
         g.Cf = which == 0 ? gr->dW_gate : gr->dW_up; g.c_estride = (long)d * f; g.ldc = f;
     } else {
         g.A = win.rows<uint16_t>(ws, L.Hw, f); g.lda = f; g.a_nrows = win.span();
         g.B = dY; g.ldb = d; g.b_rows = at<int>(ws, L.rowidx); g.b_nrows = T > 0 ? T : 1;
+        g.b_local = dense_rows ? 1 : 0;
         g.M = f; g.N = d;
         g.Cf = gr->dW_down; g.c_estride = (long)f * d; g.ldc = d;
     }
@@ -460,8 +475,11 @@ hipError_t shared_dx(const moe_shape &sh, const Layout &L, void *ws, const moe_w
     return launch_gemm_bwd_dx(g, T, 1, s);
 }
 
+// xt, dyt: X^T and dY^T [d][L.xt_ld] when the caller made them (dense
+// routing): the products then read them K-contiguous.
 hipError_t shared_wgrads(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *dY,
-                         const moe_bf16 *X, const moe_grads *gr, hipStream_t s) {
+                         const moe_bf16 *X, const moe_grads *gr, hipStream_t s,
+                         const uint16_t *xt = nullptr, const uint16_t *dyt = nullptr) {
     const int T = (int)sh.T, d = (int)sh.d, fs = (int)sh.f_shared;
     const int Tn = T > 0 ? T : 1;
     hipError_t e;
@@ -472,9 +490,11 @@ hipError_t shared_wgrads(const moe_shape &sh, const Layout &L, void *ws, const m
         g.B = at<uint16_t>(ws, L.dAs); g.ldb = fs; g.b_nrows = Tn;
         g.M = d; g.N = fs; g.K = T;
         g.Cf = gr->dWg_s; g.ldc = fs;
-        if ((e = launch_gemm_wgrad(g, 1, s)) != hipSuccess) return e;
+        if (xt) { g.A = xt; g.lda = L.xt_ld; }
+        auto wg = [&]() { return xt ? launch_gemm_wgrad_t(g, 1, s) : launch_gemm_wgrad(g, 1, s); };
+        if ((e = wg()) != hipSuccess) return e;
         g.B = at<uint16_t>(ws, L.dBs); g.Cf = gr->dWu_s;
-        if ((e = launch_gemm_wgrad(g, 1, s)) != hipSuccess) return e;
+        if ((e = wg()) != hipSuccess) return e;
     }
     GemmArgs g;
     g.zeros = at<uint16_t>(ws, L.zeros);
@@ -482,6 +502,10 @@ hipError_t shared_wgrads(const moe_shape &sh, const Layout &L, void *ws, const m
     g.B = dY; g.ldb = d; g.b_nrows = Tn;
     g.M = fs; g.N = d; g.K = T;
     g.Cf = gr->dWd_s; g.ldc = d;
+    if (dyt) {
+        g.B = dyt; g.ldb = L.xt_ld;
+        return launch_gemm_wgrad_tb(g, 1, s);
+    }
     return launch_gemm_wgrad(g, 1, s);
 }
 
@@ -505,7 +529,6 @@ hipError_t shared_backward(const moe_shape &sh, const Layout &L, void *ws, const
 // product then writes Y directly from fp32, with no per-route output and no
 // combine pass; the dX product likewise writes dX with the shared expert's
 // and the router's terms.
-bool dense_routing(const moe_shape &sh) { return sh.k == sh.E; }
 
 // Y = sum_e (w h)_e W_down[e] + Hs Wd_s over K segments (H holds w h).
 GemmArgs down_cmb_args(const moe_shape &sh, const Layout &L, void *ws, const moe_weights *w,
@@ -814,6 +837,8 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
     float *dZ = grads->dZ ? grads->dZ : at<float>(ws, L.dZ);
     const StageMarks mk{events, s};
 
+    const bool shared = shape->f_shared > 0;
+
     MOE_TRY(mk.mark(0));
     MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, at<int>(ws, L.rowidx),
                         at<float>(ws, L.wperm), at<uint16_t>(ws, L.zeros), s));
@@ -826,20 +851,32 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
         // dX in one product over every expert, the shared expert and the
         // router term (stage 3, the routed dX, and stage 10, the reverse
         // combine, are empty; stage 7 is the whole dX)
-        const bool shared = shape->f_shared > 0;
         MOE_TRY(launch_router_split(dZ, W_r, T, d, E, at<uint16_t>(ws, L.dzs), at<uint16_t>(ws, L.wrs), s));
         MOE_TRY(mk.mark(3));
+        // X^T and dY^T once: the weight gradients of every expert (and of
+        // the shared expert) contract X and dY over the tokens in order, so
+        // they read them K-contiguous instead of as 14 KB-pitch column tiles
+        uint16_t *xt = at<uint16_t>(ws, L.xtt), *dyt = at<uint16_t>(ws, L.dytt);
+        MOE_TRY(launch_transpose_rows(X, T, d, xt, L.xt_ld, s));
+        MOE_TRY(launch_transpose_rows(dY, T, d, dyt, L.xt_ld, s));
         MOE_TRY(mk.mark(4));
-        MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, 0), E, s));
-        MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, 1), E, s));
+        for (int which = 0; which < 2; ++which) {
+            GemmArgs g = wgrad_args(*shape, L, ws, X, dY, grads, all, false, which);
+            g.A = xt; g.lda = L.xt_ld; g.a_rows = nullptr; g.a_local = 1;
+            MOE_TRY(launch_gemm_wgrad_t(g, E, s));
+        }
         MOE_TRY(mk.mark(5));
-        MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, 2), E, s));
+        {
+            GemmArgs g = wgrad_args(*shape, L, ws, X, dY, grads, all, false, 2);
+            g.B = dyt; g.ldb = L.xt_ld; g.b_rows = nullptr; g.b_local = 1;
+            MOE_TRY(launch_gemm_wgrad_tb(g, E, s));
+        }
         MOE_TRY(mk.mark(6));
         if (shared) MOE_TRY(shared_dgrad(*shape, L, ws, dY, weights, s));
         MOE_TRY(mk.mark(7));
         MOE_TRY(launch_gemm_bwd_dx_cmb(dx_cmb_args(*shape, L, ws, weights, plan->offsets, dX), s));
         MOE_TRY(mk.mark(8));
-        if (shared) MOE_TRY(shared_wgrads(*shape, L, ws, dY, X, grads, s));
+        if (shared) MOE_TRY(shared_wgrads(*shape, L, ws, dY, X, grads, s, xt, dyt));
         MOE_TRY(mk.mark(9));
         MOE_TRY(launch_dwr(X, dZ, T, d, E, at<float>(ws, L.dwr_part), grads->dW_r, s));
         MOE_TRY(mk.mark(10));
@@ -854,7 +891,6 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
     MOE_TRY(mk.mark(5));
     MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, 2), E, s));
     MOE_TRY(mk.mark(6));
-    const bool shared = shape->f_shared > 0;
     if (shared) {
         MOE_TRY(shared_backward(*shape, L, ws, dY, X, weights, grads, mk, s));
     } else {

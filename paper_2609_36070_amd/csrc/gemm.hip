@@ -72,16 +72,17 @@ constexpr int LOADS_PER_K = 2 * LD_PER_OP; // direct-load instructions per threa
 static_assert(WN == 64 || WN == 128, "gate/up column pairs and the epilogue need 64- or 128-column wave tiles");
 
 enum Mode { FWD_UP = 0, FWD_DOWN = 1, BWD_DGRAD = 2, BWD_DX = 3, WGRAD = 4, FWD_DOWN_CMB = 5,
-            BWD_DX_CMB = 6 };
+            BWD_DX_CMB = 6, WGRAD_T = 7, WGRAD_TB = 8 };
 
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 
 template <int MODE>
 struct Traits {
-    static constexpr bool A_COL = (MODE == WGRAD);                       // A stored [K][M]
+    static constexpr bool A_COL = (MODE == WGRAD || MODE == WGRAD_TB);   // A stored [K][M]
     static constexpr bool B_COL = (MODE == FWD_UP || MODE == FWD_DOWN || MODE == WGRAD ||
-                                   MODE == FWD_DOWN_CMB);
-    static constexpr bool GROUPED_ROWS = (MODE != WGRAD);
+                                   MODE == FWD_DOWN_CMB || MODE == WGRAD_T);
+    static constexpr bool WG = (MODE == WGRAD || MODE == WGRAD_T || MODE == WGRAD_TB);  // K = tokens
+    static constexpr bool GROUPED_ROWS = !WG;
     static constexpr bool CMB = (MODE == FWD_DOWN_CMB || MODE == BWD_DX_CMB);   // K segments
 };
 
@@ -315,6 +316,16 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
     // token / output row of each load, its chunk, and (B col tiles) its column
     uint32_t cm_t[LD_PER_OP], cm_c[LD_PER_OP], cm_b[LD_PER_OP];   // filled once col_of exists
     if constexpr (Tr::CMB) {
+    } else if constexpr (MODE == WGRAD_T) {
+        // A^T rows m0 + r; its columns are the expert's positions (from
+        // kbeg), or with a_local the tokens (from 0)
+        const long acol0 = g.a_local ? 0 : kbeg;
+#pragma unroll
+        for (int i = 0; i < LD_PER_OP; ++i) {
+            const int r = ROWS_PER_LD * (LD_PER_OP * wave + i) + lane / (BK / 8);
+            const int c = row_swz(r, lane % (BK / 8));
+            a_row[i] = g.A + (long)(m0 + r) * g.lda + acol0 + 8 * c;
+        }
     } else if constexpr (!Tr::A_COL) {
 #pragma unroll
         for (int i = 0; i < LD_PER_OP; ++i) {
@@ -322,7 +333,7 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
             const int c = row_swz(r, lane % (BK / 8));
             // rows past the region's end load its last row; their results are never stored
             const int p = min(row0 + r, row_end - 1);
-            int phys = a_rows ? a_rows[p] : p;
+            int phys = g.a_local ? p - uniform(g.offsets[e]) : a_rows ? a_rows[p] : p;
             phys = min(max(phys, 0), g.a_nrows - 1);
             a_row[i] = g.A + (long)phys * g.lda + 8 * c;
             if (MODE == BWD_DX) a2_row[i] = g.A2 + (long)phys * g.lda + 8 * c;
@@ -332,6 +343,16 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
     }
     if constexpr (Tr::CMB) {
         // set above
+    } else if constexpr (MODE == WGRAD_TB) {
+        // B^T rows n0 + r; its columns are the expert's positions (from
+        // kbeg), or with b_local the tokens (from 0)
+        const long bcol0 = g.b_local ? 0 : kbeg;
+#pragma unroll
+        for (int i = 0; i < LD_PER_OP; ++i) {
+            const int r = ROWS_PER_LD * (LD_PER_OP * wave + i) + lane / (BK / 8);
+            const int c = row_swz(r, lane % (BK / 8));
+            b_row[i] = g.B + (long)(n0 + r) * g.ldb + bcol0 + 8 * c;
+        }
     } else if constexpr (!Tr::B_COL) {
 #pragma unroll
         for (int i = 0; i < LD_PER_OP; ++i) {
@@ -466,28 +487,29 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
             return;
         }
         int pa[LD_PER_OP], pb[LD_PER_OP];
-        if constexpr (MODE == WGRAD) {
+        if constexpr (Tr::WG) {
             int ia[2 * LD_PER_OP], ib[2 * LD_PER_OP];
             // this wave's k rows are the 2 LD_PER_OP consecutive positions from r0
             const int r0 = kt * BK + 2 * LD_PER_OP * wave;
             if (kt * BK + BK <= klen) {
                 // the whole step lies in the expert's range: one scalar load per operand
                 static_assert(LD_PER_OP % 2 == 0, "4-index scalar loads");
+                const int abase = g.a_local ? 0 : kbeg, bbase = g.b_local ? 0 : kbeg;
 #pragma unroll
                 for (int q = 0; q < 2 * LD_PER_OP; q += 4) {
-                    if (a_rows) {
+                    if (a_rows && !g.a_local) {
                         const idx4_t v = *reinterpret_cast<const idx4_t *>(a_rows + kbeg + r0 + q);
                         ia[q] = v[0]; ia[q + 1] = v[1]; ia[q + 2] = v[2]; ia[q + 3] = v[3];
                     } else {
 #pragma unroll
-                        for (int u = 0; u < 4; ++u) ia[q + u] = kbeg + r0 + q + u;
+                        for (int u = 0; u < 4; ++u) ia[q + u] = abase + r0 + q + u;
                     }
-                    if (b_rows) {
+                    if (b_rows && !g.b_local) {
                         const idx4_t v = *reinterpret_cast<const idx4_t *>(b_rows + kbeg + r0 + q);
                         ib[q] = v[0]; ib[q + 1] = v[1]; ib[q + 2] = v[2]; ib[q + 3] = v[3];
                     } else {
 #pragma unroll
-                        for (int u = 0; u < 4; ++u) ib[q + u] = kbeg + r0 + q + u;
+                        for (int u = 0; u < 4; ++u) ib[q + u] = bbase + r0 + q + u;
                     }
                 }
             } else {
@@ -496,8 +518,8 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
 #pragma unroll
                 for (int q = 0; q < 2 * LD_PER_OP; ++q) {
                     const int p = kbeg + min(r0 + q, klen - 1);
-                    ia[q] = a_rows ? a_rows[p] : p;
-                    ib[q] = b_rows ? b_rows[p] : p;
+                    ia[q] = g.a_local ? p - kbeg : a_rows ? a_rows[p] : p;
+                    ib[q] = g.b_local ? p - kbeg : b_rows ? b_rows[p] : p;
                 }
             }
 #pragma unroll
@@ -538,7 +560,7 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
                 const int kk = kt * BK + kr;
                 const int col = col_of(kr);
                 const uint16_t *src;
-                if constexpr (MODE == WGRAD) {
+                if constexpr (Tr::WG) {
                     src = kk < klen ? b_col_base + (long)pb[i] * ldb + b_col_off + col
                                     : g.zeros + col;
                 } else {
@@ -769,7 +791,7 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
                 g.dgpart[(long)p * g.dg_ld + ntile] = sum;
             }
         }
-    } else {  // WGRAD
+    } else {  // WGRAD, WGRAD_T, WGRAD_TB
         // accumulator q of MFMA tile (i, j) is row 8 (q >> 2) + 4 lhalf + (q & 3)
         // of the 32-row block, column lrow
         float *out = g.Cf + (long)e * g.c_estride + (long)(m0 + wm * WM + 4 * lhalf) * g.ldc
@@ -882,6 +904,14 @@ hipError_t launch_gemm_fwd_down_cmb(const GemmArgs &g, hipStream_t st) {
 hipError_t launch_gemm_bwd_dx_cmb(const GemmArgs &g, hipStream_t st) {
     if (g.offsets) return hipErrorInvalidValue;
     return launch_mode<BWD_DX_CMB>(g, (g.M + BM - 1) / BM, g.N / BN, st);
+}
+hipError_t launch_gemm_wgrad_tb(const GemmArgs &g, int groups, hipStream_t st) {
+    return launch_mode<WGRAD_TB>(g, groups * (g.M / BM), g.N / BN, st,
+                                 wgrad_grid(groups, g.M / BM, g.N / BN));
+}
+hipError_t launch_gemm_wgrad_t(const GemmArgs &g, int groups, hipStream_t st) {
+    return launch_mode<WGRAD_T>(g, groups * (g.M / BM), g.N / BN, st,
+                                wgrad_grid(groups, g.M / BM, g.N / BN));
 }
 hipError_t launch_gemm_wgrad(const GemmArgs &g, int groups, hipStream_t st) {
     return launch_mode<WGRAD>(g, groups * (g.M / BM), g.N / BN, st,

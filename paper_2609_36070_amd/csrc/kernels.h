@@ -63,6 +63,11 @@ struct GemmArgs {
     const int *dep2 = nullptr;
     int dep_need2 = 0;
     int dep_slots = 0;                 // counters in dep (per-expert indices are clamped to it)
+    // Dense routing: expert e's plan rows are all tokens in order, so a
+    // gathered operand's row is the position minus offsets[e] (no index
+    // loads); a_local for A (rows of a row product, k rows of WGRAD), b_local
+    // for WGRAD's B.  The gather pointers are then ignored.
+    int a_local = 0, b_local = 0;
 };
 
 int gemm_tile_m();
@@ -72,6 +77,17 @@ hipError_t launch_gemm_fwd_down(const GemmArgs &g, long rows, int groups, hipStr
 hipError_t launch_gemm_bwd_dgrad(const GemmArgs &g, long rows, int groups, hipStream_t st);
 hipError_t launch_gemm_bwd_dx(const GemmArgs &g, long rows, int groups, hipStream_t st);
 hipError_t launch_gemm_wgrad(const GemmArgs &g, int groups, hipStream_t st);
+// The weight gradient with A given transposed: A [M][lda] row-major with its
+// columns the expert's positions (from offsets[e]; with a_local the tokens,
+// from 0), K-contiguous like the row products' operands; B as for WGRAD.  A's
+// columns past an expert's last row must hold finite values (a padded pitch).
+hipError_t launch_gemm_wgrad_t(const GemmArgs &g, int groups, hipStream_t st);
+// ... and with B given transposed instead: B [N][ldb], columns as A's above.
+hipError_t launch_gemm_wgrad_tb(const GemmArgs &g, int groups, hipStream_t st);
+// X [T][d] -> XT [d][ldt] (ldt >= T rounded up to 64; columns T .. ldt-1 zero),
+// for `batch` matrices stored one after the other on both sides.
+hipError_t launch_transpose_rows(const uint16_t *X, int T, int d, uint16_t *XT, long ldt,
+                                 hipStream_t st, int batch = 1);
 // Dense routing (k == E): Y = sum over experts of (w h) W_down[e], plus the
 // shared expert, over one token tile's K segments (the combine folded into the
 // down product); dX likewise with dA W_gate^T + dB W_up^T per expert, the

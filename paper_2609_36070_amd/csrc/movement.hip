@@ -521,6 +521,39 @@ __global__ __launch_bounds__(256) void dwr_reduce_kernel(const float *__restrict
 
 inline unsigned rows_grid(long rows) { return (unsigned)(rows < 16384 ? (rows > 0 ? rows : 1) : 16384); }
 
+// Transpose of a [T][d] bf16 matrix into [d][ldt] through 64 x 64 LDS tiles;
+// columns T .. ldt - 1 of the result are written as zeros.  Grid (ldt / 64,
+// d / 64); each thread moves two 16-byte chunks each way.
+__global__ __launch_bounds__(256) void transpose_rows_kernel(const uint16_t *__restrict__ X, int T,
+                                                             int d, uint16_t *__restrict__ XT,
+                                                             long ldt) {
+    __shared__ uint16_t tile[64][64 + 8];
+    const int t0 = blockIdx.x * 64, c0 = blockIdx.y * 64, tid = threadIdx.x;
+    X += (long)blockIdx.z * T * d;       // matrix z of a batch
+    XT += (long)blockIdx.z * d * ldt;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int ch = h * 256 + tid, r = ch >> 3, c = 8 * (ch & 7);   // row t0 + r, columns c0 + c ..
+        u32x4_t v = u32x4_t{0, 0, 0, 0};
+        if (t0 + r < T) v = ld_u32x4(X + (long)(t0 + r) * d + c0 + c);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            tile[r][c + 2 * q] = (uint16_t)(v[q] & 0xffffu);
+            tile[r][c + 2 * q + 1] = (uint16_t)(v[q] >> 16);
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int ch = h * 256 + tid, r = ch >> 3, c = 8 * (ch & 7);   // XT row c0 + r, columns t0 + c ..
+        u32x4_t v;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            v[q] = (uint32_t)tile[c + 2 * q][r] | ((uint32_t)tile[c + 2 * q + 1][r] << 16);
+        st_u32x4(XT + (long)(c0 + r) * ldt + t0 + c, v);
+    }
+}
+
 // Rows of 64 bf16 for the router term of the dense dX product: row t < T
 // holds the high and low bf16 parts of dZ[t][e] (hi = RNE(v), lo = RNE(v - hi),
 // so hi + lo carries about 16 significant bits) in columns e and 32 + e; row
@@ -655,5 +688,14 @@ hipError_t launch_router_split(const float *dZ, const uint16_t *W_r, int T, int 
     if (n <= 0) return hipSuccess;
     router_split_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st>>>(dZ, W_r, T, d, E,
                                                                                   dz_split, wr_split);
+    return hipGetLastError();
+}
+
+hipError_t launch_transpose_rows(const uint16_t *X, int T, int d, uint16_t *XT, long ldt,
+                                 hipStream_t st, int batch) {
+    if (ldt % 64 || ldt < T || d % 64 || batch < 1) return hipErrorInvalidValue;
+    if (ldt == 0 || d == 0) return hipSuccess;
+    transpose_rows_kernel<<<dim3((unsigned)(ldt / 64), (unsigned)(d / 64), (unsigned)batch), dim3(256), 0,
+                            st>>>(X, T, d, XT, ldt);
     return hipGetLastError();
 }
