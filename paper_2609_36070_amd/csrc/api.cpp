@@ -447,6 +447,39 @@ GemmArgs wgrad_args(const moe_shape &sh, const Layout &L, void *ws, const moe_bf
     return g;
 }
 
+// Dense routing: X^T and dY^T ([d][xt_ld], zero-padded), made once per
+// backward.  The weight gradients of every expert (and of the shared expert)
+// contract X and dY over the tokens in order, so they read them as
+// K-contiguous rows instead of column tiles of 2d-byte rows.
+hipError_t dense_transposes(const moe_shape &sh, const Layout &L, const moe_bf16 *X,
+                            const moe_bf16 *dY, uint16_t *xt, uint16_t *dyt, hipStream_t s) {
+    hipError_t e = launch_transpose_rows(X, (int)sh.T, (int)sh.d, xt, L.xt_ld, s);
+    if (e != hipSuccess) return e;
+    return launch_transpose_rows(dY, (int)sh.T, (int)sh.d, dyt, L.xt_ld, s);
+}
+
+// Routed weight gradients which0 .. which1 - 1 (0 dW_gate, 1 dW_up, 2 dW_down)
+// of a one-pass backward with dense routing, on X^T / dY^T.
+hipError_t dense_wgrads(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *X,
+                        const moe_bf16 *dY, const moe_grads *gr, const int *offsets,
+                        const uint16_t *xt, const uint16_t *dyt, int which0, int which1,
+                        hipStream_t s) {
+    const Window all{offsets, 0, (int)(sh.T * sh.k)};
+    for (int which = which0; which < which1; ++which) {
+        GemmArgs g = wgrad_args(sh, L, ws, X, dY, gr, all, false, which);
+        hipError_t e;
+        if (which < 2) {
+            g.A = xt; g.lda = L.xt_ld; g.a_rows = nullptr; g.a_local = 1;
+            e = launch_gemm_wgrad_t(g, (int)sh.E, s);
+        } else {
+            g.B = dyt; g.ldb = L.xt_ld; g.b_rows = nullptr; g.b_local = 1;
+            e = launch_gemm_wgrad_tb(g, (int)sh.E, s);
+        }
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 // Shared-expert backward, in three parts: dAs/dBs (the gated-activation
 // backward on the saved As, Bs), dXsh, and the three weight gradients.
 hipError_t shared_dgrad(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *dY,
@@ -853,24 +886,12 @@ moe_status moe_backward(const moe_shape *shape, const moe_bf16 *dY, const moe_bf
         // combine, are empty; stage 7 is the whole dX)
         MOE_TRY(launch_router_split(dZ, W_r, T, d, E, at<uint16_t>(ws, L.dzs), at<uint16_t>(ws, L.wrs), s));
         MOE_TRY(mk.mark(3));
-        // X^T and dY^T once: the weight gradients of every expert (and of
-        // the shared expert) contract X and dY over the tokens in order, so
-        // they read them K-contiguous instead of as 14 KB-pitch column tiles
         uint16_t *xt = at<uint16_t>(ws, L.xtt), *dyt = at<uint16_t>(ws, L.dytt);
-        MOE_TRY(launch_transpose_rows(X, T, d, xt, L.xt_ld, s));
-        MOE_TRY(launch_transpose_rows(dY, T, d, dyt, L.xt_ld, s));
+        MOE_TRY(dense_transposes(*shape, L, X, dY, xt, dyt, s));
         MOE_TRY(mk.mark(4));
-        for (int which = 0; which < 2; ++which) {
-            GemmArgs g = wgrad_args(*shape, L, ws, X, dY, grads, all, false, which);
-            g.A = xt; g.lda = L.xt_ld; g.a_rows = nullptr; g.a_local = 1;
-            MOE_TRY(launch_gemm_wgrad_t(g, E, s));
-        }
+        MOE_TRY(dense_wgrads(*shape, L, ws, X, dY, grads, plan->offsets, xt, dyt, 0, 2, s));
         MOE_TRY(mk.mark(5));
-        {
-            GemmArgs g = wgrad_args(*shape, L, ws, X, dY, grads, all, false, 2);
-            g.B = dyt; g.ldb = L.xt_ld; g.b_rows = nullptr; g.b_local = 1;
-            MOE_TRY(launch_gemm_wgrad_tb(g, E, s));
-        }
+        MOE_TRY(dense_wgrads(*shape, L, ws, X, dY, grads, plan->offsets, xt, dyt, 2, 3, s));
         MOE_TRY(mk.mark(6));
         if (shared) MOE_TRY(shared_dgrad(*shape, L, ws, dY, weights, s));
         MOE_TRY(mk.mark(7));
@@ -1272,12 +1293,24 @@ moe_status moe_backward_mx(const moe_shape *shape, const moe_bf16 *dY, const moe
         MOE_TRY(wg(L.xt, L.xts, d, L.dat, L.dats, f, grads->dW_gate));
         MOE_TRY(wg(L.xt, L.xts, d, L.dbt, L.dbts, f, grads->dW_up));
         MOE_TRY(wg(L.hwt, L.hwts, f, L.dyt, L.dyts, d, grads->dW_down));
+    } else if (dense_routing(*shape)) {
+        // weight gradients in BF16 on the unquantised operands, X and dY
+        // read transposed (dense routing; see dense_transposes)
+        uint16_t *xt = at<uint16_t>(ws, L.xtt), *dyt = at<uint16_t>(ws, L.dytt);
+        MOE_TRY(dense_transposes(*shape, L, X, dY, xt, dyt, s));
+        MOE_TRY(dense_wgrads(*shape, L, ws, X, dY, grads, plan->offsets, xt, dyt, 0, 3, s));
+        if (shared) {
+            MOE_TRY(shared_dgrad(*shape, L, ws, dY, weights, s));
+            MOE_TRY(shared_dx(*shape, L, ws, weights, s));
+            MOE_TRY(shared_wgrads(*shape, L, ws, dY, X, grads, s, xt, dyt));
+        }
     } else {
         // weight gradients in BF16 on the unquantised operands
         for (int i = 0; i < 3; ++i)
             MOE_TRY(launch_gemm_wgrad(wgrad_args(*shape, L, ws, X, dY, grads, all, false, i), E, s));
     }
-    if (shared) MOE_TRY(shared_backward(*shape, L, ws, dY, X, weights, grads, StageMarks{nullptr, s}, s));
+    if (shared && (wgrad_mxfp8 || !dense_routing(*shape)))
+        MOE_TRY(shared_backward(*shape, L, ws, dY, X, weights, grads, StageMarks{nullptr, s}, s));
     MOE_TRY(launch_dwr(X, dZ, T, d, E, at<float>(ws, L.dwr_part), grads->dW_r, s));
     MOE_TRY(launch_reverse_combine(at<uint16_t>(ws, L.dXperm), shared ? at<uint16_t>(ws, L.dXsh) : nullptr,
                                    dZ, W_r, plan->route_pos, T, d, k, E, nullptr, dX, s));
