@@ -2,11 +2,12 @@
 // renormalised softmax weights (§2.1: a router projection selects the top-k
 // routed experts and assigns each a router weight).
 //
-// Layout: 16 tokens per block, 4 waves.  The d axis is cut into 64-wide
-// chunks dealt round-robin to the waves (split-K); each wave accumulates
-// 16 x EPAD partial logits with v_mfma_f32_16x16x32_bf16 reading X rows
-// straight from HBM and the transposed router W_r^T from L2.  The four
-// partial sums are added in wave order, so the result is deterministic.
+// Layout: 16 tokens per block, NW waves (8, or 4 when 256 experts make the
+// partial sums large).  The d axis is cut into 64-wide chunks dealt
+// round-robin to the waves (split-K); each wave accumulates 16 x EPAD partial
+// logits with v_mfma_f32_16x16x32_bf16 reading X rows straight from HBM and
+// the transposed router W_r^T from L2.  The partial sums are added in wave
+// order, so the result is deterministic.
 #include "common.h"
 #include "kernels.h"
 
@@ -22,8 +23,8 @@ __global__ __launch_bounds__(256) void wr_transpose_kernel(const uint16_t *__res
     WrT[i] = e < E ? Wr[(long)kk * E + e] : (uint16_t)0;
 }
 
-template <int EPAD>
-__global__ __launch_bounds__(256) void route_kernel(const uint16_t *__restrict__ X,
+template <int EPAD, int NW, int MT>
+__global__ __launch_bounds__(64 * NW) void route_kernel(const uint16_t *__restrict__ X,
                                                     const uint16_t *__restrict__ WrT,
                                                     const float *__restrict__ bias,
                                                     float *__restrict__ logits,
@@ -32,35 +33,43 @@ __global__ __launch_bounds__(256) void route_kernel(const uint16_t *__restrict__
                                                     int T, int d, int E, int k) {
     constexpr int NT = EPAD / 16;
     constexpr int PER = (EPAD + 63) / 64;
-    __shared__ float red[4][16][EPAD + 1];
-    __shared__ float zs[16][EPAD + 1];
+    constexpr int BT = 16 * MT;             // tokens per block
+    constexpr int TPW = BT / NW;            // tokens per wave in the top-k
+    __shared__ float red[NW][BT][EPAD + 1];
+    __shared__ float zs[BT][EPAD + 1];
 
     const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
     const int g = l >> 4, r = l & 15;
-    const int t0 = blockIdx.x * 16;
-    const int tok = t0 + r;
-    const bool tok_ok = tok < T;
-    const uint16_t *xrow = X + (long)(tok_ok ? tok : 0) * d;
+    const int t0 = blockIdx.x * BT;
 
-    f32x4_t acc[NT];
+    f32x4_t acc[MT][NT];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     // CU chunks per pass: all their loads first, then the MFMAs in chunk
-    // order (so the sums are those of one chunk at a time)
-    constexpr int CU = NT <= 2 ? 4 : NT <= 4 ? 2 : 1;
+    // order (so the sums are those of one chunk at a time).  Each W_r^T
+    // fragment serves the MT token tiles of the wave.
+    constexpr int CU = 24 / (2 * MT + 2 * NT) < 1 ? 1 : 24 / (2 * MT + 2 * NT) > 4 ? 4
+                                                     : 24 / (2 * MT + 2 * NT);
     const int nchunks = d / 64;
-    for (int c0 = w; c0 < nchunks; c0 += 4 * CU) {
-        u32x4_t a0[CU], a1[CU], b0[CU][NT], b1[CU][NT];
+    for (int c0 = w; c0 < nchunks; c0 += NW * CU) {
+        u32x4_t a0[CU][MT], a1[CU][MT], b0[CU][NT], b1[CU][NT];
 #pragma unroll
         for (int u = 0; u < CU; ++u) {
-            const int c = c0 + 4 * u;
+            const int c = c0 + NW * u;
             const int kb = min(c, nchunks - 1) * 64 + 16 * g;
-            a0[u] = u32x4_t{0, 0, 0, 0};
-            a1[u] = u32x4_t{0, 0, 0, 0};
-            if (tok_ok && c < nchunks) {
-                a0[u] = ld_u32x4(xrow + kb);
-                a1[u] = ld_u32x4(xrow + kb + 8);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const int tok = t0 + 16 * mt + r;
+                a0[u][mt] = u32x4_t{0, 0, 0, 0};
+                a1[u][mt] = u32x4_t{0, 0, 0, 0};
+                if (tok < T && c < nchunks) {
+                    const uint16_t *xrow = X + (long)tok * d + kb;
+                    a0[u][mt] = ld_u32x4(xrow);
+                    a1[u][mt] = ld_u32x4(xrow + 8);
+                }
             }
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
@@ -71,31 +80,35 @@ __global__ __launch_bounds__(256) void route_kernel(const uint16_t *__restrict__
         }
 #pragma unroll
         for (int u = 0; u < CU; ++u) {
-            if (c0 + 4 * u < nchunks) {
+            if (c0 + NW * u < nchunks) {
 #pragma unroll
-                for (int nt = 0; nt < NT; ++nt) {
-                    acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(bf16x8_t, a0[u]), __builtin_bit_cast(bf16x8_t, b0[u][nt]),
-                        acc[nt], 0, 0, 0);
-                    acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(bf16x8_t, a1[u]), __builtin_bit_cast(bf16x8_t, b1[u][nt]),
-                        acc[nt], 0, 0, 0);
-                }
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) {
+                        acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            __builtin_bit_cast(bf16x8_t, a0[u][mt]),
+                            __builtin_bit_cast(bf16x8_t, b0[u][nt]), acc[mt][nt], 0, 0, 0);
+                        acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            __builtin_bit_cast(bf16x8_t, a1[u][mt]),
+                            __builtin_bit_cast(bf16x8_t, b1[u][nt]), acc[mt][nt], 0, 0, 0);
+                    }
             }
         }
     }
     // 16x16 accumulator layout: lane (g, r) register q holds row 4g+q, column r.
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) red[w][4 * g + q][16 * nt + r] = acc[nt][q];
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) red[w][16 * mt + 4 * g + q][16 * nt + r] = acc[mt][nt][q];
     __syncthreads();
 
-    for (int i = threadIdx.x; i < 16 * EPAD; i += 256) {
+    for (int i = threadIdx.x; i < BT * EPAD; i += 64 * NW) {
         const int tt = i / EPAD, e = i % EPAD;
         float z = red[0][tt][e] + red[1][tt][e];
-        z = z + red[2][tt][e];
-        z = z + red[3][tt][e];
+#pragma unroll
+        for (int v = 2; v < NW; ++v) z = z + red[v][tt][e];
         if (e < E) {
             if (bias) z = z + bias[e];
             if (t0 + tt < T) logits[(long)(t0 + tt) * E + e] = z;
@@ -104,69 +117,91 @@ __global__ __launch_bounds__(256) void route_kernel(const uint16_t *__restrict__
     }
     __syncthreads();
 
-    // top-k: wave w selects for tokens 4w .. 4w+3.
-    for (int q = 0; q < 4; ++q) {
-        const int tt = 4 * w + q, t = t0 + tt;
-        if (t >= T) break;
+    // top-k: wave w selects for tokens TPW w .. TPW w + TPW - 1 (rows past
+    // the batch hold finite logits too and are computed, not stored); lane
+    // l holds experts
+    // l + 64 m.  Each logit maps to an unsigned key with the same order (-0
+    // and +0 share one key; a NaN ranks as -inf; padding entries get key 0,
+    // below every logit), so that the k-th largest key and the largest key
+    // fall out of a bitwise radix search whose counts are ballots: every
+    // step is wave-uniform and no lane exchanges values.  The kept set is
+    // every key above the k-th largest plus, among keys equal to it, the
+    // lowest ids up to k (ties go to the lower expert id).  Each lane writes
+    // its own kept experts at their rank among the kept ids, so the ids come
+    // out ascending; the weights are exp(z - zmax) over their sum taken in
+    // ascending id order.
+    const unsigned long long lt = (l == 0) ? 0ull : (~0ull >> (64 - l));
+#pragma unroll
+    for (int q = 0; q < TPW; ++q) {
+        const int tt = TPW * w + q, t = t0 + tt;
         float v[PER];
+        uint32_t key[PER];
+        uint32_t lane_max = 0;
 #pragma unroll
         for (int m = 0; m < PER; ++m) {
             const int e = l + 64 * m;
-            v[m] = e < E ? zs[tt][e] : -INFINITY;
+            float z = e < E ? zs[tt][e] : -INFINITY;
+            z = z == z ? z : -INFINITY;
+            z = z == 0.f ? 0.f : z;
+            v[m] = z;
+            const uint32_t u = __float_as_uint(z);
+            key[m] = e < E ? ((u & 0x80000000u) ? ~u : (u | 0x80000000u)) : 0u;
+            lane_max = max(lane_max, key[m]);
         }
-        uint32_t taken = 0;
-        int sel[16];
-        float selz[16];
+        uint32_t kth = 0, top = 0;
 #pragma unroll
-        for (int s = 0; s < 16; ++s) {
-            sel[s] = 0x7fffffff;
-            selz[s] = 0.f;
-            if (s < k) {
-                float bv = -INFINITY;
-                int bi = 0x7fffffff;
+        for (int b = 31; b >= 0; --b) {
+            const uint32_t ck = kth | (1u << b), ct = top | (1u << b);
+            int n = 0;
 #pragma unroll
-                for (int m = 0; m < PER; ++m) {
-                    const int e = l + 64 * m;
-                    if (e < E && !((taken >> m) & 1u)) {
-                        if (v[m] > bv || (v[m] == bv && e < bi)) { bv = v[m]; bi = e; }
-                    }
+            for (int m = 0; m < PER; ++m) n += __popcll(__ballot(key[m] >= ck));
+            if (n >= k) kth = ck;
+            if (__ballot(lane_max >= ct)) top = ct;
+        }
+        unsigned long long sel[PER];
+        int need = k;
+#pragma unroll
+        for (int m = 0; m < PER; ++m) {
+            sel[m] = __ballot(key[m] > kth);
+            need -= __popcll(sel[m]);
+        }
+#pragma unroll
+        for (int m = 0; m < PER; ++m) {
+            unsigned long long eq = __ballot(key[m] == kth);
+            const int c = __popcll(eq);
+            if (c <= need) {
+                sel[m] |= eq;
+                need -= c;
+            } else {
+                for (; need > 0; --need) {
+                    sel[m] |= eq & (~eq + 1);
+                    eq &= eq - 1;
                 }
-#pragma unroll
-                for (int off = 32; off >= 1; off >>= 1) {
-                    const float ov = shfl_xor_f(bv, off);
-                    const int oi = shfl_xor_i(bi, off);
-                    if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
-                }
-                sel[s] = bi;
-                selz[s] = bv;
-                if ((bi & 63) == l) taken |= 1u << (bi >> 6);
             }
         }
-        const float zmax = selz[0];
-        // ascending expert order (entries past k hold INT_MAX and stay last)
+        const uint32_t ut = (top & 0x80000000u) ? (top ^ 0x80000000u) : ~top;
+        const float zmax = __uint_as_float(ut);
+        float ex[PER];
 #pragma unroll
-        for (int a = 0; a < 15; ++a)
-#pragma unroll
-            for (int b = 0; b < 15 - a; ++b)
-                if (sel[b] > sel[b + 1]) {
-                    int ti = sel[b]; sel[b] = sel[b + 1]; sel[b + 1] = ti;
-                    float tz = selz[b]; selz[b] = selz[b + 1]; selz[b + 1] = tz;
-                }
-        float ex[16];
+        for (int m = 0; m < PER; ++m) ex[m] = expf(v[m] - zmax);
         float sum = 0.f;
 #pragma unroll
-        for (int s = 0; s < 16; ++s) {
-            ex[s] = s < k ? expf(selz[s] - zmax) : 0.f;
-            sum = sum + ex[s];
+        for (int m = 0; m < PER; ++m) {
+            for (unsigned long long s = sel[m]; s; s &= s - 1) {
+                const int src = __builtin_ctzll(s);
+                sum = sum + __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ex[m]), src));
+            }
         }
         const float inv = 1.0f / sum;
-        if (l == 0) {
+        int before = 0;   // kept ids in lower blocks of 64
 #pragma unroll
-            for (int s = 0; s < 16; ++s)
-                if (s < k) {
-                    topk_idx[(long)t * k + s] = sel[s];
-                    topk_w[(long)t * k + s] = ex[s] * inv;
-                }
+        for (int m = 0; m < PER; ++m) {
+            if (t < T && ((sel[m] >> l) & 1ull)) {
+                const int rank = before + __popcll(sel[m] & lt);
+                topk_idx[(long)t * k + rank] = l + 64 * m;
+                topk_w[(long)t * k + rank] = ex[m] * inv;
+            }
+            before += __popcll(sel[m]);
         }
     }
 }
@@ -186,14 +221,31 @@ hipError_t launch_route(const uint16_t *X, const uint16_t *W_r, const float *bia
     const long n = (long)EPAD * d;
     wr_transpose_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st>>>(W_r, WrT, d, E, EPAD);
     if (T == 0) return hipGetLastError();
-    dim3 grid((unsigned)((T + 15) / 16)), block(256);
-    switch (EPAD) {
-        case 16: route_kernel<16><<<grid, block, 0, st>>>(X, WrT, bias, logits, topk_idx, topk_w, T, d, E, k); break;
-        case 32: route_kernel<32><<<grid, block, 0, st>>>(X, WrT, bias, logits, topk_idx, topk_w, T, d, E, k); break;
-        case 64: route_kernel<64><<<grid, block, 0, st>>>(X, WrT, bias, logits, topk_idx, topk_w, T, d, E, k); break;
-        case 128: route_kernel<128><<<grid, block, 0, st>>>(X, WrT, bias, logits, topk_idx, topk_w, T, d, E, k); break;
-        case 256: route_kernel<256><<<grid, block, 0, st>>>(X, WrT, bias, logits, topk_idx, topk_w, T, d, E, k); break;
+    // token tiles per wave: each W_r^T fragment a wave loads serves MT tiles
+    // of 16 tokens, as many as keep about one block per compute unit (the
+    // partial sums of 8 waves must fit the 160 KiB of LDS)
+    const int mt_max = EPAD <= 64 ? 4 : EPAD == 128 ? 2 : 1;
+    int mt = 1;
+    while (mt < mt_max && (T + 32 * mt - 1) / (32 * mt) >= 256) mt *= 2;
+    const dim3 b8(512), b4(256);
+    auto grid = [&](int m) { return dim3((unsigned)((T + 16 * m - 1) / (16 * m))); };
+#define ROUTE_LAUNCH(EP, NW, M) \
+    route_kernel<EP, NW, M><<<grid(M), NW == 8 ? b8 : b4, 0, st>>>(X, WrT, bias, logits, topk_idx, topk_w, T, d, E, k)
+    switch (EPAD * 8 + mt) {
+        case 16 * 8 + 1: ROUTE_LAUNCH(16, 8, 1); break;
+        case 16 * 8 + 2: ROUTE_LAUNCH(16, 8, 2); break;
+        case 16 * 8 + 4: ROUTE_LAUNCH(16, 8, 4); break;
+        case 32 * 8 + 1: ROUTE_LAUNCH(32, 8, 1); break;
+        case 32 * 8 + 2: ROUTE_LAUNCH(32, 8, 2); break;
+        case 32 * 8 + 4: ROUTE_LAUNCH(32, 8, 4); break;
+        case 64 * 8 + 1: ROUTE_LAUNCH(64, 8, 1); break;
+        case 64 * 8 + 2: ROUTE_LAUNCH(64, 8, 2); break;
+        case 64 * 8 + 4: ROUTE_LAUNCH(64, 8, 4); break;
+        case 128 * 8 + 1: ROUTE_LAUNCH(128, 8, 1); break;
+        case 128 * 8 + 2: ROUTE_LAUNCH(128, 8, 2); break;
+        case 256 * 8 + 1: ROUTE_LAUNCH(256, 4, 1); break;
         default: return hipErrorInvalidValue;
     }
+#undef ROUTE_LAUNCH
     return hipGetLastError();
 }

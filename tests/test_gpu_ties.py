@@ -133,3 +133,24 @@ def test_planted_ties_at_the_kth_slot(T, d, E, k):
     tied = int((srt[:, k - 1] == srt[:, k]).sum())
     say(f"  {tied} of {T} tokens have a tie across the k-th slot")
     assert tied >= T // 2, "the fixture must actually tie at the k-th slot"
+
+
+@pytest.mark.parametrize("T,d,E,k", [(16461, 256, 32, 8), (8197, 256, 128, 8), (16400, 256, 64, 6)])
+def test_planted_ties_large_batches(T, d, E, k):
+    """Batches large enough that each wave of the router serves two or four
+    16-token tiles per W_r fragment, with a ragged last block."""
+    X, W_r, bias = planted_ties(T, d, E, k, seed=T)
+    say(f"[gpu] planted ties, large batch T={T} d={d} E={E} k={k}")
+    Zo, _, _ = check_exact(X, W_r, bias, k)
+    srt = -np.sort(-Zo, axis=1)
+    assert int((srt[:, k - 1] == srt[:, k]).sum()) >= T // 2
+
+
+def test_every_expert_kept_large_batch():
+    """k == E on a large ragged batch: every token keeps every expert, in id
+    order, with the softmax weights of all its logits."""
+    T, d, E = 16390, 256, 8
+    X, W_r, bias = planted_ties(T, d, E, E, seed=5)
+    say(f"[gpu] k == E, large batch T={T} E={E}")
+    _, idx, _ = check_exact(X, W_r, bias, E)
+    assert np.all(idx == np.arange(E)[None, :])
