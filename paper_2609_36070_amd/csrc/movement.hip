@@ -438,75 +438,157 @@ __global__ __launch_bounds__(256) void clip_offsets_kernel(const int *__restrict
     for (int e = threadIdx.x; e <= E; e += 256) out[e] = min(max(offsets[e], w0), w1);
 }
 
-// dW_r = X^T dZ in two fixed-order stages.  Stage 1: block (512-column
-// block, chunk of 256 tokens) -> part[chunk][i][e]; within the block each
-// wave sums 64 consecutive tokens for 8 columns per lane and 8 experts at a
-// time, and the 4 waves' sums are added in wave order.  Stage 2 sums the
-// chunks in order.
-constexpr int DWR_TC = 256;   // tokens per chunk (4 waves x 64)
-constexpr int DWR_TW = 64;    // tokens per wave
-constexpr int DWR_CB = 512;   // columns per block (64 lanes x 8)
-constexpr int DWR_TB = 8;     // token rows loaded together
+// dW_r = X^T dZ in two fixed-order stages.  Stage 1: block (256 columns,
+// chunk of DWR_TC tokens) -> part[chunk][i][e]; stage 2 sums the chunks in
+// order.
+constexpr int DWR_TC = 256;             // tokens per chunk
 
-__global__ __launch_bounds__(256) void dwr_partial_kernel(const uint16_t *__restrict__ X,
-                                                          const float *__restrict__ dZ, int T,
-                                                          int d, int E,
-                                                          float *__restrict__ part) {
-    __shared__ float red[4][64 * 65];   // [wave][lane * 65 + 8 column + expert], padded rows
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int i0 = blockIdx.x * DWR_CB + 8 * lane;
+// Stage 1 on MFMA.  dZ is split into bf16 hi + lo (hi = dZ rounded to bf16,
+// lo = the rest rounded again; each bf16 x bf16 product is exact in fp32), so
+// dW_r[i][e] = sum_t X[t][i] hi[t][e] + sum_t X[t][i] lo[t][e] with fp32
+// accumulation, and the contraction over tokens runs as
+// v_mfma_f32_16x16x32_bf16 with M = 16 columns of X, N = 8 experts x
+// {hi, lo}, K = 32 tokens.  A block owns 256 columns and one chunk of
+// DWR_TC tokens (4 steps of 64); each wave owns 64 columns (4 m-tiles).
+// X[64][256] tiles reach LDS by direct loads (global_load_lds_dwordx4, two
+// stages, the next step in flight while one is multiplied); the chunk's
+// split dZ is staged once per group of 8 experts.  X fragments come from the
+// transposing ds_read_b64_tr_b16, which hands each lane one column of a
+// 4 x 16 block.  X's LDS rows are 512 bytes with the 32-byte block index XOR
+// s(k) = (k & 3) | ((k >> 3) & 3) << 2, so the 16 rows one transposing read
+// touches sit at 16 different block positions; the swizzle is applied on the
+// global side of the loads.  74 KB of LDS: two blocks per CU.
+constexpr int DWM_COLS = 256;            // columns per block
+constexpr int DWM_STEP = 64;             // tokens per LDS stage
+constexpr int DWM_ZLD = DWR_TC + 8;      // padded row of the split-dZ tile
+
+typedef __bf16 dwm_bf16x4_t __attribute__((ext_vector_type(4)));
+#define DWM_LDS __attribute__((address_space(3)))
+
+DEV int dwm_swz(int k) { return (k & 3) | (((k >> 3) & 3) << 2); }
+
+// Workgroup barrier without the fence __syncthreads() carries (which would
+// wait for the direct loads still in flight); each wave waits for its own
+// loads first, and LDS reads before it have all been consumed.
+DEV void dwm_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// s_waitcnt vmcnt(N), other counters untouched (gfx9 encoding).
+template <int N>
+DEV void dwm_wait_vmcnt() {
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+__global__ __launch_bounds__(256) void dwr_mfma_kernel(const uint16_t *__restrict__ X,
+                                                       const float *__restrict__ dZ, int T, int d,
+                                                       int E, float *__restrict__ part) {
+    __shared__ __attribute__((aligned(16))) uint16_t xa[DWM_STEP * DWM_COLS];
+    __shared__ __attribute__((aligned(16))) uint16_t xb[DWM_STEP * DWM_COLS];
+    __shared__ __attribute__((aligned(16))) uint16_t zsh[16 * DWM_ZLD];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, r = lane & 15;
+    const int i0 = blockIdx.x * DWM_COLS;
     const int ch = blockIdx.y;
-    const int tw0 = ch * DWR_TC + wave * DWR_TW;
-    const int tw1 = min(T, tw0 + DWR_TW);
-    const bool col_ok = i0 < d;
-    for (int e0 = 0; e0 < E; e0 += 8) {
-        float acc[8][8];   // [column][expert]
+    const int tc0 = ch * DWR_TC, tc1 = min(T, tc0 + DWR_TC);
+    const int n = (tc1 - tc0 + DWM_STEP - 1) / DWM_STEP;
+
+    // this lane's 8 direct loads of a step: LDS row 16 wave + 2p + lane / 32,
+    // 16-byte position lane % 32, which holds global chunk lcol (swizzle)
+    int lrow[8], lcol[8];
 #pragma unroll
-        for (int c = 0; c < 8; ++c)
+    for (int p = 0; p < 8; ++p) {
+        const int row = 16 * wave + 2 * p + (lane >> 5), pos = lane & 31;
+        lrow[p] = row;
+        lcol[p] = i0 + 8 * (2 * ((pos >> 1) ^ dwm_swz(row)) + (pos & 1));
+    }
+    // rows past the chunk re-read its last token; their dZ entries are 0
+    auto issue = [&](uint16_t *buf, int st) {
+        const int tb = tc0 + st * DWM_STEP;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[c][e] = 0.f;
-        for (int tb = tw0; tb < tw1; tb += DWR_TB) {
-            u32x4_t xv[DWR_TB];
+        for (int p = 0; p < 8; ++p) {
+            const int t = min(tb + lrow[p], tc1 - 1);
+            __builtin_amdgcn_global_load_lds(X + (long)t * d + lcol[p],
+                                             (DWM_LDS void *)(buf + (8 * wave + p) * 512), 16, 0, 0);
+        }
+    };
+    auto compute = [&](const uint16_t *buf, int st, f32x4_t (&acc)[4]) {
 #pragma unroll
-            for (int u = 0; u < DWR_TB; ++u) {
-                const int t = min(tb + u, tw1 - 1);
-                xv[u] = col_ok ? ld_u32x4(X + (long)t * d + i0) : u32x4_t{0, 0, 0, 0};
+        for (int ks = 0; ks < DWM_STEP / 32; ++ks) {
+            const bf16x8_t bz = __builtin_bit_cast(
+                bf16x8_t, *reinterpret_cast<const u32x4_t *>(
+                              &zsh[r * DWM_ZLD + DWM_STEP * st + 32 * ks + 8 * g]));
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+                const int cb = wave * 64 + 16 * mt;   // first column of the m-tile
+                dwm_bf16x4_t v[2];
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    const int k = 32 * ks + 8 * g + 4 * q + (r >> 2);
+                    const int off = k * DWM_COLS + (((cb >> 4) ^ dwm_swz(k)) << 4) + 4 * (r & 3);
+                    v[q] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((DWM_LDS dwm_bf16x4_t *)(buf + off));
+                }
+                const bf16x8_t a = bf16x8_t{v[0][0], v[0][1], v[0][2], v[0][3],
+                                            v[1][0], v[1][1], v[1][2], v[1][3]};
+                acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bz, acc[mt], 0, 0, 0);
             }
+        }
+    };
+
+    for (int eg0 = 0; eg0 < E; eg0 += 8) {
+        // the chunk's dZ for experts eg0 .. eg0 + 7, split: rows 0-7 hi, 8-15 lo
+        {
+            // all 8 loads issued together (clamped in bounds), then masked
+            const int t = tc0 + tid;   // 256 threads = DWR_TC tokens
+            const float *zrow = dZ + (long)min(t, tc1 - 1) * E;
+            float v[8];
 #pragma unroll
-            for (int u = 0; u < DWR_TB; ++u) {
-                if (tb + u < tw1) {
-                    const int t = tb + u;
-                    float dz[8];
+            for (int e = 0; e < 8; ++e) v[e] = zrow[min(eg0 + e, E - 1)];
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) dz[e] = e0 + e < E ? dZ[(long)t * E + e0 + e] : 0.f;
+            for (int e = 0; e < 8; ++e) {
+                const float z = (t < tc1 && eg0 + e < E) ? v[e] : 0.f;
+                const uint16_t hi = f2bf(z);
+                zsh[e * DWM_ZLD + tid] = hi;
+                zsh[(8 + e) * DWM_ZLD + tid] = f2bf(z - bf2f(hi));
+            }
+        }
+        __syncthreads();
+        f32x4_t acc[4];
 #pragma unroll
-                    for (int h = 0; h < 4; ++h) {
-                        const float x0 = bf_lo(xv[u][h]), x1 = bf_hi(xv[u][h]);
+        for (int mt = 0; mt < 4; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        issue(xa, 0);
+        if (n > 1) issue(xb, 1);
+        for (int st = 0; st < n; st += 2) {
+            // step st from xa: in flight are st and, if it exists, st + 1
+            if (st + 1 < n) dwm_wait_vmcnt<8>(); else dwm_wait_vmcnt<0>();
+            dwm_barrier();
+            compute(xa, st, acc);
+            dwm_barrier();
+            if (st + 2 < n) issue(xa, st + 2);
+            if (st + 1 < n) {
+                if (st + 2 < n) dwm_wait_vmcnt<8>(); else dwm_wait_vmcnt<0>();
+                dwm_barrier();
+                compute(xb, st + 1, acc);
+                dwm_barrier();
+                if (st + 3 < n) issue(xb, st + 3);
+            }
+        }
+        // lane (g, r) holds columns 4g + q of each m-tile for n = r: hi for
+        // r < 8, lo for r >= 8; hi + lo, then the lane with r < 8 stores
 #pragma unroll
-                        for (int e = 0; e < 8; ++e) {
-                            acc[2 * h][e] = acc[2 * h][e] + x0 * dz[e];
-                            acc[2 * h + 1][e] = acc[2 * h + 1][e] + x1 * dz[e];
-                        }
-                    }
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float lo = __shfl_xor(acc[mt][q], 8);
+                const int e = eg0 + r;
+                if (r < 8 && e < E) {
+                    const int i = i0 + wave * 64 + 16 * mt + 4 * g + q;
+                    part[((long)ch * d + i) * E + e] = acc[mt][q] + lo;
                 }
             }
-        }
-        __syncthreads();   // the previous expert group's reads of red are done
-#pragma unroll
-        for (int c = 0; c < 8; ++c)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) red[wave][lane * 65 + 8 * c + e] = acc[c][e];
-        __syncthreads();
-        // 4096 sums of this block: entry q = 64 lane + 8 c + e, wave order fixed
-        for (int q = threadIdx.x; q < 64 * 64; q += 256) {
-            const int l = q >> 6, c = (q >> 3) & 7, e = q & 7;
-            const int i = blockIdx.x * DWR_CB + 8 * l + c;
-            if (i < d && e0 + e < E) {
-                const int r = l * 65 + 8 * c + e;
-                part[((long)ch * d + i) * E + e0 + e] = red[0][r] + red[1][r] + red[2][r] + red[3][r];
-            }
-        }
     }
 }
 
@@ -514,8 +596,16 @@ __global__ __launch_bounds__(256) void dwr_reduce_kernel(const float *__restrict
                                                          long n, float *__restrict__ dWr) {
     const long q = (long)blockIdx.x * 256 + threadIdx.x;
     if (q >= n) return;
+    // 16 chunk loads in flight at a time, added in chunk order
     float acc = 0.f;
-    for (int c = 0; c < nch; ++c) acc = acc + part[(long)c * n + q];
+    for (int c0 = 0; c0 < nch; c0 += 16) {
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = c0 + u < nch ? part[(long)(c0 + u) * n + q] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 16; ++u)
+            if (c0 + u < nch) acc = acc + v[u];
+    }
     dWr[q] = acc;
 }
 
@@ -671,11 +761,12 @@ hipError_t launch_clip_offsets(const int *offsets, int E, int w0, int w1, int *o
 
 hipError_t launch_dwr(const uint16_t *X, const float *dZ, int T, int d, int E, float *part,
                       float *dWr, hipStream_t st) {
+    if (d % DWM_COLS) return hipErrorInvalidValue;   // the layer requires d % 256 == 0
     const int nch = dwr_nchunks(T);
     const long n = (long)d * E;
     if (nch > 0) {
-        dim3 grid((unsigned)((d + DWR_CB - 1) / DWR_CB), (unsigned)nch);
-        dwr_partial_kernel<<<grid, dim3(256), 0, st>>>(X, dZ, T, d, E, part);
+        dim3 grid((unsigned)(d / DWM_COLS), (unsigned)nch);
+        dwr_mfma_kernel<<<grid, dim3(256), 0, st>>>(X, dZ, T, d, E, part);
     }
     dwr_reduce_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st>>>(part, nch, n, dWr);
     return hipGetLastError();
