@@ -462,7 +462,10 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
         }
     }
 
-    auto issue = [&](int kt, uint16_t *la, uint16_t *lb) {
+    // issue() in parts: the WGRAD k-row index fetch, the A loads, the B loads
+    constexpr int LD_IDX = 1, LD_A = 2, LD_B = 4, LD_ALL = 7;
+    int pa[LD_PER_OP], pb[LD_PER_OP];
+    auto issue = [&](int kt, uint16_t *la, uint16_t *lb, int parts) {
         // WGRAD k rows come through the plan's token index: fetch every index
         // this K step needs first (scalar loads, one wait), then issue the
         // direct loads.  A wave's k rows are consecutive plan positions, so
@@ -471,10 +474,15 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
             // steps run in order: the current segment's bases advance by one
             // K step per call, and a new segment is entered when one ends
             const int kl = cs_st * BK;
+            // row offsets in 32 bits (token < 2^24, pitch < 2^21)
+            if (parts & LD_A) {
+#pragma unroll
+                for (int i = 0; i < LD_PER_OP; ++i)
+                    load_lds16(cs.ab + kl + (cm_t[i] * cs.lda + cm_c[i]), la + lds_off[i]);
+            }
+            if (!(parts & LD_B)) return;   // the step advances with its B loads
 #pragma unroll
             for (int i = 0; i < LD_PER_OP; ++i) {
-                // row offsets in 32 bits (token < 2^24, pitch < 2^21)
-                load_lds16(cs.ab + kl + (cm_t[i] * cs.lda + cm_c[i]), la + lds_off[i]);
                 if constexpr (Tr::B_COL)
                     load_lds16(cs.bb + (long)kl * cs.ldb + cm_b[i], lb + lds_off[i]);
                 else
@@ -486,8 +494,7 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
             }
             return;
         }
-        int pa[LD_PER_OP], pb[LD_PER_OP];
-        if constexpr (Tr::WG) {
+        if constexpr (Tr::WG) if (parts & LD_IDX) {
             int ia[2 * LD_PER_OP], ib[2 * LD_PER_OP];
             // this wave's k rows are the 2 LD_PER_OP consecutive positions from r0
             const int r0 = kt * BK + 2 * LD_PER_OP * wave;
@@ -529,7 +536,8 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
             }
         }
         // ---- operand A ----
-        if constexpr (!Tr::A_COL) {
+        if (!(parts & LD_A)) {
+        } else if constexpr (!Tr::A_COL) {
             const bool second = (MODE == BWD_DX) && kt >= nk_half;
             const int kk = (second ? kt - nk_half : kt) * BK;
 #pragma unroll
@@ -547,7 +555,8 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
             }
         }
         // ---- operand B ----
-        if constexpr (!Tr::B_COL) {
+        if (!(parts & LD_B)) {
+        } else if constexpr (!Tr::B_COL) {
             const bool second = (MODE == BWD_DX) && kt >= nk_half;
             const int kk = (second ? kt - nk_half : kt) * BK;
 #pragma unroll
@@ -609,13 +618,30 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
     // ks + 1 are issued before the MFMAs of sub-step ks (the scheduling
     // barrier stops the compiler from sinking them to their uses), so LDS
     // latency hides behind the matrix cores.
-    auto compute = [&](const uint16_t *la, const uint16_t *lb) {
+    //
+    // The next tile's direct loads (step nkt, into stages nla / nlb) go out in
+    // two halves, one operand ahead of the MFMAs of sub-step 0 and the other
+    // ahead of sub-step 1, instead of all at the step's start: every wave of
+    // every CU of an XCD reaches the step's barrier together, and 64 KB per CU
+    // requested at once queue in L2.  The K-contiguous row tile goes first.
+    // Measured on the training step: 3-6 % per GEMM; later halves (sub-steps
+    // 0 and 2, or 1 and 2) were slower, and so was the column tile first.
+    // The gathered WGRAD (index fetch and both operands as column tiles)
+    // keeps all its loads at the step's start.
+    constexpr int SPLIT = (MODE == WGRAD) ? 0 : (Tr::A_COL && !Tr::B_COL) ? 2 : 1;
+    auto compute = [&](const uint16_t *la, const uint16_t *lb, int nkt, uint16_t *nla, uint16_t *nlb) {
         bf16x8_t af[2][TM], bfr[2][TN];
         load_frags(la, lb, 0, af[0], bfr[0]);
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
             const int cur = ks & 1;
             if (ks + 1 < BK / 16) load_frags(la, lb, ks + 1, af[cur ^ 1], bfr[cur ^ 1]);
+            if (SPLIT != 0 && nkt >= 0 && ks < 2) {
+                const int first = SPLIT == 1 ? LD_A : LD_B;
+                asm volatile("" ::: "memory");   // after this sub-step's LDS reads
+                issue(nkt, nla, nlb, ks == 0 ? (LD_IDX | first) : (LD_A | LD_B) ^ first);
+                asm volatile("" ::: "memory");
+            }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
@@ -628,26 +654,30 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
 
     // Double-buffered K loop, unrolled by two so each half names its stages:
     // wait for this wave's loads of the tile about to be read, barrier (all
-    // waves' loads landed, all reads of the other stage done), start filling
-    // the other stage with the next tile, then compute on this one.
-    if (nk > 0) issue(0, lds_a0, lds_b0);
+    // waves' loads landed, all reads of the other stage done), then compute on
+    // this stage while the next tile streams into the other one.
+    if (nk > 0) issue(0, lds_a0, lds_b0, LD_ALL);
     int kt = 0;
     for (; kt + 1 < nk; kt += 2) {
         wait_vmcnt<0>();
         barrier_no_fence();
-        issue(kt + 1, lds_a1, lds_b1);
-        asm volatile("" ::: "memory");   // keep the loads ahead of this step's LDS reads
-        compute(lds_a0, lds_b0);
+        if constexpr (SPLIT == 0) {
+            issue(kt + 1, lds_a1, lds_b1, LD_ALL);
+            asm volatile("" ::: "memory");   // keep the loads ahead of this step's LDS reads
+        }
+        compute(lds_a0, lds_b0, kt + 1, lds_a1, lds_b1);
         wait_vmcnt<0>();
         barrier_no_fence();
-        if (kt + 2 < nk) issue(kt + 2, lds_a0, lds_b0);
-        asm volatile("" ::: "memory");
-        compute(lds_a1, lds_b1);
+        if constexpr (SPLIT == 0) {
+            if (kt + 2 < nk) issue(kt + 2, lds_a0, lds_b0, LD_ALL);
+            asm volatile("" ::: "memory");
+        }
+        compute(lds_a1, lds_b1, kt + 2 < nk ? kt + 2 : -1, lds_a0, lds_b0);
     }
     if (kt < nk) {
         wait_vmcnt<0>();
         barrier_no_fence();
-        compute(lds_a0, lds_b0);
+        compute(lds_a0, lds_b0, -1, nullptr, nullptr);
     }
     __syncthreads();
 
