@@ -152,7 +152,9 @@ __shared__ __attribute__((aligned(16))) uint16_t lds_a1[TILE_ELEMS];
 __shared__ __attribute__((aligned(16))) uint16_t lds_b1[TILE_ELEMS];
 __shared__ int s_info[2];
 // fused forward: first m-tile slot of every expert in the grouped raster
+// (entry E: the total), and the plan's offsets [E+1]
 __shared__ int s_tilebase[257];
+__shared__ int s_offs[257];
 
 // One output tile of product MODE: workgroup vb of a grid of nvb (a multiple
 // of 8, so vb % 8 is the XCD the tile runs on).
@@ -188,10 +190,15 @@ DEV void wait_count(const int *ctr, int need, int *err) {
 
 // Publish a finished tile: every wave waits for its own stores, then one
 // release add (which writes this XCD's L2 back) makes them visible to all XCDs.
-DEV void signal_done(int *ctr) {
+// When every waiter runs on this XCD (local), the stores are already in the
+// L2 they read through, so the add skips the write-back.
+DEV void signal_done(int *ctr, bool local) {
     wait_vmcnt<0>();
     __syncthreads();
-    if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0) {
+        if (local) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        else __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
 }
 
 // Four consecutive plan indices; plan positions carry no alignment beyond 4 bytes.
@@ -221,12 +228,29 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
     // ---------------- tile assignment ----------------
     int e = 0, row0 = 0, row_end = 0, n0 = 0, ntile = 0;
     int m0 = 0, kbeg = 0, klen = 0;
+    int ebase = 0;   // grouped row products: the expert's first plan row
     if constexpr (Tr::GROUPED_ROWS) {
         const int ntn = (MODE == FWD_UP) ? g.N / (BN / 2) : g.N / BN;
         int mt = 0;
         if (!map_tile(vb, g.tiles_m, ntn, mt, ntile)) return;
         n0 = ntile * ((MODE == FWD_UP) ? BN / 2 : BN);
-        if constexpr (GROUPED) {
+        if constexpr (GROUPED && PERSISTENT) {
+            // the fused kernel keeps the grouped raster's prefix and the
+            // offsets in LDS: each wave finds the expert of m-tile slot mt by
+            // a ballot over them (no global loads, no barrier)
+            e = -1;
+            for (int base = 0; base < g.E && e < 0; base += 64) {
+                const int ee = base + lane;
+                const bool hit = ee < g.E && mt >= s_tilebase[ee] && mt < s_tilebase[ee + 1];
+                const unsigned long long m = __ballot(hit);
+                if (m) e = base + __builtin_ctzll(m);
+            }
+            e = uniform(e);
+            if (e < 0) return;
+            ebase = uniform(s_offs[e]);
+            row0 = ebase + (mt - uniform(s_tilebase[e])) * BM;
+            row_end = uniform(s_offs[e + 1]);
+        } else if constexpr (GROUPED) {
             if (tid == 0) s_info[0] = -1;
             __syncthreads();
             if (tid < 64) {
@@ -252,7 +276,8 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
             __syncthreads();
             e = uniform(s_info[0]);
             if (e < 0) return;
-            row0 = uniform(g.offsets[e] + uniform(s_info[1]) * BM);
+            ebase = uniform(g.offsets[e]);
+            row0 = ebase + uniform(s_info[1]) * BM;
             row_end = uniform(g.offsets[e + 1]);
         } else {
             row0 = mt * BM;
@@ -333,7 +358,7 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
             const int c = row_swz(r, lane % (BK / 8));
             // rows past the region's end load its last row; their results are never stored
             const int p = min(row0 + r, row_end - 1);
-            int phys = g.a_local ? p - uniform(g.offsets[e]) : a_rows ? a_rows[p] : p;
+            int phys = g.a_local ? p - ebase : a_rows ? a_rows[p] : p;
             phys = min(max(phys, 0), g.a_nrows - 1);
             a_row[i] = g.A + (long)phys * g.lda + 8 * c;
             if (MODE == BWD_DX) a2_row[i] = g.A2 + (long)phys * g.lda + 8 * c;
@@ -853,7 +878,7 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
         }
     }
     if constexpr (Tr::GROUPED_ROWS) {
-        if (g.sig) signal_done(g.sig + slot);
+        if (g.sig) signal_done(g.sig + slot, g.sig_local);
     }
 }
 
@@ -1021,6 +1046,13 @@ struct FusedFwd {
     const int *route_pos, *topk_idx, *offsets;
     const int *down_done_r, *down_done_s;
     int need_r, need_s;  // n-tiles per m-tile of the routed / shared down products
+    // dense routing with every expert's m-tiles a multiple of 32: an XCD's
+    // routed up/gate items are taken token group first (groups_x token groups
+    // of 4 m-tiles per expert on each XCD), so the folded down tiles of its
+    // first token group are ready long before the up/gate phase ends; 0 keeps
+    // the raster's expert-major order
+    int groups_x;
+    int tpg_up;          // routed up/gate tiles per group (4 m-tiles x its n-tiles)
     int T, d, k, E, R;
     uint16_t *Y;
 };
@@ -1114,9 +1146,14 @@ DEV void fused_combine(const FusedFwd &fa, int blk) {
     }
 }
 
+// The XCD this wave runs on (hardware register XCC_ID, bits 3:0).
+DEV int xcc_id() { return __builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20) & 7; }
+
 __global__ __launch_bounds__(NTHREADS, 1) void fused_forward_kernel(FusedFwd fa) {
     const int tid = threadIdx.x;
-    const int q = blockIdx.x & 7;
+    // every workgroup serves the queue of the XCD it runs on, so a tile and
+    // the items that wait for it share that XCD's L2
+    const int q = xcc_id();
     // first m-tile slot of every expert (the grouped raster's prefix)
     if (tid < 64) {
         const int lane = tid;
@@ -1134,7 +1171,9 @@ __global__ __launch_bounds__(NTHREADS, 1) void fused_forward_kernel(FusedFwd fa)
             if (ee < fa.E) s_tilebase[ee] = cum + x - tiles;
             cum += __shfl(x, 63, 64);
         }
+        if (lane == 0) s_tilebase[fa.E] = cum;
     }
+    for (int i = tid; i <= fa.E; i += NTHREADS) s_offs[i] = fa.offsets[i];
     __syncthreads();
     // the next ticket is requested when an item starts, so its round trip
     // overlaps the item instead of stalling the workgroup between items
@@ -1149,7 +1188,11 @@ __global__ __launch_bounds__(NTHREADS, 1) void fused_forward_kernel(FusedFwd fa)
 #pragma unroll
         for (int i = 1; i < 5; ++i)
             if (t >= fa.base[i]) P = i;
-        const int j = t - fa.base[P];
+        int j = t - fa.base[P];
+        if (P == 1 && fa.groups_x > 0) {
+            const int gi = j / fa.tpg_up, w = j % fa.tpg_up;   // this XCD's gi-th group
+            if (gi < fa.E * fa.groups_x) j = ((gi % fa.E) * fa.groups_x + gi / fa.E) * fa.tpg_up + w;
+        }
         const int vb = 8 * j + q;
         if (P == 0) gemm_tile<FWD_UP, false, true>(fa.g[0], fa.g[0].a_rows, fa.g[0].b_rows, vb, fa.grid[0]);
         else if (P == 1) gemm_tile<FWD_UP, true, true>(fa.g[1], fa.g[1].a_rows, fa.g[1].b_rows, vb, fa.grid[1]);
@@ -1250,6 +1293,14 @@ hipError_t launch_fused_forward(const GemmArgs &up_s, const GemmArgs &up_r, cons
     fa.need_r = ntn_dn_r; fa.need_s = ntn_dn_s;
     fa.T = (int)T; fa.d = d; fa.k = k; fa.E = E; fa.R = (int)R;
     fa.Y = Y;
+    // Dense routing with T a multiple of 32 tiles: expert e's m-tile t is the
+    // raster's slot e (T / BM) + t, in group (e T / BM + t) / 4, which goes
+    // to the same XCD as the shared tile t and the token tile t of the folded
+    // down product (group t / 4): every wait is XCD-local.
+    const bool local = dense && T % (32 * BM) == 0;
+    fa.groups_x = local ? (int)(T / BM / 32) : 0;
+    fa.tpg_up = RASTER_GM * ntn_up_r;
+    fa.g[0].sig_local = fa.g[1].sig_local = local ? 1 : 0;
     const int grid = cu_count() / 8 * 8 > 0 ? cu_count() / 8 * 8 : 8;
     fused_forward_kernel<<<dim3(grid), dim3(NTHREADS), 0, st>>>(fa);
     return hipGetLastError();

@@ -46,6 +46,7 @@ struct GemmArgs {
     const int *dep = nullptr;
     int dep_need = 0;
     int *sig = nullptr;
+    int sig_local = 0;                 // every waiter on sig runs on this tile's XCD
     int *err = nullptr;                // bit 1 set when a wait gave up
     // Dense routing (every token routes to every one of the E experts): the
     // K loop of a token tile runs over segments.  Routed segment e reads the
