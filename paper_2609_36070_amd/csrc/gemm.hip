@@ -1053,6 +1053,7 @@ struct FusedFwd {
     // the raster's expert-major order
     int groups_x;
     int tpg_up;          // routed up/gate tiles per group (4 m-tiles x its n-tiles)
+    int xcc_queues;      // the device is 8 XCDs: serve the queue of the XCD read from XCC_ID
     int T, d, k, E, R;
     uint16_t *Y;
 };
@@ -1152,8 +1153,9 @@ DEV int xcc_id() { return __builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20) &
 __global__ __launch_bounds__(NTHREADS, 1) void fused_forward_kernel(FusedFwd fa) {
     const int tid = threadIdx.x;
     // every workgroup serves the queue of the XCD it runs on, so a tile and
-    // the items that wait for it share that XCD's L2
-    const int q = xcc_id();
+    // the items that wait for it share that XCD's L2 (on a device of another
+    // shape, workgroup b serves queue b mod 8 and nothing is XCD-local)
+    const int q = fa.xcc_queues ? xcc_id() : (int)(blockIdx.x & 7);
     // first m-tile slot of every expert (the grouped raster's prefix)
     if (tid < 64) {
         const int lane = tid;
@@ -1297,7 +1299,9 @@ hipError_t launch_fused_forward(const GemmArgs &up_s, const GemmArgs &up_r, cons
     // raster's slot e (T / BM) + t, in group (e T / BM + t) / 4, which goes
     // to the same XCD as the shared tile t and the token tile t of the folded
     // down product (group t / 4): every wait is XCD-local.
-    const bool local = dense && T % (32 * BM) == 0;
+    // an MI355X in its 8-XCD mode: 256 CUs, 32 per XCD
+    fa.xcc_queues = cu_count() == 256 ? 1 : 0;
+    const bool local = fa.xcc_queues && dense && T % (32 * BM) == 0;
     fa.groups_x = local ? (int)(T / BM / 32) : 0;
     fa.tpg_up = RASTER_GM * ntn_up_r;
     fa.g[0].sig_local = fa.g[1].sig_local = local ? 1 : 0;
