@@ -381,6 +381,26 @@ def hbm_bytes(w):
     return out
 
 
+STEP_OUTPUTS = ("logits", "topk_idx", "topk_w", "counts", "offsets", "perm", "route_pos", "Y", "dX",
+                "dZ", "dW_r", "dW_gate", "dW_up", "dW_down", "dWg_s", "dWu_s", "dWd_s")
+
+
+def determinism_check(L, reps=2):
+    """Every output of the step (routing, plan, Y, and with a backward dX
+    and every gradient) after `reps` more whole steps on the same inputs,
+    compared bitwise with its value after the timed steps."""
+    import torch
+    torch.cuda.synchronize()
+    first = {n: getattr(L, n).clone() for n in STEP_OUTPUTS if getattr(L, n, None) is not None}
+    differ = set()
+    for _ in range(reps):
+        L.step()
+        torch.cuda.synchronize()
+        differ |= {n for n, t in first.items() if not torch.equal(getattr(L, n), t)}
+    return {"runs": reps + 1, "bitwise_identical": not differ, "outputs": len(first),
+            "differing": sorted(differ)}
+
+
 def copy_ceiling(H, stream, mib=2048, reps=5):
     """The practical HBM ceiling of this GPU (bytes read + bytes written per
     second) from two plain streaming kernels over `mib` MiB of fp32: torch's
@@ -818,6 +838,8 @@ def main():
 
     step_flops = w.fwd_flops() + (w.bwd_flops() if w.backward else 0.0)
     value = step_flops / (ms_step * 1e-3) / 1e12
+    determinism = determinism_check(L)
+    log(f"[bench] determinism: {determinism}")
     stage_report = {}
     for name, ms in stages.items():
         key = name.split(".", 1)[-1]
@@ -917,6 +939,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "graph_replay": graph,
+        "determinism": determinism,
         "hbm_copy": copy,
         "hbm_kernels": hbm,
         "stages": stage_report,
