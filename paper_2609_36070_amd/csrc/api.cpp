@@ -94,7 +94,10 @@ Layout make_layout(const moe_shape &s, long ring_rows = -1) {
     L.dwr_part = take((size_t)dwr_nchunks((long)T) * d * E * 4);
     L.dzs = take(T * 64 * 2);   // dense routing: router-term rows of dX
     L.wrs = take(d * 64 * 2);
-    L.xt_ld = (long)((T + 63) / 64 * 64);
+    // X^T and dY^T rows: the tokens rounded up to a K step, plus one more
+    // (zero) K step, so a window of the bounded-memory backward that starts
+    // mid-expert (an unaligned first column) still reads inside the row
+    L.xt_ld = (long)((T + 63) / 64 * 64 + 64);
     L.xtt = take(s.k == s.E ? d * (size_t)L.xt_ld * 2 : 0);   // dense routing: X^T [d][xt_ld]
     L.dytt = take(s.k == s.E ? d * (size_t)L.xt_ld * 2 : 0);  // dense routing: dY^T likewise
     L.bwd_total = o;
@@ -546,13 +549,14 @@ hipError_t shared_wgrads(const moe_shape &sh, const Layout &L, void *ws, const m
 // events between its GEMMs.
 hipError_t shared_backward(const moe_shape &sh, const Layout &L, void *ws, const moe_bf16 *dY,
                            const moe_bf16 *X, const moe_weights *w, const moe_grads *gr,
-                           const StageMarks &mk, hipStream_t s) {
+                           const StageMarks &mk, hipStream_t s, const uint16_t *xt = nullptr,
+                           const uint16_t *dyt = nullptr) {
     hipError_t e;
     if ((e = shared_dgrad(sh, L, ws, dY, w, s)) != hipSuccess) return e;
     if ((e = mk.mark(7)) != hipSuccess) return e;
     if ((e = shared_dx(sh, L, ws, w, s)) != hipSuccess) return e;
     if ((e = mk.mark(8)) != hipSuccess) return e;
-    return shared_wgrads(sh, L, ws, dY, X, gr, s);
+    return shared_wgrads(sh, L, ws, dY, X, gr, s, xt, dyt);
 }
 
 // Dense routing (k == E): every token routes to every local expert, so its
@@ -999,7 +1003,14 @@ moe_status moe_backward_ring(const moe_shape *shape, const moe_bf16 *dY, const m
 
     MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, at<int>(ws, L.rowidx),
                         at<float>(ws, L.wperm), at<uint16_t>(ws, L.zeros), s));
-    if (shared) MOE_TRY(shared_backward(*shape, L, ws, dY, X, weights, grads, none, s));
+    // dense routing: the weight gradients of every window read X^T and dY^T
+    // (made once) as K-contiguous rows, each expert's rows of the window
+    // being the tokens from (first row - the expert's first plan row)
+    const bool dense = dense_routing(*shape);
+    uint16_t *xt = dense ? at<uint16_t>(ws, L.xtt) : nullptr;
+    uint16_t *dyt = dense ? at<uint16_t>(ws, L.dytt) : nullptr;
+    if (dense) MOE_TRY(dense_transposes(*shape, L, X, dY, xt, dyt, s));
+    if (shared) MOE_TRY(shared_backward(*shape, L, ws, dY, X, weights, grads, none, s, xt, dyt));
     // windows alternate between two clipped-offset arrays, so the replay of
     // window m + 1 can share a launch with the weight gradients of window m
     auto window = [&](int m) {
@@ -1023,16 +1034,28 @@ moe_status moe_backward_ring(const moe_shape *shape, const moe_bf16 *dY, const m
                                     plan->route_pos, T, d, k, acc, m == 0,
                                     shared ? at<uint16_t>(ws, L.dXsh) : nullptr, nullptr, s));
         GemmArgs wg[3];
-        for (int i = 0; i < 3; ++i) wg[i] = wgrad_args(*shape, L, ws, X, dY, grads, win, m > 0, i);
+        int modes[3] = {0, 0, 0};
+        for (int i = 0; i < 3; ++i) {
+            wg[i] = wgrad_args(*shape, L, ws, X, dY, grads, win, m > 0, i);
+            if (!dense) continue;
+            wg[i].tok_offsets = plan->offsets;
+            if (i < 2) {
+                wg[i].A = xt; wg[i].lda = L.xt_ld; wg[i].a_rows = nullptr; wg[i].a_local = 1;
+                modes[i] = 1;
+            } else {
+                wg[i].B = dyt; wg[i].ldb = L.xt_ld; wg[i].b_rows = nullptr; wg[i].b_local = 1;
+                modes[i] = 2;
+            }
+        }
         if (m + 1 < nwin) {
             // recompute only A and B of the next window (no H, no down
             // projection): its dgrad reads nothing else
             const Window nxt = window(m + 1);
             MOE_TRY(clip(m + 1));
             const GemmArgs up = up_args(*shape, L, ws, X, weights, nxt, false, true);
-            MOE_TRY(launch_gemm_wgrad_batch(wg, 3, E, &up, nxt.count(), s));
+            MOE_TRY(launch_gemm_wgrad_batch(wg, 3, E, &up, nxt.count(), s, modes));
         } else {
-            MOE_TRY(launch_gemm_wgrad_batch(wg, 3, E, nullptr, 0, s));
+            MOE_TRY(launch_gemm_wgrad_batch(wg, 3, E, nullptr, 0, s, modes));
         }
     }
     MOE_TRY(launch_softmax_bwd(at<float>(ws, L.dgpart), L.dg_parts, plan->route_pos, topk_w, topk_idx,

@@ -229,6 +229,7 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
     int e = 0, row0 = 0, row_end = 0, n0 = 0, ntile = 0;
     int m0 = 0, kbeg = 0, klen = 0;
     int ebase = 0;   // grouped row products: the expert's first plan row
+    int tok_base = 0;   // weight gradients: the expert's first plan row of the whole plan
     if constexpr (Tr::GROUPED_ROWS) {
         const int ntn = (MODE == FWD_UP) ? g.N / (BN / 2) : g.N / BN;
         int mt = 0;
@@ -308,6 +309,7 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
         if constexpr (GROUPED) {
             kbeg = uniform(g.offsets[e]);
             klen = uniform(g.offsets[e + 1]) - kbeg;
+            tok_base = g.tok_offsets ? uniform(g.tok_offsets[e]) : kbeg;
         } else {
             kbeg = 0;
             klen = g.K;
@@ -343,8 +345,8 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
     if constexpr (Tr::CMB) {
     } else if constexpr (MODE == WGRAD_T) {
         // A^T rows m0 + r; its columns are the expert's positions (from
-        // kbeg), or with a_local the tokens (from 0)
-        const long acol0 = g.a_local ? 0 : kbeg;
+        // kbeg), or with a_local the tokens (from the token of plan row kbeg)
+        const long acol0 = g.a_local ? kbeg - tok_base : kbeg;
 #pragma unroll
         for (int i = 0; i < LD_PER_OP; ++i) {
             const int r = ROWS_PER_LD * (LD_PER_OP * wave + i) + lane / (BK / 8);
@@ -370,8 +372,8 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
         // set above
     } else if constexpr (MODE == WGRAD_TB) {
         // B^T rows n0 + r; its columns are the expert's positions (from
-        // kbeg), or with b_local the tokens (from 0)
-        const long bcol0 = g.b_local ? 0 : kbeg;
+        // kbeg), or with b_local the tokens (from the token of plan row kbeg)
+        const long bcol0 = g.b_local ? kbeg - tok_base : kbeg;
 #pragma unroll
         for (int i = 0; i < LD_PER_OP; ++i) {
             const int r = ROWS_PER_LD * (LD_PER_OP * wave + i) + lane / (BK / 8);
@@ -898,6 +900,7 @@ constexpr int MAX_BATCH = 4;
 struct GemmBatch {
     GemmArgs g[MAX_BATCH];
     int start[MAX_BATCH + 1];
+    int mode[MAX_BATCH];   // weight-gradient products: 0 WGRAD, 1 WGRAD_T, 2 WGRAD_TB
     int n;          // products
     int up_last;    // the last product is FWD_UP
 };
@@ -911,6 +914,10 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_batch_kernel(GemmBatch bt) {
     const int vb = b - bt.start[i], nvb = bt.start[i + 1] - bt.start[i];
     if (bt.up_last && i == bt.n - 1)
         gemm_tile<FWD_UP, true>(bt.g[i], bt.g[i].a_rows, bt.g[i].b_rows, vb, nvb);
+    else if (bt.mode[i] == 1)
+        gemm_tile<WGRAD_T, true>(bt.g[i], bt.g[i].a_rows, bt.g[i].b_rows, vb, nvb);
+    else if (bt.mode[i] == 2)
+        gemm_tile<WGRAD_TB, true>(bt.g[i], bt.g[i].a_rows, bt.g[i].b_rows, vb, nvb);
     else
         gemm_tile<WGRAD, true>(bt.g[i], bt.g[i].a_rows, bt.g[i].b_rows, vb, nvb);
 }
@@ -974,7 +981,7 @@ hipError_t launch_gemm_wgrad(const GemmArgs &g, int groups, hipStream_t st) {
 }
 
 hipError_t launch_gemm_wgrad_batch(const GemmArgs *wg, int nw, int groups, const GemmArgs *up,
-                                   long up_rows, hipStream_t st) {
+                                   long up_rows, hipStream_t st, const int *modes) {
     GemmBatch bt{};
     if (nw < 0 || nw + (up ? 1 : 0) > MAX_BATCH) return hipErrorInvalidValue;
     long at = 0;
@@ -987,6 +994,8 @@ hipError_t launch_gemm_wgrad_batch(const GemmArgs *wg, int nw, int groups, const
         const long blocks = wgrad_grid(groups, ntm, ntn);
         if ((long)g.tiles_m * ntn <= 0) continue;
         bt.g[bt.n] = g;
+        bt.mode[bt.n] = modes ? modes[i] : 0;
+        if (bt.mode[bt.n] < 0 || bt.mode[bt.n] > 2) return hipErrorInvalidValue;
         bt.start[bt.n] = (int)at;
         at += blocks;
         ++bt.n;

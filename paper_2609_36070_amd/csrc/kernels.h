@@ -69,6 +69,10 @@ struct GemmArgs {
     // loads); a_local for A (rows of a row product, k rows of WGRAD), b_local
     // for WGRAD's B.  The gather pointers are then ignored.
     int a_local = 0, b_local = 0;
+    // The plan's offsets that turn such a row into a token (row minus the
+    // expert's first plan row) when `offsets` are clipped to a window of the
+    // plan (bounded-memory execution); null: `offsets` themselves.
+    const int *tok_offsets = nullptr;
 };
 
 int gemm_tile_m();
@@ -114,8 +118,11 @@ hipError_t launch_fused_forward(const GemmArgs &up_s, const GemmArgs &up_r, cons
                                 const uint16_t *Yexp, const uint16_t *Ysh, const float *topk_w,
                                 const int *route_pos, const int *topk_idx, const int *offsets, int d,
                                 int k, uint16_t *Y, int *counters, int *err, hipStream_t st);
+// modes[i] (null: all 0): 0 the weight gradient on column tiles, 1 with A
+// read as the K-contiguous X^T (as launch_gemm_wgrad_t), 2 with B read as
+// dY^T (as launch_gemm_wgrad_tb).
 hipError_t launch_gemm_wgrad_batch(const GemmArgs *wg, int nw, int groups, const GemmArgs *up,
-                                   long up_rows, hipStream_t st);
+                                   long up_rows, hipStream_t st, const int *modes = nullptr);
 
 int route_epad(int E);
 hipError_t launch_route(const uint16_t *X, const uint16_t *W_r, const float *bias, float *logits,
