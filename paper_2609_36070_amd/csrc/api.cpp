@@ -651,6 +651,37 @@ int ring_windows(const moe_shape &sh, int64_t ring_rows) {
     return m > 0 ? (int)m : 1;   // an empty batch still runs one (empty) window
 }
 
+// Dense routing whose windows hold whole experts (every expert's region is T
+// rows, so a window of a multiple of T rows, or of the whole batch, cuts
+// none): the ring then runs the folded down and dX products of one-pass
+// dense routing on each window's experts, keeping a running fp32 sum per
+// token across windows instead of per-route outputs and a combine pass.
+bool ring_folds(const moe_shape &sh, int64_t ring_rows) {
+    const long R = (long)sh.T * sh.k;
+    return dense_routing(sh) && sh.T > 0 && (ring_rows % sh.T == 0 || ring_rows >= R);
+}
+
+// The folded product of window [w0, w1) (whole experts w0 / T .. w1 / T - 1)
+// of a pass over nwin windows, `first` / `last` in processing order: the
+// first writes the running sum (or, alone, the output), later ones add to
+// it, the last writes the output.
+void fold_window(GemmArgs &g, const moe_shape &sh, long w0, long w1, int nwin, bool first,
+                 bool last, float *acc, moe_bf16 *out) {
+    const long T = sh.T;
+    const long e0 = w0 / T;
+    g.a_row0 = (int)w0;
+    g.a_nrows = (int)w1;
+    g.seg_offsets += e0;
+    g.nseg = (int)(w1 / T - e0);
+    g.B += e0 * g.b_estride;
+    if (g.B2) g.B2 += e0 * g.b_estride;
+    if (nwin > 1) {
+        g.Cf = acc;
+        g.accumulate = first ? 0 : 1;
+        g.C = last ? out : nullptr;
+    }
+}
+
 }  // namespace
 
 extern "C" {
@@ -959,6 +990,27 @@ moe_status moe_forward_ring(const moe_shape *shape, const moe_bf16 *X, const moe
 
     MOE_TRY(launch_prep(plan->perm, plan->offsets, E, topk_w, k, T, at<int>(ws, L.rowidx),
                         at<float>(ws, L.wperm), at<uint16_t>(ws, L.zeros), s));
+    if (ring_folds(*shape, ring_rows)) {
+        // per window: up/gate (H keeps w h) and the folded down product of
+        // its experts; the first window processed also takes the shared
+        // expert's segment
+        if (fs > 0) MOE_TRY(shared_up(*shape, L, ws, X, weights, save_for_backward != 0, s));
+        for (int m = nwin - 1; m >= 0; --m) {
+            const int w0 = (int)(m * ring_rows);
+            const int w1 = (int)(R < w0 + ring_rows ? R : w0 + ring_rows);
+            const Window win{coff, w0, w1};
+            MOE_TRY(launch_clip_offsets(plan->offsets, E, w0, w1, coff, s));
+            GemmArgs gu = up_args(*shape, L, ws, X, weights, win, true, save_for_backward != 0);
+            gu.rowscale = at<float>(ws, L.wperm);
+            MOE_TRY(launch_gemm_fwd_up(gu, win.count(), E, s));
+            GemmArgs gd = down_cmb_args(*shape, L, ws, weights, plan->offsets, Y);
+            gd.A = win.rows<uint16_t>(ws, L.H, (int)shape->f);
+            if (m != nwin - 1) gd.segK_s = 0;
+            fold_window(gd, *shape, w0, w1, nwin, m == nwin - 1, m == 0, at<float>(ws, L.acc), Y);
+            MOE_TRY(launch_gemm_fwd_down_cmb(gd, s));
+        }
+        return MOE_OK;
+    }
     if (fs > 0) {   // first: its output seeds every token's accumulator
         MOE_TRY(shared_up(*shape, L, ws, X, weights, save_for_backward != 0, s));
         MOE_TRY(shared_down(*shape, L, ws, weights, s));
@@ -1010,7 +1062,14 @@ moe_status moe_backward_ring(const moe_shape *shape, const moe_bf16 *dY, const m
     uint16_t *xt = dense ? at<uint16_t>(ws, L.xtt) : nullptr;
     uint16_t *dyt = dense ? at<uint16_t>(ws, L.dytt) : nullptr;
     if (dense) MOE_TRY(dense_transposes(*shape, L, X, dY, xt, dyt, s));
-    if (shared) MOE_TRY(shared_backward(*shape, L, ws, dY, X, weights, grads, none, s, xt, dyt));
+    const bool fold = ring_folds(*shape, ring_rows);
+    if (shared && fold) {
+        // dXsh is folded into the first window's dX product
+        MOE_TRY(shared_dgrad(*shape, L, ws, dY, weights, s));
+        MOE_TRY(shared_wgrads(*shape, L, ws, dY, X, grads, s, xt, dyt));
+    } else if (shared) {
+        MOE_TRY(shared_backward(*shape, L, ws, dY, X, weights, grads, none, s, xt, dyt));
+    }
     // windows alternate between two clipped-offset arrays, so the replay of
     // window m + 1 can share a launch with the weight gradients of window m
     auto window = [&](int m) {
@@ -1029,10 +1088,29 @@ moe_status moe_backward_ring(const moe_shape *shape, const moe_bf16 *dY, const m
         // pre-activations of every later window were recomputed in the
         // previous window's weight-gradient launch
         MOE_TRY(routed_dgrad(*shape, L, ws, dY, weights, win, s));
-        MOE_TRY(routed_dx(*shape, L, ws, weights, win, s));
-        MOE_TRY(launch_window_accum(at<uint16_t>(ws, L.dXperm), win.w0, win.w1, nullptr,
-                                    plan->route_pos, T, d, k, acc, m == 0,
-                                    shared ? at<uint16_t>(ws, L.dXsh) : nullptr, nullptr, s));
+        if (fold) {
+            // the folded dX product of the window's experts; the first also
+            // takes the shared expert's segments, the last the router term
+            // (every dg is known once the last window's dgrad has run)
+            if (m == nwin - 1) {
+                MOE_TRY(launch_softmax_bwd(at<float>(ws, L.dgpart), L.dg_parts, plan->route_pos, topk_w,
+                                           topk_idx, T, k, E, at<float>(ws, L.dg), dZ, s));
+                MOE_TRY(launch_router_split(dZ, W_r, T, d, E, at<uint16_t>(ws, L.dzs),
+                                            at<uint16_t>(ws, L.wrs), s));
+            }
+            GemmArgs gx = dx_cmb_args(*shape, L, ws, weights, plan->offsets, dX);
+            gx.A = win.rows<uint16_t>(ws, L.dA, (int)shape->f);
+            gx.A2 = win.rows<uint16_t>(ws, L.dB, (int)shape->f);
+            if (m != 0) gx.segK_s = 0;
+            if (m != nwin - 1) gx.Ar = nullptr;
+            fold_window(gx, *shape, win.w0, win.w1, nwin, m == 0, m == nwin - 1, acc, dX);
+            MOE_TRY(launch_gemm_bwd_dx_cmb(gx, s));
+        } else {
+            MOE_TRY(routed_dx(*shape, L, ws, weights, win, s));
+            MOE_TRY(launch_window_accum(at<uint16_t>(ws, L.dXperm), win.w0, win.w1, nullptr,
+                                        plan->route_pos, T, d, k, acc, m == 0,
+                                        shared ? at<uint16_t>(ws, L.dXsh) : nullptr, nullptr, s));
+        }
         GemmArgs wg[3];
         int modes[3] = {0, 0, 0};
         for (int i = 0; i < 3; ++i) {
@@ -1057,6 +1135,10 @@ moe_status moe_backward_ring(const moe_shape *shape, const moe_bf16 *dY, const m
         } else {
             MOE_TRY(launch_gemm_wgrad_batch(wg, 3, E, nullptr, 0, s, modes));
         }
+    }
+    if (fold) {
+        MOE_TRY(launch_dwr(X, dZ, T, d, E, at<float>(ws, L.dwr_part), grads->dW_r, s));
+        return MOE_OK;
     }
     MOE_TRY(launch_softmax_bwd(at<float>(ws, L.dgpart), L.dg_parts, plan->route_pos, topk_w, topk_idx,
                                T, k, E, at<float>(ws, L.dg), dZ, s));

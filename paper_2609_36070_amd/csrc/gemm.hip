@@ -440,7 +440,7 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
             const int ex = sg / CM_H, half = sg - ex * CM_H;
             // the tokens' rows in expert ex's region; an offset that a
             // malformed plan would push past the buffer is clamped into it
-            const int off = min(max(uniform(g.seg_offsets[ex]), 0), g.a_nrows - g.M);
+            const int off = min(max(uniform(g.seg_offsets[ex]), g.a_row0), g.a_nrows - g.M);
             c.ab = (half ? g.A2 : g.A) + (long)off * g.lda;
             c.bb = (half ? g.B2 : g.B) + (long)ex * g.b_estride;
             c.lda = (uint32_t)g.lda;
@@ -774,8 +774,21 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
             for (int t = 0; t < 32 / RPP; ++t) {
                 const int row = lane / LPR + RPP * t, c = 8 * (lane % LPR);
                 const int p = row0 + wm * WM + 32 * i + row;
-                const f32x8 v = read8(row, c);
-                if (p < row_end) st_nt(g.C + (long)p * g.ldc + n0 + wn * WN + c, pack_bf8(v));
+                f32x8 v = read8(row, c);
+                if (p >= row_end) continue;
+                const long o = (long)p * g.ldc + n0 + wn * WN + c;
+                if (Tr::CMB && g.Cf) {
+                    if (g.accumulate) {
+                        const f32x8 prev = ld_f32x8(g.Cf + o);
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) v[q] = prev[q] + v[q];
+                    }
+                    if (!g.C) {
+                        st_f32x8(g.Cf + o, v);
+                        continue;
+                    }
+                }
+                st_nt(g.C + o, pack_bf8(v));
             }
         }
     } else if constexpr (MODE == BWD_DGRAD) {

@@ -56,6 +56,13 @@ struct GemmArgs {
     // ends with one 64-wide step of the router term (Ar, Br rows of 64).
     const int *seg_offsets = nullptr;  // the plan's offsets [E+1]
     int nseg = 0, segK = 0, segK_s = 0;
+    // a segment's first row is clamped into [a_row0, a_nrows - M] (a window
+    // of the plan held in a ring: its first row)
+    int a_row0 = 0;
+    // With Cf set, the token tiles keep a running fp32 sum over the windows
+    // of a bounded-memory pass: Cf [M][ldc] holds the earlier windows' sum
+    // (added first when accumulate), and the result goes to C (bf16, the
+    // last window) or back to Cf.
     const uint16_t *As = nullptr, *As2 = nullptr, *Bs = nullptr, *Bs2 = nullptr;
     long lda_s = 0, ldb_s = 0;
     const uint16_t *Ar = nullptr, *Br = nullptr;

@@ -93,6 +93,12 @@ def test_ring_parity(ring_rows):
     (Workload("many_tiles", T=700, d=768, E=3, k=2, f=768, backward=True), 600),
     (Workload("sixteen_experts", T=333, d=768, E=16, k=5, f=256, f_s=256, bias_std=0.5,
               backward=True), 500),
+    # dense routing with windows of whole experts: the folded down and dX
+    # products run per window on a running fp32 sum (2 and 4 windows)
+    (Workload("dense_two_windows", T=520, d=512, E=4, k=4, f=512, f_s=256, bias_std=0.5,
+              backward=True), 1040),
+    (Workload("dense_four_windows", T=300, d=256, E=4, k=4, f=256, f_s=256, bias_std=0.5,
+              backward=True), 300),
 ], ids=lambda v: v.name if isinstance(v, Workload) else str(v))
 def test_ring_edge_shapes(w, ring_rows):
     full, ring, inp = run_pair(w, ring_rows, seed=12)
