@@ -21,7 +21,7 @@ size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 // scratch, W_r^T, position tables, zero page) is the same in every layout,
 // so moe_route and moe_plan work with any of them.
 struct Layout {
-    size_t err, blockcounts, blockbase, blockflags, wrt, rowidx, wperm, zeros, fused;
+    size_t err, blockcounts, blockbase, blockflags, wrt, rpart, rowidx, wperm, zeros, fused;
     size_t prefix_total;
     size_t acc, coff;          // ring only: fp32 per-token accumulator, window regions
     size_t A, B, H, Yexp, As, Bs, Hs, Ysh;
@@ -62,6 +62,7 @@ Layout make_layout(const moe_shape &s, long ring_rows = -1) {
     L.blockbase = take(nb * E * 4);
     L.blockflags = take(nb * 4);
     L.wrt = take(epad * d * 2);
+    L.rpart = take(route_part_bytes((long)T, (int)d, (int)E));
     L.rowidx = take(R * 4);
     L.wperm = take(R * 4);
     L.zeros = take(ZERO_PAGE_ELEMS * 2);
@@ -730,6 +731,7 @@ moe_status moe_route(const moe_shape *shape, const moe_bf16 *X, const moe_bf16 *
     const Layout L = make_layout(*shape);
     hipStream_t s = static_cast<hipStream_t>(stream);
     MOE_TRY(launch_route(X, W_r, bias, logits, topk_idx, topk_w, at<uint16_t>(ws, L.wrt),
+                         at<float>(ws, L.rpart),
                          (int)shape->T, (int)shape->d, (int)shape->E, (int)shape->k, s));
     return MOE_OK;
 }

@@ -132,9 +132,12 @@ hipError_t launch_gemm_wgrad_batch(const GemmArgs *wg, int nw, int groups, const
                                    long up_rows, hipStream_t st, const int *modes = nullptr);
 
 int route_epad(int E);
+// Scratch of the split router (many experts): fp32 partial logits of its d
+// slices; 0 for shapes on the one-pass router.
+size_t route_part_bytes(long T, int d, int E);
 hipError_t launch_route(const uint16_t *X, const uint16_t *W_r, const float *bias, float *logits,
-                        int *topk_idx, float *topk_w, uint16_t *WrT, int T, int d, int E, int k,
-                        hipStream_t st);
+                        int *topk_idx, float *topk_w, uint16_t *WrT, float *part, int T,
+                        int d, int E, int k, hipStream_t st);
 
 int plan_nblocks(long R);
 hipError_t launch_plan(const int *topk_idx, int R, int E, int *counts, int *offsets, int *perm,
