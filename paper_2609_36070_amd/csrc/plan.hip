@@ -26,9 +26,19 @@ __global__ __launch_bounds__(64) void plan_hist_kernel(const int *__restrict__ i
     __syncthreads();
     const int j0 = b * PLAN_CHUNK;
     const int j1 = min(R, j0 + PLAN_CHUNK);
+    // all of the lane's ids first (their loads overlap), then the counts
+    constexpr int PER = PLAN_CHUNK / 64;
+    int ev[PER];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        const int j = j0 + l + 64 * q;
+        ev[q] = j < j1 ? idx[j] : 0;
+    }
     int bad = 0;
-    for (int j = j0 + l; j < j1; j += 64) {
-        const int e = idx[j];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        if (j0 + l + 64 * q >= j1) break;
+        const int e = ev[q];
         if (e >= 0 && e < E) atomicAdd(&cnt[e], 1);
         else bad = 1;
     }
@@ -56,16 +66,46 @@ __global__ __launch_bounds__(1024) void plan_scan_kernel(int nb, int E,
                                                          int *__restrict__ err) {
     __shared__ int tot[MAXE];
     const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
-    for (int e = w; e < E; e += 16) {
-        int run = 0;
-        for (int base = 0; base < nb; base += 64) {
-            const int b = base + l;
-            const int v = b < nb ? blockcounts[(long)b * E + e] : 0;
-            const int x = wave_incl_scan(v, l);
-            if (b < nb) blockbase[(long)b * E + e] = run + x - v;
-            run += __shfl(x, 63, 64);
+    if (nb <= 256) {
+        // up to 256 chunks: lane l holds chunks l + 64 m of each of the
+        // wave's experts (e = w + 16 q), all loaded before any scan
+        constexpr int QN = MAXE / 16;
+        int v[QN][4];
+        const int nm = (nb + 63) / 64;   // 64-chunk groups in use
+#pragma unroll
+        for (int q = 0; q < QN; ++q)
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const int e = w + 16 * q, b = l + 64 * m;
+                v[q][m] = (e < E && m < nm && b < nb) ? blockcounts[(long)b * E + e] : 0;
+            }
+#pragma unroll
+        for (int q = 0; q < QN; ++q) {
+            const int e = w + 16 * q;
+            if (e >= E) break;
+            int run = 0;
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                if (m >= nm) break;
+                const int b = l + 64 * m;
+                const int x = wave_incl_scan(v[q][m], l);
+                if (b < nb) blockbase[(long)b * E + e] = run + x - v[q][m];
+                run += __shfl(x, 63, 64);
+            }
+            if (l == 0) tot[e] = run;
         }
-        if (l == 0) tot[e] = run;
+    } else {
+        for (int e = w; e < E; e += 16) {
+            int run = 0;
+            for (int base = 0; base < nb; base += 64) {
+                const int b = base + l;
+                const int v = b < nb ? blockcounts[(long)b * E + e] : 0;
+                const int x = wave_incl_scan(v, l);
+                if (b < nb) blockbase[(long)b * E + e] = run + x - v;
+                run += __shfl(x, 63, 64);
+            }
+            if (l == 0) tot[e] = run;
+        }
     }
     __syncthreads();
     if (w == 0) {
@@ -102,10 +142,21 @@ __global__ __launch_bounds__(64) void plan_scatter_kernel(const int *__restrict_
     const int j0 = b * PLAN_CHUNK;
     const int j1 = min(R, j0 + PLAN_CHUNK);
     const unsigned long long lt = (l == 0) ? 0ull : (~0ull >> (64 - l));
-    for (int base = j0; base < j1; base += 64) {
+    // all of the lane's ids first (their loads overlap), then the ranks
+    constexpr int PER = PLAN_CHUNK / 64;
+    int ev[PER];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        const int j = j0 + l + 64 * q;
+        ev[q] = j < j1 ? idx[j] : -1;
+    }
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        const int base = j0 + 64 * q;
+        if (base >= j1) break;
         const int j = base + l;
         const bool valid = j < j1;
-        const int e = valid ? idx[j] : -1;
+        const int e = valid ? ev[q] : -1;
         const bool ok = valid && e >= 0 && e < E;
         unsigned long long m = __ballot(ok);
         for (int bit = 0; bit < ebits; ++bit) {
