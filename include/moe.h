@@ -203,7 +203,9 @@ moe_status moe_workspace_region(const moe_shape *shape, int with_backward,
  *   topk_idx [T, k] int32 out: the k largest logits, ties to the lower
  *            expert id, listed in ascending expert id.
  *   topk_w  [T, k] fp32 out: exp(Z_te) / sum_{e' in S_t} exp(Z_te').
- * Uses the workspace for a transposed copy of W_r. */
+ * Uses the workspace for a transposed copy of W_r and, with 128 or more
+ * experts, for fp32 partial logits of slices of the d axis (added in slice
+ * order, so the logits are deterministic). */
 moe_status moe_route(const moe_shape *shape, const moe_bf16 *X, const moe_bf16 *W_r,
                      const float *bias, float *logits, int32_t *topk_idx, float *topk_w,
                      void *ws, size_t ws_bytes, moe_stream stream);
