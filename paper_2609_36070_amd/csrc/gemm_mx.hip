@@ -275,31 +275,35 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
                                            : wn * WN + 32 * j + (lane & 31);
             wb[j] = sb[wd];
         }
+        // Fragments one step ahead of their MFMAs: the A fragment of row
+        // tile i + 1 (or of the next k step's row tile 0) is read before the
+        // MFMAs of row tile i, and each B fragment of the next k step right
+        // after its last MFMA of this one, into the same registers, so the
+        // LDS round trips overlap the matrix unit with no extra registers.
+        constexpr int KS = BK / 64;
+        i32x8_t bfr[TN];
 #pragma unroll
-        for (int ks = 0; ks < BK / 64; ++ks) {
+        for (int j = 0; j < TN; ++j) bfr[j] = frag(lb, wn * WN + 32 * j, 0, lane);
+        i32x8_t a_cur = frag(la, wm * WM, 0, lane);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
             // this lane's scales: block 2 ks + h of its row / column
             const int sh = 8 * (2 * ks + h);
-            i32x8_t bfr[TN];
 #pragma unroll
-            for (int j = 0; j < TN; ++j) bfr[j] = frag(lb, wn * WN + 32 * j, ks, lane);
-            // A fragments two at a time: more would not fit next to the
-            // accumulators
+            for (int i = 0; i < TM; ++i) {
+                i32x8_t a_nxt = a_cur;
+                if (i + 1 < TM) a_nxt = frag(la, wm * WM + 32 * (i + 1), ks, lane);
+                else if (ks + 1 < KS) a_nxt = frag(la, wm * WM, ks + 1, lane);
+                const int sai = (int)((wa[i] >> sh) & 0xffu);
 #pragma unroll
-            for (int i0 = 0; i0 < TM; i0 += 2) {
-                __builtin_amdgcn_sched_barrier(0);
-                i32x8_t af[2];
-#pragma unroll
-                for (int ii = 0; ii < 2; ++ii) af[ii] = frag(la, wm * WM + 32 * (i0 + ii), ks, lane);
-#pragma unroll
-                for (int ii = 0; ii < 2; ++ii) {
-                    const int sai = (int)((wa[i0 + ii] >> sh) & 0xffu);
-#pragma unroll
-                    for (int j = 0; j < TN; ++j) {
-                        const int sbj = (int)((wb[j] >> sh) & 0xffu);
-                        acc[i0 + ii][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                            af[ii], bfr[j], acc[i0 + ii][j], 0, 0, 0, sai, 0, sbj);
-                    }
+                for (int j = 0; j < TN; ++j) {
+                    const int sbj = (int)((wb[j] >> sh) & 0xffu);
+                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                        a_cur, bfr[j], acc[i][j], 0, 0, 0, sai, 0, sbj);
+                    if (i == TM - 1 && ks + 1 < KS) bfr[j] = frag(lb, wn * WN + 32 * j, ks + 1, lane);
                 }
+                a_cur = a_nxt;
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
     };
