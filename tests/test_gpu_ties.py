@@ -171,3 +171,35 @@ def test_split_router_slice_counts(T, d, E, k):
     Zo, _, _ = check_exact(X, W_r, bias, k)
     srt = -np.sort(-Zo, axis=1)
     assert int((srt[:, k - 1] == srt[:, k]).sum()) >= T // 2
+
+
+@pytest.mark.parametrize("T,d,E,k", [(8192, 2048, 128, 8), (3000, 1024, 256, 16)])
+def test_split_router_repeats_bitwise(T, d, E, k):
+    """Random fp32-valued logits through the router for 128 or more experts
+    (partial logits of several d slices added in a fixed order): three calls
+    give the same logits, ids and weights bit for bit."""
+    rng = np.random.default_rng(T + d)
+    X = rng.standard_normal((T, d), dtype=np.float32)
+    W_r = rng.standard_normal((d, E), dtype=np.float32) / np.float32(np.sqrt(d))
+    sh = B.make_shape(T, d, E, k, 256, 0)
+    dev = torch.device("cuda")
+    ws = torch.empty(B.moe_workspace_bytes(sh, False), dtype=torch.uint8, device=dev)
+    Xd = torch.from_numpy(X).to(torch.bfloat16).to(dev)
+    Wd = torch.from_numpy(W_r).to(torch.bfloat16).to(dev)
+    bias = torch.from_numpy(rng.standard_normal(E, dtype=np.float32) * np.float32(0.5)).to(dev)
+    say(f"[gpu] split router repeats T={T} d={d} E={E} k={k}")
+    runs = []
+    for _ in range(3):
+        logits = torch.empty((T, E), dtype=torch.float32, device=dev)
+        idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+        wts = torch.empty((T, k), dtype=torch.float32, device=dev)
+        ws.fill_(0x5A)   # stale partials from an earlier call must not matter
+        B.moe_route(sh, Xd, Wd, bias, logits, idx, wts, ws)
+        torch.cuda.synchronize()
+        runs.append((logits, idx, wts))
+    for r in runs[1:]:
+        for a, b in zip(runs[0], r):
+            assert torch.equal(a, b)
+    # and the selection is the oracle's on the GPU's own logits
+    Zg = to_np(runs[0][0])
+    assert np.array_equal(O.topk_select(Zg, k), to_np(runs[0][1]))
