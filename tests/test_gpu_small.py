@@ -88,6 +88,12 @@ def test_ragged_forward_backward():
     Workload("dense_shared", T=555, d=768, E=6, k=6, f=256, f_s=512, bias_std=0.5, backward=True),
     Workload("dense_one_expert", T=260, d=512, E=1, k=1, f=512, f_s=256, backward=True),
     Workload("dense_sixteen", T=130, d=256, E=16, k=16, f=256, backward=True),
+    # the router for 128 or more experts (d sliced across blocks, partial
+    # logits added in a reduce kernel) through a whole training step, with a
+    # padded expert count, empty experts and k = 16
+    Workload("experts_128_train", T=600, d=512, E=128, k=8, f=256, f_s=256, bias_std=0.5,
+             backward=True),
+    Workload("experts_200_train", T=257, d=768, E=200, k=16, f=256, bias_std=1.0, backward=True),
 ], ids=lambda w: w.name)
 def test_edge_shapes(w):
     L, inp, Zo, idx_g, w_orc = forward_parity(w, seed=2)
