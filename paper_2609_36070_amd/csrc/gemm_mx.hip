@@ -30,7 +30,7 @@
 //
 // Pipeline as in the BF16 kernels: 256 x 256 block tile, K step 128 bytes,
 // two LDS stages filled by direct global->LDS loads (128-byte rows, chunk
-// XOR (row >> 1) & 7), 4 waves of 128 x 128 (accumulators in AGPRs), tiles
+// XOR (row >> 1) & 7), 8 waves of 128 x 64 (two per SIMD), tiles
 // rastered XCD-aware.  The scale words of a K step (4 blocks of a row) go
 // to LDS by the same direct loads, one stage ahead, together with the tiles.
 #include "common.h"
@@ -43,11 +43,12 @@ namespace {
 
 constexpr int BM = 256, BN = 256, BK = 128;
 #ifndef MOE_MX_WAVES_N
-#define MOE_MX_WAVES_N 2
+#define MOE_MX_WAVES_N 4
 #endif
-// 2 x 2 waves of 128 x 128 (one wave per SIMD, accumulators in AGPRs) by
-// default: at 2 waves per SIMD the 128 accumulators of a 128 x 64 wave tile
-// leave too few registers for the fp8 fragments, scale words and addresses.
+// 2 x 4 waves of 128 x 64 (two waves per SIMD, so one can issue matrix
+// instructions while the other waits on its loads or the barrier); 2 x 2
+// waves of 128 x 128 (one per SIMD, accumulators in AGPRs) with
+// MOE_MX_WAVES_N=2.
 constexpr int WAVES_M = 2, WAVES_N = MOE_MX_WAVES_N, NWAVES = WAVES_M * WAVES_N;
 constexpr int NTHREADS = 64 * NWAVES;
 constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N, TM = WM / 32, TN = WN / 32;
@@ -90,13 +91,16 @@ DEV i32x8_t frag(const uint8_t *t, int r0, int ks, int lane) {
 
 template <int MODE>
 __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, const int *__restrict__ a_rows) {
-    __shared__ __attribute__((aligned(16))) uint8_t lds_a0[TILE];
-    __shared__ __attribute__((aligned(16))) uint8_t lds_b0[TILE];
-    __shared__ __attribute__((aligned(16))) uint8_t lds_a1[TILE];
-    __shared__ __attribute__((aligned(16))) uint8_t lds_b1[TILE];
+    // one LDS object for both stages of both operands: the K loop picks the
+    // stage by a wave-uniform offset at run time (see there)
+    __shared__ __attribute__((aligned(16))) uint8_t lds_all[4 * TILE];
+    uint8_t *const lds_a0 = lds_all, *const lds_a1 = lds_all + TILE;
+    uint8_t *const lds_b0 = lds_all + 2 * TILE, *const lds_b1 = lds_all + 3 * TILE;
     // scale words of the K step per stage: A tile rows; B tile columns (MX_UP:
     // 128 gate then 128 up columns of the tile's f range)
-    __shared__ uint32_t sc_a0[BM], sc_b0[BN], sc_a1[BM], sc_b1[BN];
+    __shared__ uint32_t sc_all[2 * BM + 2 * BN];
+    uint32_t *const sc_a0 = sc_all, *const sc_a1 = sc_all + BM;
+    uint32_t *const sc_b0 = sc_all + 2 * BM, *const sc_b1 = sc_all + 2 * BM + BN;
     __shared__ int s_info[2];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -303,30 +307,32 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
                     if (i == TM - 1 && ks + 1 < KS) bfr[j] = frag(lb, wn * WN + 32 * j, ks + 1, lane);
                 }
                 a_cur = a_nxt;
+                asm volatile("" ::: "memory");
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
     };
 
-    // double-buffered K loop (stages named per half, as in the BF16 kernels)
+    // Double-buffered K loop with the stage as a wave-uniform run-time
+    // offset.  With both stages named in an unrolled pair of steps the
+    // compiler keeps a lane address register per stage for every fragment
+    // read, which at two waves per SIMD (256 registers, 128 of them
+    // accumulators) spills inside the loop; with the offset added at each
+    // read it needs 195-238 registers and none spill.
     if (nk > 0) issue(0, lds_a0, lds_b0, sc_a0, sc_b0);
-    int kt = 0;
-    for (; kt + 1 < nk; kt += 2) {
+    int cur = 0;
+#pragma clang loop unroll(disable)
+    for (int kt = 0; kt < nk; ++kt) {
         wait_vmcnt<0>();
         barrier_no_fence();
-        issue(kt + 1, lds_a1, lds_b1, sc_a1, sc_b1);
-        asm volatile("" ::: "memory");
-        compute(lds_a0, lds_b0, sc_a0, sc_b0);
-        wait_vmcnt<0>();
-        barrier_no_fence();
-        if (kt + 2 < nk) issue(kt + 2, lds_a0, lds_b0, sc_a0, sc_b0);
-        asm volatile("" ::: "memory");
-        compute(lds_a1, lds_b1, sc_a1, sc_b1);
-    }
-    if (kt < nk) {
-        wait_vmcnt<0>();
-        barrier_no_fence();
-        compute(lds_a0, lds_b0, sc_a0, sc_b0);
+        const int nxt = uniform(cur ^ 1);
+        if (kt + 1 < nk)
+            issue(kt + 1, lds_all + nxt * TILE, lds_all + (2 + nxt) * TILE, sc_all + nxt * BM,
+                  sc_all + 2 * BM + nxt * BN);
+        asm volatile("" ::: "memory");   // keep the loads ahead of this step's LDS reads
+        compute(lds_all + cur * TILE, lds_all + (2 + cur) * TILE, sc_all + cur * BM,
+                sc_all + 2 * BM + cur * BN);
+        cur = nxt;
     }
     __syncthreads();
 
