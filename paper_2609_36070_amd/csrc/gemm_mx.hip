@@ -208,40 +208,46 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
 
     const int nk_half = g.K / BK;
     const int nk = (MODE == MX_DX) ? 2 * nk_half : (MODE == MX_WGRAD) ? nk_w : nk_half;
-    auto issue = [&](int kt_all, uint8_t *la, uint8_t *lb, uint32_t *sa, uint32_t *sb) {
+    // parts: 1 = the A tile and the scale words, 2 = the B tile
+    auto issue = [&](int kt_all, uint8_t *la, uint8_t *lb, uint32_t *sa, uint32_t *sb, int parts) {
         // MX_DX: the second half of the K loop reads dBq against the W_up rows
         const bool second = (MODE == MX_DX) && kt_all >= nk_half;
         const int kt = second ? kt_all - nk_half : kt_all;
         const uint32_t kb = kbase + (uint32_t)kt * BK;
+        if (parts & 1) {
 #pragma unroll
-        for (int i = 0; i < LD_PER_OP; ++i) {
-            const int q = LD_PER_OP * wave + i;
-            if constexpr (GATHER) {
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (LDSP void *)(la + q * 1024), 16, a_off[i],
-                                                         kb, 0, 0);
-            } else {
-                // rows past the region (or the operand) hold results that are never stored
-                const uint32_t arow = (uint32_t)(row0 + 8 * q);
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(second ? g.A2 : g.A, g.a_bytes),
-                                                         (LDSP void *)(la + q * 1024), 16,
-                                                         (q & 1) ? b_lane_odd : b_lane_even,
-                                                         arow * K + kb, 0, 0);
+            for (int i = 0; i < LD_PER_OP; ++i) {
+                const int q = LD_PER_OP * wave + i;
+                if constexpr (GATHER) {
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (LDSP void *)(la + q * 1024), 16, a_off[i],
+                                                             kb, 0, 0);
+                } else {
+                    // rows past the region (or the operand) hold results that are never stored
+                    const uint32_t arow = (uint32_t)(row0 + 8 * q);
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(second ? g.A2 : g.A, g.a_bytes),
+                                                             (LDSP void *)(la + q * 1024), 16,
+                                                             (q & 1) ? b_lane_odd : b_lane_even,
+                                                             arow * K + kb, 0, 0);
+                }
             }
         }
+        if (parts & 2) {
 #pragma unroll
-        for (int i = 0; i < LD_PER_OP; ++i) {
-            const int q = LD_PER_OP * wave + i;
-            // B row of instruction q less the lane part l8 (uniform); MX_UP: tile
-            // rows 8 q .. 8 q + 7 lie in column group q / 4, gate or up
-            const bool up = ((MODE == MX_UP) && ((q >> 2) & 1)) || second;
-            const uint32_t brow = (MODE == MX_UP)
-                ? (uint32_t)(e * g.N + n0 + (q >> 3) * 32 + 8 * (q & 3))
-                : (uint32_t)((MODE == MX_WGRAD ? 0 : e * g.N) + n0 + 8 * q);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(up ? g.B2 : g.B, g.b_bytes),
-                                                     (LDSP void *)(lb + q * 1024), 16,
-                                                     (q & 1) ? b_lane_odd : b_lane_even,
-                                                     brow * K + kb, 0, 0);
+            for (int i = 0; i < LD_PER_OP; ++i) {
+                const int q = LD_PER_OP * wave + i;
+                // B row of instruction q less the lane part l8 (uniform); MX_UP: tile
+                // rows 8 q .. 8 q + 7 lie in column group q / 4, gate or up
+                const bool up = ((MODE == MX_UP) && ((q >> 2) & 1)) || second;
+                const uint32_t brow = (MODE == MX_UP)
+                    ? (uint32_t)(e * g.N + n0 + (q >> 3) * 32 + 8 * (q & 3))
+                    : (uint32_t)((MODE == MX_WGRAD ? 0 : e * g.N) + n0 + 8 * q);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(up ? g.B2 : g.B, g.b_bytes),
+                                                         (LDSP void *)(lb + q * 1024), 16,
+                                                         (q & 1) ? b_lane_odd : b_lane_even,
+                                                         brow * K + kb, 0, 0);
+            }
         }
+        if (!(parts & 1)) return;
 #pragma unroll
         for (int i = 0; i < SC_PER_WAVE; ++i) {
             const int c = SC_PER_WAVE * wave + i;
@@ -267,49 +273,51 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
             for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
     const int h = lane >> 5;
-    auto compute = [&](const uint8_t *la, const uint8_t *lb, const uint32_t *sa, const uint32_t *sb) {
-        uint32_t wa[TM], wb[TN];
+    // Fragments one step ahead of their MFMAs: the A fragment of row tile
+    // i + 1 (or of the next k sub-step's row tile 0) is read before the MFMAs
+    // of row tile i, and each B fragment of the next k sub-step right after
+    // its last MFMA of this one, into the same registers, so the LDS round
+    // trips overlap the matrix unit with no extra registers.  The fragments
+    // and scale words live here, across the two sub-step calls of a K step.
+    constexpr int KS = BK / 64;
+    static_assert(KS == 2, "two 64-wide k sub-steps per K step");
+    uint32_t wa[TM], wb[TN];
+    i32x8_t bfr[TN], a_cur;
+    auto compute_ks = [&](const uint8_t *la, const uint8_t *lb, const uint32_t *sa, const uint32_t *sb,
+                          int ks) {
+        if (ks == 0) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i) wa[i] = sa[wm * WM + 32 * i + (lane & 31)];
+            for (int i = 0; i < TM; ++i) wa[i] = sa[wm * WM + 32 * i + (lane & 31)];
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            // scale word of tile column wn WN + 32 j + lane % 32 (MX_UP: gate words
-            // 0..127, up words 128..255 of the tile's f range)
-            const int wd = (MODE == MX_UP) ? (j & 1) * 128 + (wn * WN / 64 + j / 2) * 32 + (lane & 31)
-                                           : wn * WN + 32 * j + (lane & 31);
-            wb[j] = sb[wd];
-        }
-        // Fragments one step ahead of their MFMAs: the A fragment of row
-        // tile i + 1 (or of the next k step's row tile 0) is read before the
-        // MFMAs of row tile i, and each B fragment of the next k step right
-        // after its last MFMA of this one, into the same registers, so the
-        // LDS round trips overlap the matrix unit with no extra registers.
-        constexpr int KS = BK / 64;
-        i32x8_t bfr[TN];
-#pragma unroll
-        for (int j = 0; j < TN; ++j) bfr[j] = frag(lb, wn * WN + 32 * j, 0, lane);
-        i32x8_t a_cur = frag(la, wm * WM, 0, lane);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            // this lane's scales: block 2 ks + h of its row / column
-            const int sh = 8 * (2 * ks + h);
-#pragma unroll
-            for (int i = 0; i < TM; ++i) {
-                i32x8_t a_nxt = a_cur;
-                if (i + 1 < TM) a_nxt = frag(la, wm * WM + 32 * (i + 1), ks, lane);
-                else if (ks + 1 < KS) a_nxt = frag(la, wm * WM, ks + 1, lane);
-                const int sai = (int)((wa[i] >> sh) & 0xffu);
-#pragma unroll
-                for (int j = 0; j < TN; ++j) {
-                    const int sbj = (int)((wb[j] >> sh) & 0xffu);
-                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                        a_cur, bfr[j], acc[i][j], 0, 0, 0, sai, 0, sbj);
-                    if (i == TM - 1 && ks + 1 < KS) bfr[j] = frag(lb, wn * WN + 32 * j, ks + 1, lane);
-                }
-                a_cur = a_nxt;
-                asm volatile("" ::: "memory");
-                __builtin_amdgcn_sched_barrier(0);
+            for (int j = 0; j < TN; ++j) {
+                // scale word of tile column wn WN + 32 j + lane % 32 (MX_UP: gate
+                // words 0..127, up words 128..255 of the tile's f range)
+                const int wd = (MODE == MX_UP) ? (j & 1) * 128 + (wn * WN / 64 + j / 2) * 32 + (lane & 31)
+                                               : wn * WN + 32 * j + (lane & 31);
+                wb[j] = sb[wd];
             }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) bfr[j] = frag(lb, wn * WN + 32 * j, 0, lane);
+            a_cur = frag(la, wm * WM, 0, lane);
+        }
+        // this lane's scales: block 2 ks + h of its row / column
+        const int sh = 8 * (2 * ks + h);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            i32x8_t a_nxt = a_cur;
+            if (i + 1 < TM) a_nxt = frag(la, wm * WM + 32 * (i + 1), ks, lane);
+            else if (ks + 1 < KS) a_nxt = frag(la, wm * WM, ks + 1, lane);
+            const int sai = (int)((wa[i] >> sh) & 0xffu);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int sbj = (int)((wb[j] >> sh) & 0xffu);
+                acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                    a_cur, bfr[j], acc[i][j], 0, 0, 0, sai, 0, sbj);
+                if (i == TM - 1 && ks + 1 < KS) bfr[j] = frag(lb, wn * WN + 32 * j, ks + 1, lane);
+            }
+            a_cur = a_nxt;
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_sched_barrier(0);
         }
     };
 
@@ -319,19 +327,33 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
     // read, which at two waves per SIMD (256 registers, 128 of them
     // accumulators) spills inside the loop; with the offset added at each
     // read it needs 195-238 registers and none spill.
-    if (nk > 0) issue(0, lds_a0, lds_b0, sc_a0, sc_b0);
+    //
+    // The next step's B tile goes out before the MFMAs of sub-step 0 and its
+    // A tile and scale words before those of sub-step 1 (the row products:
+    // down 2.20 -> 2.12 ms, training step -0.9 %; A first was slower).  The
+    // weight gradients keep all their loads at the step's start (split, they
+    // were 0.5 % slower).
+    constexpr int FIRST = (MODE == MX_WGRAD) ? 3 : 2;
+    if (nk > 0) issue(0, lds_a0, lds_b0, sc_a0, sc_b0, 3);
     int cur = 0;
 #pragma clang loop unroll(disable)
     for (int kt = 0; kt < nk; ++kt) {
         wait_vmcnt<0>();
         barrier_no_fence();
         const int nxt = uniform(cur ^ 1);
-        if (kt + 1 < nk)
-            issue(kt + 1, lds_all + nxt * TILE, lds_all + (2 + nxt) * TILE, sc_all + nxt * BM,
-                  sc_all + 2 * BM + nxt * BN);
+        uint8_t *nla = lds_all + nxt * TILE, *nlb = lds_all + (2 + nxt) * TILE;
+        uint32_t *nsa = sc_all + nxt * BM, *nsb = sc_all + 2 * BM + nxt * BN;
+        const uint8_t *la = lds_all + cur * TILE, *lb = lds_all + (2 + cur) * TILE;
+        const uint32_t *sa = sc_all + cur * BM, *sb = sc_all + 2 * BM + cur * BN;
+        if (kt + 1 < nk) issue(kt + 1, nla, nlb, nsa, nsb, FIRST);
         asm volatile("" ::: "memory");   // keep the loads ahead of this step's LDS reads
-        compute(lds_all + cur * TILE, lds_all + (2 + cur) * TILE, sc_all + cur * BM,
-                sc_all + 2 * BM + cur * BN);
+        compute_ks(la, lb, sa, sb, 0);
+        if (FIRST != 3 && kt + 1 < nk) {
+            asm volatile("" ::: "memory");
+            issue(kt + 1, nla, nlb, nsa, nsb, 3 ^ FIRST);
+            asm volatile("" ::: "memory");
+        }
+        compute_ks(la, lb, sa, sb, 1);
         cur = nxt;
     }
     __syncthreads();
