@@ -3,7 +3,9 @@
 // expert e's region is the number of earlier routes to e, so the plan is a
 // stable counting sort of the routes by expert:
 //
-//   1. plan_hist:    per-chunk expert histograms (LDS integer counters);
+//   1. plan_hist:    per-chunk expert histograms (LDS integer counters),
+//                    stored expert-major ([E][chunks]) so that the scan's
+//                    lanes, one chunk each, read and write consecutive words;
 //   2. plan_scan:    exclusive scans over chunks (per expert) and experts;
 //   3. plan_scatter: each chunk walks its routes in order in 64-lane groups;
 //                    lanes with equal expert ids are matched with ballots, so
@@ -43,7 +45,7 @@ __global__ __launch_bounds__(64) void plan_hist_kernel(const int *__restrict__ i
         else bad = 1;
     }
     __syncthreads();
-    for (int e = l; e < E; e += 64) blockcounts[(long)b * E + e] = cnt[e];
+    for (int e = l; e < E; e += 64) blockcounts[(long)e * gridDim.x + b] = cnt[e];
     const unsigned long long anybad = __ballot(bad);
     if (l == 0) blockflags[b] = anybad != 0ull;
 }
@@ -77,7 +79,7 @@ __global__ __launch_bounds__(1024) void plan_scan_kernel(int nb, int E,
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
                 const int e = w + 16 * q, b = l + 64 * m;
-                v[q][m] = (e < E && m < nm && b < nb) ? blockcounts[(long)b * E + e] : 0;
+                v[q][m] = (e < E && m < nm && b < nb) ? blockcounts[(long)e * nb + b] : 0;
             }
 #pragma unroll
         for (int q = 0; q < QN; ++q) {
@@ -89,7 +91,7 @@ __global__ __launch_bounds__(1024) void plan_scan_kernel(int nb, int E,
                 if (m >= nm) break;
                 const int b = l + 64 * m;
                 const int x = wave_incl_scan(v[q][m], l);
-                if (b < nb) blockbase[(long)b * E + e] = run + x - v[q][m];
+                if (b < nb) blockbase[(long)e * nb + b] = run + x - v[q][m];
                 run += __shfl(x, 63, 64);
             }
             if (l == 0) tot[e] = run;
@@ -99,9 +101,9 @@ __global__ __launch_bounds__(1024) void plan_scan_kernel(int nb, int E,
             int run = 0;
             for (int base = 0; base < nb; base += 64) {
                 const int b = base + l;
-                const int v = b < nb ? blockcounts[(long)b * E + e] : 0;
+                const int v = b < nb ? blockcounts[(long)e * nb + b] : 0;
                 const int x = wave_incl_scan(v, l);
-                if (b < nb) blockbase[(long)b * E + e] = run + x - v;
+                if (b < nb) blockbase[(long)e * nb + b] = run + x - v;
                 run += __shfl(x, 63, 64);
             }
             if (l == 0) tot[e] = run;
@@ -137,7 +139,7 @@ __global__ __launch_bounds__(64) void plan_scatter_kernel(const int *__restrict_
                                                           int *__restrict__ route_pos) {
     __shared__ int run[MAXE];
     const int b = blockIdx.x, l = threadIdx.x;
-    for (int e = l; e < E; e += 64) run[e] = offsets[e] + blockbase[(long)b * E + e];
+    for (int e = l; e < E; e += 64) run[e] = offsets[e] + blockbase[(long)e * gridDim.x + b];
     __syncthreads();
     const int j0 = b * PLAN_CHUNK;
     const int j1 = min(R, j0 + PLAN_CHUNK);
