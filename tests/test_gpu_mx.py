@@ -121,6 +121,10 @@ def test_mx_ragged():
     Workload("mx_k_equals_E", T=300, d=256, E=4, k=4, f=512, bias_std=0.5),
     Workload("mx_empty_experts", T=40, d=256, E=64, k=1, f=256, bias_std=3.0),
     Workload("mx_many_tiles", T=700, d=768, E=3, k=2, f=768),
+    # more than 64 experts: the GEMMs' expert lookup runs over several
+    # 64-expert groups (and the router is the split one)
+    Workload("mx_128_experts", T=600, d=512, E=128, k=8, f=256, f_s=256, bias_std=0.5),
+    Workload("mx_200_experts", T=257, d=768, E=200, k=16, f=256, bias_std=1.0),
 ], ids=lambda w: w.name)
 def test_mx_edge_shapes(w):
     mx_parity(w, seed=3)

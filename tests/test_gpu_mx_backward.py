@@ -203,6 +203,22 @@ def test_mx_backward_edge_shapes(w):
     mx_backward_parity(w, seed=32)
 
 
+MANY = [
+    Workload("mx_128_experts_train", T=600, d=512, E=128, k=8, f=256, f_s=256, bias_std=0.5,
+             backward=True),
+    Workload("mx_200_experts_train", T=257, d=768, E=200, k=16, f=256, bias_std=1.0, backward=True),
+]
+
+
+@pytest.mark.parametrize("wgrad", [False, True], ids=["bf16_wgrad", "mxfp8_wgrad"])
+@pytest.mark.parametrize("w", MANY, ids=lambda w: w.name)
+def test_mx_backward_many_experts(w, wgrad):
+    """More than 64 experts (several 64-expert groups in every GEMM's expert
+    lookup and in the weight gradients' tile map), many of them with a few
+    rows, with both weight-gradient variants."""
+    mx_backward_parity(w, seed=33, wgrad=wgrad)
+
+
 @pytest.mark.parametrize("w", EDGE + [
     Workload("mx_wgrad_block_edges", T=160, d=512, E=5, k=3, f=256, f_s=256, bias_std=1.0,
              backward=True),
