@@ -26,7 +26,16 @@ DEV uint32_t pack_bf2(float lo, float hi) {
     return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
 }
 
-DEV float silu_f(float a) { return a / (1.0f + expf(-a)); }
+// The gated activation's logistic function from the hardware base-2
+// exponential and reciprocal (v_exp_f32, v_rcp_f32, each within about 1 ulp,
+// plus the rounding of -a log2(e)): a handful of instructions where expf and
+// an IEEE division take about twenty, which matters in the SwiGLU epilogues,
+// whose per-element arithmetic is a large part of their time.  Limits:
+// a -> +inf gives 1, a -> -inf gives 0, NaN stays NaN.
+DEV float sigmoid_f(float a) {
+    return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-a * 1.4426950408889634f));
+}
+DEV float silu_f(float a) { return a * sigmoid_f(a); }
 
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 

@@ -832,7 +832,7 @@ DEV void gemm_tile(const GemmArgs &g, const int *__restrict__ a_rows, const int 
                     for (int k = 0; k < 8; ++k) {
                         const float a = (k & 1) ? bf_hi(ap[k >> 1]) : bf_lo(ap[k >> 1]);
                         const float b = (k & 1) ? bf_hi(bp[k >> 1]) : bf_lo(bp[k >> 1]);
-                        const float sg = 1.0f / (1.0f + expf(-a));
+                        const float sg = sigmoid_f(a);
                         const float sl = a * sg;
                         const float h = sl * b;
                         prod = prod + dhp[k] * h;

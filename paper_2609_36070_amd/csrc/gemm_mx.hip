@@ -474,7 +474,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
 #pragma unroll
                 for (int k = 0; k < 8; ++k) {
                     const float a = av[k], b = bv[k];
-                    const float sg = 1.0f / (1.0f + expf(-a));
+                    const float sg = sigmoid_f(a);
                     const float sl = a * sg;
                     const float h = sl * b;
                     prod = prod + dhp[k] * h;
