@@ -22,8 +22,12 @@ DEV uint16_t f2bf(float x) {
     __bf16 b = (__bf16)x;
     return __builtin_bit_cast(uint16_t, b);
 }
+// Two at once: one v_cvt_pk_bf16_f32 with both sources (the scalar
+// conversions above take one each, plus a shift and an OR to combine them).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 DEV uint32_t pack_bf2(float lo, float hi) {
-    return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 
 // The gated activation's logistic function from the hardware base-2
