@@ -133,6 +133,29 @@ def test_identical_experts_router_gradient_vanishes():
                                                                (w.T * w.k,)))).max()
 
 
+def test_saturated_gated_activation():
+    """Gate weights scaled by 64 (a power of two, so still bf16-exact): the
+    gate pre-activations reach a few hundred in magnitude, so the logistic
+    function saturates at 0 and 1 and its exponential overflows for the most
+    negative ones.  Forward and backward against the oracle, every element."""
+    w = Workload("saturated", T=300, d=256, E=4, k=2, f=256, f_s=256, bias_std=0.5, backward=True)
+    from paper_2609_36070_amd.workloads import make_inputs
+    inp = make_inputs(w, 7)
+    for key in ("W_gate", "Wg_s"):
+        inp[key] = inp[key] * np.float32(64.0)
+    L, _ = run_layer(w, inputs=inp)
+    Zo, idx_g = check_route_and_plan(L, inp, w)
+    w_orc = O.gate_weights(Zo, idx_g)
+    fw = O.moe_forward(inp["X"], weights_dict(inp), idx_g, w_orc)
+    amax = float(np.abs(fw["A"]).max())
+    say(f"  max |a| = {amax:.1f}")
+    assert amax > 100.0, "the fixture must reach the saturated range"
+    assert_close("Y", to_np(L.Y), fw["Y"])
+    R = w.T * w.k
+    assert_close("H", to_np(L.ws_tensor(B.WS_H, torch.bfloat16, (R, w.f))), fw["H"])
+    backward_parity(L, inp, w, idx_g, w_orc)
+
+
 def test_bad_expert_index_sets_error_word():
     w = Workload("bad_idx", T=64, d=256, E=8, k=2, f=256)
     from paper_2609_36070_amd.workloads import make_inputs
