@@ -131,7 +131,10 @@ typedef enum {
     /* MXFP8 weight gradients only (moe_backward_mx with wgrad_mxfp8 = 1).
      * Expert e's plan rows sit at padded positions [poff[e], poff[e] + count)
      * of a token axis of P = roundup(T*k + 128 E, 128) positions; poff[e] is
-     * a multiple of 128, and positions past an expert's rows hold zeros. */
+     * a multiple of 128, and positions past an expert's rows hold zeros.
+     * With dense routing (k = E) every expert's rows are tokens 0 .. T-1 in
+     * order, so X^T and dY^T are written for expert 0's range only, which
+     * every expert's weight-gradient product reads. */
     MOE_WS_POFF = 20,   /* int32 [E+1]    padded expert offsets             */
     MOE_WS_XTQ = 21,    /* E4M3 [d, P]    X^T by token, 32-blocks along P   */
     MOE_WS_XTS = 22,    /* E8M0 [d, P/32]                                   */

@@ -1376,9 +1376,15 @@ moe_status moe_backward_mx(const moe_shape *shape, const moe_bf16 *dY, const moe
         const long P = L.tpad;
         const int *rowidx = at<int>(ws, L.rowidx);
         MOE_TRY(launch_mx_pad_offsets(plan->offsets, E, poff, s));
-        MOE_TRY(launch_mx_quant_tokens(X, d, T, rowidx, plan->offsets, poff, E, d, P, P,
+        // With dense routing every expert's range holds tokens 0 .. T-1 in
+        // order, so the token-axis codes of X and dY are the same for every
+        // expert: quantise expert 0's range only and let the weight-gradient
+        // products read it from position 0 (bitwise the same operands).
+        const bool dense = dense_routing(*shape);
+        const int qE = dense ? 1 : E;
+        MOE_TRY(launch_mx_quant_tokens(X, d, T, rowidx, plan->offsets, poff, qE, d, P, P,
                                        at<uint8_t>(ws, L.xt), at<uint8_t>(ws, L.xts), s));
-        MOE_TRY(launch_mx_quant_tokens(dY, d, T, rowidx, plan->offsets, poff, E, d, P, P,
+        MOE_TRY(launch_mx_quant_tokens(dY, d, T, rowidx, plan->offsets, poff, qE, d, P, P,
                                        at<uint8_t>(ws, L.dyt), at<uint8_t>(ws, L.dyts), s));
         MOE_TRY(launch_mx_quant_tokens_f32(at<float>(ws, L.da32), f, R, plan->offsets, poff, E, f, P,
                                            P, at<uint8_t>(ws, L.dat), at<uint8_t>(ws, L.dats), s));
@@ -1386,8 +1392,10 @@ moe_status moe_backward_mx(const moe_shape *shape, const moe_bf16 *dY, const moe
                                            P, at<uint8_t>(ws, L.dbt), at<uint8_t>(ws, L.dbts), s));
         MOE_TRY(launch_mx_quant_tokens_f32(at<float>(ws, L.hw32), f, R, plan->offsets, poff, E, f, P,
                                            P, at<uint8_t>(ws, L.hwt), at<uint8_t>(ws, L.hwts), s));
-        auto wg = [&](size_t a, size_t as, int M, size_t b, size_t bs, int N, float *out) {
+        auto wg = [&](size_t a, size_t as, int M, size_t b, size_t bs, int N, float *out, int a_sh,
+                      int b_sh) {
             MxGemmArgs g;
+            g.a_shared = a_sh; g.b_shared = b_sh;
             g.A = at<uint8_t>(ws, a); g.As = at<uint8_t>(ws, as); g.a_nrows = M;
             g.B = at<uint8_t>(ws, b); g.Bs = at<uint8_t>(ws, bs);
             g.M = M; g.N = N; g.K = (int)P; g.offsets = poff; g.E = E; g.Cf = out;
@@ -1397,9 +1405,9 @@ moe_status moe_backward_mx(const moe_shape *shape, const moe_bf16 *dY, const moe
             g.bs_bytes = (uint32_t)((long)N * P / 32);
             return launch_gemm_mx_wgrad(g, E, s);
         };
-        MOE_TRY(wg(L.xt, L.xts, d, L.dat, L.dats, f, grads->dW_gate));
-        MOE_TRY(wg(L.xt, L.xts, d, L.dbt, L.dbts, f, grads->dW_up));
-        MOE_TRY(wg(L.hwt, L.hwts, f, L.dyt, L.dyts, d, grads->dW_down));
+        MOE_TRY(wg(L.xt, L.xts, d, L.dat, L.dats, f, grads->dW_gate, dense, 0));
+        MOE_TRY(wg(L.xt, L.xts, d, L.dbt, L.dbts, f, grads->dW_up, dense, 0));
+        MOE_TRY(wg(L.hwt, L.hwts, f, L.dyt, L.dyts, d, grads->dW_down, 0, dense));
     } else if (dense_routing(*shape)) {
         // weight gradients in BF16 on the unquantised operands, X and dY
         // read transposed (dense routing; see dense_transposes)

@@ -213,7 +213,10 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
         // MX_DX: the second half of the K loop reads dBq against the W_up rows
         const bool second = (MODE == MX_DX) && kt_all >= nk_half;
         const int kt = second ? kt_all - nk_half : kt_all;
+        // MX_WGRAD: an operand shared by all experts starts at position 0
         const uint32_t kb = kbase + (uint32_t)kt * BK;
+        const uint32_t kb_a = (MODE == MX_WGRAD && g.a_shared) ? (uint32_t)kt * BK : kb;
+        const uint32_t kb_b = (MODE == MX_WGRAD && g.b_shared) ? (uint32_t)kt * BK : kb;
         if (parts & 1) {
 #pragma unroll
             for (int i = 0; i < LD_PER_OP; ++i) {
@@ -227,7 +230,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
                     __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(second ? g.A2 : g.A, g.a_bytes),
                                                              (LDSP void *)(la + q * 1024), 16,
                                                              (q & 1) ? b_lane_odd : b_lane_even,
-                                                             arow * K + kb, 0, 0);
+                                                             arow * K + kb_a, 0, 0);
                 }
             }
         }
@@ -244,7 +247,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(up ? g.B2 : g.B, g.b_bytes),
                                                          (LDSP void *)(lb + q * 1024), 16,
                                                          (q & 1) ? b_lane_odd : b_lane_even,
-                                                         brow * K + kb, 0, 0);
+                                                         brow * K + kb_b, 0, 0);
             }
         }
         if (!(parts & 1)) return;
@@ -254,12 +257,12 @@ __global__ __launch_bounds__(NTHREADS, 1) void gemm_mx_kernel(MxGemmArgs g, cons
             if (c < 4) {
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(second ? g.As2 : g.As, g.as_bytes),
                                                          (LDSP void *)(sa + 64 * c), 4, sc_off[i],
-                                                         kbase / 32 + 4 * kt, 0, 0);
+                                                         (MODE == MX_WGRAD ? kb_a / 32 : kbase / 32 + 4 * kt), 0, 0);
             } else {
                 const bool up = ((MODE == MX_UP) && (c - 4 >= 2)) || second;
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(up ? g.Bs2 : g.Bs, g.bs_bytes),
                                                          (LDSP void *)(sb + 64 * (c - 4)), 4,
-                                                         sc_off[i], kbase / 32 + 4 * kt, 0, 0);
+                                                         sc_off[i], (MODE == MX_WGRAD ? kb_b / 32 : kbase / 32 + 4 * kt), 0, 0);
             }
         }
     };

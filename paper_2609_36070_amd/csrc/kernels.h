@@ -184,6 +184,10 @@ struct MxGemmArgs {
     // B [N][K] hold token-axis codes, K is their row pitch in bytes
     int M = 0;
     float *Cf = nullptr;               // MX_WGRAD: fp32 [E][M][N]
+    // MX_WGRAD with dense routing: every expert's token range holds the same
+    // tokens, so X^T (A of dW_gate, dW_up) or dY^T (B of dW_down) is quantised
+    // once, as expert 0's range, and read from position 0 for every expert
+    int a_shared = 0, b_shared = 0;
 };
 hipError_t launch_gemm_mx_up(const MxGemmArgs &g, long rows, int groups, hipStream_t st);
 hipError_t launch_gemm_mx_down(const MxGemmArgs &g, long rows, int groups, hipStream_t st);

@@ -59,6 +59,11 @@ def check_token_codes(L, inp, w, idx_g, experts, cols=None):
     from the expert's first row, zeros past its rows), bit-exact against the
     oracle's quantiser on the same values; cols: a sample of the d columns."""
     poff = padded_offsets(L, w)
+    if w.k == w.E:
+        # dense routing: every expert's rows are the same tokens in the same
+        # order, so the library quantises expert 0's range once and every
+        # expert's product reads it
+        experts = [0]
     _, nbytes = B.moe_mx_workspace_region(L.shape, B.WS_XTQ)
     P = nbytes // w.d
     assert P % 128 == 0 and P >= poff[-1]
